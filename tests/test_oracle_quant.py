@@ -1,0 +1,109 @@
+"""Pins of the oracle's quantisers: brute-force nearest code, error bounds, exact grids,
+int4 pack/unpack round trips."""
+import os
+
+import numpy as np
+
+from oracle.quant import (quant_int8_channel, dequant_int8_channel, quant_int4_g128,
+                          dequant_int4_g128, pack_int4, unpack_int4, quant_kv_int8)
+from oracle.numerics import bf16_round
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bf16_weights(rng, shape, sigma=0.02):
+    return bf16_round(rng.normal(0, sigma, shape).astype(np.float32))
+
+
+def test_int8_codes_are_brute_force_nearest():
+    rng = np.random.default_rng(0)
+    w = _bf16_weights(rng, (64, 256))
+    codes, s = quant_int8_channel(w)
+    cand = np.arange(-127, 128, dtype=np.float64)
+    for n in range(w.shape[0]):
+        err = np.abs(w[n].astype(np.float64)[:, None] - cand[None, :] * float(s[n]))
+        best = err.min(axis=1)
+        mine = np.abs(w[n].astype(np.float64) - codes[n].astype(np.float64) * float(s[n]))
+        assert np.array_equal(mine, best)
+    # the absmax element lands on +-127 and the scale is absmax/127 to fp16 precision
+    am = np.abs(w).max(axis=1)
+    assert np.all(np.abs(codes).max(axis=1) == 127)
+    assert np.all(np.abs(s.astype(np.float64) * 127 / am - 1) <= 2.0 ** -11)
+
+
+def test_int8_error_bound_and_grid():
+    rng = np.random.default_rng(1)
+    w = _bf16_weights(rng, (32, 512))
+    c, s = quant_int8_channel(w)
+    deq = dequant_int8_channel(c, s)
+    assert np.all(np.abs(w - deq) <= s[:, None] / 2)
+    # exact multiples k*s quantise to k
+    s0 = np.float32(0.0078125)
+    k = np.arange(-127, 128).astype(np.float32)
+    grid = (k * s0)[None, :]
+    cg, sg = quant_int8_channel(grid)
+    assert sg[0] == np.float32(127 * s0 / 127) and np.array_equal(cg[0], k.astype(np.int8))
+    # all-zero row
+    cz, sz = quant_int8_channel(np.zeros((1, 16), np.float32))
+    assert sz[0] == 0 and not cz.any()
+
+
+def test_int4_codes_are_brute_force_nearest_and_bounded():
+    rng = np.random.default_rng(2)
+    w = _bf16_weights(rng, (16, 512))
+    q, s, z = quant_int4_g128(w)
+    assert q.max() <= 15 and z.min() >= 0 and z.max() <= 15
+    deq = dequant_int4_g128(q, s, z)
+    sfull = np.repeat(s, 128, axis=1)
+    zfull = np.repeat(z, 128, axis=1)
+    err = np.abs(w.astype(np.float64) - deq.astype(np.float64))
+    assert np.all(err <= sfull / 2 + 15 * 2.0 ** -11 * sfull)
+    # brute force: no other code in 0..15 reconstructs strictly closer
+    cand = np.arange(16, dtype=np.float64)
+    allerr = np.abs(w.astype(np.float64)[..., None]
+                    - (cand[None, None, :] - zfull[..., None]) * sfull[..., None])
+    assert np.all(err <= allerr.min(axis=-1) + 1e-12 * sfull)
+    # the range of every group contains 0 and z reproduces 0 exactly
+    assert np.all((0 - z) * s == -(z * s))
+
+
+def test_int4_exact_grid_and_zero_group():
+    s0 = np.float32(0.00390625)
+    zt = 5
+    k = np.tile(np.arange(16, dtype=np.float32), 8)         # 128 values, codes 0..15
+    w = ((k - zt) * s0)[None, :]
+    q, s, z = quant_int4_g128(w)
+    assert s[0, 0] == s0 and z[0, 0] == zt and np.array_equal(q[0], k.astype(np.uint8))
+    assert np.array_equal(dequant_int4_g128(q, s, z), w)
+    q0, s1, z0 = quant_int4_g128(np.zeros((2, 128), np.float32))
+    assert np.all(s1 == 1.0) and np.all(z0 == 0) and not q0.any()
+    # an all-positive group: lo = 0 -> z = 0
+    q2, s2, z2 = quant_int4_g128(np.abs(_bf16_weights(np.random.default_rng(9), (1, 128))))
+    assert z2[0, 0] == 0 and q2.max() == 15
+
+
+def test_int4_pack_golden_and_round_trips():
+    with open(os.path.join(GOLD, "int4_nibble_order.txt")) as f:
+        lines = [l for l in f if not l.startswith("#")]
+    codes = np.array([int(t) for t in lines[0].split(":")[1].split()], dtype=np.uint8)[None, :]
+    words = [int(t, 16) for t in lines[1].split(":")[1].split()]
+    packed = pack_int4(codes)
+    assert [int(v) for v in packed.view(np.uint32)[0]] == words
+    assert np.array_equal(unpack_int4(packed), codes)
+    # every value in every nibble position
+    allc = np.array([[(v + j) % 16 for j in range(8)] for v in range(16)], dtype=np.uint8)
+    assert np.array_equal(unpack_int4(pack_int4(allc)), allc)
+    rng = np.random.default_rng(4)
+    wd = rng.integers(0, 2**32, size=(1000, 1250), dtype=np.uint64).astype(np.uint32)
+    edge = np.array([[0, 0xFFFFFFFF, 0xAAAAAAAA, 0x55555555, 0x80000000, 0x00000001]], np.uint32)
+    for arr in (wd, edge):
+        assert np.array_equal(pack_int4(unpack_int4(arr.view(np.int32))).view(np.uint32), arr)
+
+
+def test_kv_int8_per_head_bound():
+    rng = np.random.default_rng(5)
+    k = rng.normal(0, 1.3, (2, 3, 7, 128)).astype(np.float32)
+    c, s = quant_kv_int8(k)
+    assert c.shape == k.shape and s.shape == k.shape[:-1]
+    assert np.all(np.abs(k - c.astype(np.float32) * s[..., None]) <= s[..., None] / 2)
+    assert np.all(np.abs(c).max(axis=-1) == 127)
