@@ -1,0 +1,273 @@
+#!/usr/bin/env python
+"""Benchmark of the fingerprint forward pass on one MI355X.
+
+One "step" is one pass of the whole hot path over one batch: a prefill over the
+prompt (the time to first token) followed by S KV-cached decode steps, each
+feeding its output back as the next input (the time per output token) -- the
+dummy request iServe's Profiler sends to a fingerprint (paper Sec. 4.2, Sec. 5.3,
+Eq. 1).  Inputs are synthetic and already resident in HBM when timing starts.
+
+Prints ONE JSON line.  ``value`` is decode tokens/s = B * S * steps / (total
+decode time); prefill time, MFMA utilisation, the whole-pass rate and the
+dominant kernel's roofline sit beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fingerprint decode tokens/s + % HBM roofline; prefill MFMA utilisation"
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
+MFMA16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
+WBYTES = {"bf16": 2.0, "int8": 1.0, "int4": 0.5}
+
+KIND = {0: "rmsnorm", 1: "qkv", 2: "rope_kv", 3: "attn", 4: "o", 5: "resid_norm", 6: "gate_up",
+        7: "swiglu", 8: "down", 9: "pos"}
+PROJ = {"qkv", "o", "gate_up", "down"}
+
+
+def cfg_of(name):
+    from oracle.layer import CONFIGS
+    return CONFIGS[name]
+
+
+def proj_dims(s):
+    """(N, K) of the fused projections of one layer."""
+    qd, kd = s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+    return {"qkv": (qd + 2 * kd, s.hidden), "o": (s.hidden, qd), "gate_up": (2 * s.ffn, s.hidden),
+            "down": (s.hidden, s.ffn)}
+
+
+def weight_bytes(N, K, wq):
+    b = N * K * WBYTES[wq]
+    if wq == "int8":
+        b += N * 2                     # fp16 row scales
+    elif wq == "int4":
+        b += N * (K // 128) * 4        # fp16 scale + zero per group
+    return b
+
+
+def proj_bytes(kind, s, wq, M):
+    """Algorithmic bytes of one decode projection launch: weights + input + output."""
+    N, K = proj_dims(s)[kind]
+    return weight_bytes(N, K, wq) + M * K * 2 + M * N * 2
+
+
+def kv_tok_bytes(s, kvq):
+    return 2 * s.n_kv_heads * s.head_dim * (1 if kvq == "int8" else 2) + (4 * s.n_kv_heads if kvq == "int8" else 0)
+
+
+def decode_step_bytes(s, wq, kvq, B, t):
+    """Algorithmic HBM bytes of one decode step at position t (the new token's index)."""
+    per_layer = sum(weight_bytes(N, K, wq) for N, K in proj_dims(s).values()) + 2 * s.hidden * 2
+    kvt = kv_tok_bytes(s, kvq)
+    per_layer += B * (t + 1) * kvt + B * kvt
+    per_layer += B * 2 * (4 * s.hidden + 2 * s.n_heads * s.head_dim + 2 * s.ffn)
+    return s.n_layers * per_layer
+
+
+def prefill_flops(s, B, P):
+    params = sum(N * K for N, K in proj_dims(s).values())
+    return s.n_layers * (2 * B * P * params + 4 * s.head_dim * s.n_heads * B * P * (P + 1) // 2)
+
+
+def profile_decode(fp, x, y, stream_ptr):
+    """One eager decode step with HIP events around every launch (on the bench stream)."""
+    import ctypes
+    from paper_2501_13111_amd import binding
+
+    class KT(ctypes.Structure):
+        _fields_ = [("kind", ctypes.c_int32), ("layer", ctypes.c_int32), ("ms", ctypes.c_float)]
+    L = binding.load()
+    L.fp_profile_decode_step.argtypes = [ctypes.c_void_p] * 4 + [ctypes.POINTER(KT), ctypes.c_int32,
+                                                                 ctypes.POINTER(ctypes.c_int32)]
+    L.fp_profile_decode_step.restype = ctypes.c_int
+    recs = (KT * 512)()
+    n = ctypes.c_int32()
+    rc = L.fp_profile_decode_step(fp._h, x.data_ptr(), y.data_ptr(), stream_ptr, recs, 512, ctypes.byref(n))
+    if rc != 0:
+        raise RuntimeError(f"fp_profile_decode_step: {L.fp_last_error().decode()}")
+    return [(KIND[recs[i].kind], recs[i].layer, recs[i].ms) for i in range(n.value)]
+
+
+def profile_prefill(fp, x, y, B, P, stream_ptr):
+    import ctypes
+    from paper_2501_13111_amd import binding
+
+    class KT(ctypes.Structure):
+        _fields_ = [("kind", ctypes.c_int32), ("layer", ctypes.c_int32), ("ms", ctypes.c_float)]
+    L = binding.load()
+    L.fp_profile_prefill.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(KT), ctypes.c_int32,
+                                     ctypes.POINTER(ctypes.c_int32)]
+    L.fp_profile_prefill.restype = ctypes.c_int
+    recs = (KT * 512)()
+    n = ctypes.c_int32()
+    rc = L.fp_profile_prefill(fp._h, x.data_ptr(), B, P, y.data_ptr(), stream_ptr, recs, 512, ctypes.byref(n))
+    if rc != 0:
+        raise RuntimeError(f"fp_profile_prefill: {L.fp_last_error().decode()}")
+    fp.B = B
+    return [(KIND[recs[i].kind], recs[i].layer, recs[i].ms) for i in range(n.value)]
+
+
+def cpu_baseline(cfg, seed, budget_s):
+    """The oracle, as it stands, on a bounded sample of the workload: one sequence, the full
+    prompt, then decode steps until about ``budget_s`` seconds of decode have run."""
+    import numpy as np
+    import fpgen
+    from oracle.layer import Fingerprint as OracleFingerprint
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=os.cpu_count())
+    except Exception:
+        cores = os.cpu_count()
+    s = cfg["shape"]
+    orc = OracleFingerprint(s, cfg["wq"], cfg["kvq"], seed)
+    x = fpgen.prompt(seed, cfg["B"], cfg["P"], s.hidden, b_start=0, b_count=1)
+    t0 = time.perf_counter()
+    y = orc.prefill(x)
+    t_pre = time.perf_counter() - t0
+    xin = y[:, -1, :]
+    n, t_dec = 0, 0.0
+    while n < cfg["S"] and (t_dec < budget_s or n < 2):
+        t0 = time.perf_counter()
+        xin = orc.decode(xin)
+        t_dec += time.perf_counter() - t0
+        n += 1
+    return {"value": n / t_dec, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"1 of {cfg['B']} sequences, prefill of {cfg['P']} tokens "
+                      f"({t_pre:.2f} s) then {n} decode steps, float64 numpy oracle",
+            "prefill_s": round(t_pre, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="llama2-7b-bf16")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              f"(the multi-GPU sharding is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2501_13111_amd as P
+    from paper_2501_13111_amd import Fingerprint, fill_normal
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    P.load()
+
+    cfg = cfg_of(args.config)
+    s, wq, kvq, B, Pp, S = cfg["shape"], cfg["wq"], cfg["kvq"], cfg["B"], cfg["P"], cfg["S"]
+    H = s.hidden
+    fp = Fingerprint(s, wq, kvq, args.seed)
+    fp.set_decode_graph(not args.no_graph)
+    stream = torch.cuda.current_stream()
+    sp = int(stream.cuda_stream)
+    x = torch.empty(B * Pp * H, dtype=torch.bfloat16, device="cuda")
+    fill_normal(x, args.seed, -1, 15, 0.0, 1.0)
+    y = torch.empty_like(x)
+    bufs = [torch.empty(B * H, dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+
+    def one_pass(events=None):
+        fp.prefill(x, y, B, Pp)
+        if events is not None:
+            events[0].record(stream)
+        bufs[0].copy_(y.view(B, Pp, H)[:, -1, :].reshape(-1))
+        for st in range(S):
+            fp.decode_step(bufs[st % 2], bufs[(st + 1) % 2])
+            if events is not None:
+                events[st + 1].record(stream)
+
+    for _ in range(args.warmup):
+        one_pass()
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(S + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        one_pass(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    prefill_ms = [starts[k].elapsed_time(evs[k][0]) for k in range(args.steps)]
+    step_ms = [evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps) for i in range(S)]
+    decode_ms = [evs[k][0].elapsed_time(evs[k][S]) for k in range(args.steps)]
+    dec_total_s = sum(decode_ms) / 1e3
+    value = B * S * args.steps / dec_total_s
+    mean_bytes = statistics.fmean(decode_step_bytes(s, wq, kvq, B, Pp + i) for i in range(S))
+    med_step = statistics.median(step_ms)
+    step_frac = mean_bytes / (statistics.fmean(step_ms) / 1e3) / 1e9 / HBM_PEAK_GBS
+
+    # ---- per-kernel profile of a prefill and a decode step (eager, HIP events per launch)
+    pre_prof = profile_prefill(fp, x, y, B, Pp, sp)
+    bufs[0].copy_(y.view(B, Pp, H)[:, -1, :].reshape(-1))
+    dec_profs = []
+    for st in range(min(S, 8)):
+        dec_profs.append(profile_decode(fp, bufs[st % 2], bufs[(st + 1) % 2], sp))
+    by_kind = {}
+    for prof in dec_profs:
+        for kind, layer, ms in prof:
+            by_kind.setdefault(kind, []).append(ms)
+    dom = max(by_kind, key=lambda k: sum(by_kind[k]))
+    if dom in PROJ or True:
+        # the projections share one kernel (the weight-streaming skinny GEMM): report it as one
+        proj_ms = [ms for prof in dec_profs for kind, _, ms in prof if kind in PROJ]
+        proj_b = [proj_bytes(kind, s, wq, B) for prof in dec_profs for kind, _, _ in prof if kind in PROJ]
+        achieved = sum(proj_b) / (sum(proj_ms) / 1e3) / 1e9
+        roof = {"kernel": "skinny_kernel (decode weight-streaming projections qkv/o/gate_up/down)",
+                "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "avg_launch_us": round(1e3 * statistics.fmean(proj_ms), 3),
+                "bytes_per_launch_avg": int(statistics.fmean(proj_b)),
+                "dominant_by_time": dom}
+    pre_ms_total = sum(ms for _, _, ms in pre_prof)
+    pre_gemm_ms = sum(ms for kind, _, ms in pre_prof if kind in PROJ)
+    pflops = prefill_flops(s, B, Pp)
+    proj_flops = s.n_layers * 2 * B * Pp * sum(N * K for N, K in proj_dims(s).values())
+    kinds_us = {k: round(1e3 * statistics.fmean(v), 2) for k, v in sorted(by_kind.items())}
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall / args.steps, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if wq == "bf16" else "f16",
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) prompt hidden states; no checkpoint)",
+        "config": {"workload": args.config, "layers": s.n_layers, "hidden": H, "heads": s.n_heads,
+                   "kv_heads": s.n_kv_heads, "head_dim": s.head_dim, "ffn": s.ffn, "weights": wq,
+                   "kv_cache": kvq, "batch": B, "prompt": Pp, "decode_steps": S,
+                   "decode_graph": not args.no_graph},
+        "decode_step_us_median": round(1e3 * med_step, 2),
+        "decode_step_hbm_frac": round(step_frac, 4),
+        "decode_step_algorithmic_MB": round(mean_bytes / 1e6, 2),
+        "prefill_ms": round(statistics.median(prefill_ms), 4),
+        "prefill_tflops": round(pflops / (statistics.median(prefill_ms) / 1e3) / 1e12, 1),
+        "prefill_mfma_frac": round(pflops / (statistics.median(prefill_ms) / 1e3) / 1e12 / MFMA16_PEAK_TFLOPS, 4),
+        "prefill_gemm_mfma_frac": round(proj_flops / (pre_gemm_ms / 1e3) / 1e12 / MFMA16_PEAK_TFLOPS, 4),
+        "tokens_per_s_incl_prefill": round(B * S * args.steps / (sum(prefill_ms) / 1e3 + dec_total_s), 2),
+        "roofline": roof,
+        "decode_kernel_us": kinds_us,
+    }
+    fp.close()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,207 @@
+/*
+ * fp.h -- C ABI of the MI355X fingerprint forward pass.
+ *
+ * A fingerprint (iServe, arXiv 2501.13111, Sec. 1 and Sec. 5.1, Fig. 2) is an
+ * LLM cut down to a few hidden layers that keep the architecture's components.
+ * iServe's Profiler deploys it and sends dummy requests to measure the time to
+ * first token and the time per output token (Sec. 4.2, Sec. 5.3, Eq. 1):
+ * a prefill over the prompt, then one KV-cached decode step per output token.
+ * This library runs that forward pass for Llama-style decoder layers on one
+ * gfx950 GPU under the compression settings the paper searches over
+ * (Sec. 3.2, Table A.1): bf16 weights, int8 per-channel or int4 group-128
+ * weight-only quantisation, and a bf16 or int8 KV cache.
+ *
+ * Conventions shared by every call:
+ *  - Device pointers are HIP device addresses; host pointers are plain host
+ *    memory.  "stream" is a hipStream_t passed as void* (NULL = the default
+ *    stream).  Enqueuing calls return as soon as the work is queued; buffers
+ *    must stay valid until the stream has passed them.
+ *  - Activations are bf16 bit patterns (uint16), contiguous, row-major.
+ *  - Every argument and state check happens on the host before any launch;
+ *    on error nothing is modified and a negative fp_status is returned, with
+ *    a message available from fp_last_error() (thread-local).
+ *  - A handle is not thread-safe: calls on one handle must be serialised.
+ *  - The library allocates and owns weights, KV cache and workspace; the
+ *    caller owns the x / y buffers it passes.
+ */
+#ifndef FP_MI355X_H
+#define FP_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FP_OK = 0,
+    FP_ERR_INVALID_ARG = -1,   /* bad pointer, shape, size or enum */
+    FP_ERR_STATE = -2,         /* call not allowed in the handle's state (decode before prefill) */
+    FP_ERR_CAPACITY = -3,      /* batch / prompt / sequence beyond what the handle was created for */
+    FP_ERR_OOM = -4,           /* device allocation failed */
+    FP_ERR_HIP = -5,           /* HIP runtime error (no device, launch failure, ...) */
+    FP_ERR_UNSUPPORTED = -6    /* valid request this build does not implement */
+} fp_status;
+
+/* Weight compression (Sec. 3.2). */
+typedef enum {
+    FP_WQ_BF16 = 0,          /* unquantised 16-bit weights */
+    FP_WQ_INT8_CHANNEL = 1,  /* symmetric int8, one fp16 scale per output row */
+    FP_WQ_INT4_G128 = 2      /* asymmetric int4, fp16 scale and integer zero per 128 inputs */
+} fp_weight_quant;
+
+/* KV-cache compression (Sec. 3.2, "KV-cache quantization"). */
+typedef enum {
+    FP_KV_BF16 = 0,
+    FP_KV_INT8 = 1           /* int8 codes, one fp16 scale per (sequence, position, kv head) */
+} fp_kv_quant;
+
+/* Layer-stack shape and capacity, fixed at creation.
+ * Requirements: n_heads % n_kv_heads == 0; head_dim even and <= 256;
+ * hidden, n_heads*head_dim and ffn multiples of 16 (of 128 for int4 weights,
+ * whose groups run along every projection's input dimension);
+ * max_seq >= max_prompt + 1. */
+typedef struct {
+    int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn;
+    int32_t max_batch, max_prompt, max_seq;
+    float rms_eps;      /* RMSNorm epsilon, inside the square root (1e-5) */
+    float rope_theta;   /* rotary base (1e4) */
+} fp_shape;
+
+typedef struct fp_layer fp_layer;   /* opaque: weights, KV cache, workspace, position */
+
+/* Tensor ids (weights of layer l are synthesised from (seed, l, id)). */
+enum {
+    FP_T_ATTN_NORM = 0, FP_T_Q = 1, FP_T_K = 2, FP_T_V = 3, FP_T_O = 4,
+    FP_T_MLP_NORM = 5, FP_T_GATE = 6, FP_T_UP = 7, FP_T_DOWN = 8,
+    FP_T_INPUT = 15      /* prompt hidden states, layer id -1 */
+};
+
+/*
+ * Build a fingerprint: allocate weights, KV cache and workspace on the current
+ * device and synthesise the weights from `seed` (the Generator of Sec. 5.1
+ * reads a checkpoint; here weights ~N(0, 0.02) and norm gains 1 + N(0, 0.02)
+ * come from the counter-based generator of fp_fill_normal), then quantise them
+ * on the device.  Synchronous.  *out receives the handle (NULL on error).
+ */
+fp_status fp_layer_create(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant kvq,
+                          uint64_t seed, fp_layer** out);
+
+/*
+ * Validation-only handle with no device storage: fp_prefill / fp_decode_step
+ * check their arguments and advance the host-side state exactly as a real
+ * handle does, but enqueue no work; export calls return FP_ERR_STATE.  Needs
+ * no GPU (host-side tests of the argument and state checks).
+ */
+fp_status fp_layer_create_unbacked(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant kvq,
+                                   uint64_t seed, fp_layer** out);
+
+/* Free everything the handle owns (synchronises the device first).  NULL is a no-op. */
+fp_status fp_layer_destroy(fp_layer* layer);
+
+/*
+ * Prefill (time to first token, Sec. 5.3): run the layer stack over a prompt.
+ * x: device bf16 [B, P, hidden], y: device bf16 [B, P, hidden] (may not alias x).
+ * Resets the KV cache of the B sequences and sets the position to P.
+ * 1 <= B <= max_batch, 1 <= P <= max_prompt.
+ */
+fp_status fp_prefill(fp_layer* layer, const void* x, int32_t B, int32_t P, void* y, void* stream);
+
+/*
+ * One decode step (time per output token, Sec. 5.3): the B sequences of the
+ * last prefill each take one token's hidden state at the current position,
+ * append its K/V to the cache, attend over the whole prefix and produce the
+ * layer stack's output; the position then advances by one.
+ * x: device bf16 [B, hidden] (normally the previous output fed back), y: device
+ * bf16 [B, hidden], no aliasing.  FP_ERR_STATE before a prefill,
+ * FP_ERR_CAPACITY when the position has reached max_seq.
+ */
+fp_status fp_decode_step(fp_layer* layer, const void* x, void* y, void* stream);
+
+/*
+ * Replay decode steps as a captured HIP graph (1, the default) or launch the
+ * kernels one by one (0).  Results are identical.
+ */
+fp_status fp_set_decode_graph(fp_layer* layer, int32_t enable);
+
+/*
+ * Synthetic data on the device: dst[i] = bf16(mean + sigma * z_i), i < n, where
+ * z_i is element i of the Irwin-Hall-12 stream of (seed, layer, tensor):
+ *   key = mix64(mix64(seed) + G*(((layer+1) << 8) | tensor)),
+ *   words mix64(key + G*(c+1)) for c = 3i..3i+2, z_i = (sum of their twelve
+ *   16-bit lanes - 393210) * 2^-16, with mix64 the SplitMix64 finaliser
+ *   (Steele, Lea & Flood, OOPSLA 2014) and G = 0x9E3779B97F4A7C15.
+ * Prompts use layer -1, tensor FP_T_INPUT, mean 0, sigma 1.  dst: device bf16 [n].
+ */
+fp_status fp_fill_normal(void* dst, int64_t n, uint64_t seed, int32_t layer, int32_t tensor,
+                         float mean, float sigma, void* stream);
+
+/*
+ * Copy one weight tensor to host memory in its canonical layout (synchronous):
+ *  bf16:  codes = bf16 [N, K] (scales, zeros unused, may be NULL)
+ *  int8:  codes = int8 [N, K], scales = fp16 [N]
+ *  int4:  codes = int32 [N, K/8] with nibble j of word w holding column 8w+j,
+ *         scales = fp16 [N, K/128], zeros = fp16 [N, K/128] (integer values)
+ * Norm gains (FP_T_ATTN_NORM, FP_T_MLP_NORM): codes = bf16 [hidden].
+ * [N, K] is (out, in): q [nh*d, hidden], k/v [nkv*d, hidden], o [hidden, nh*d],
+ * gate/up [ffn, hidden], down [hidden, ffn].
+ */
+fp_status fp_export_weight(fp_layer* layer, int32_t l, int32_t tensor, void* codes, void* scales,
+                           void* zeros);
+
+/*
+ * Copy layer l's KV cache for the active batch to host memory (synchronous):
+ * k, v: [B, n_kv_heads, max_seq, head_dim] of bf16 or int8; k_scales, v_scales:
+ * fp16 [B, n_kv_heads, max_seq] (int8 cache only, else may be NULL).
+ */
+fp_status fp_export_kv(fp_layer* layer, int32_t l, void* k, void* v, void* k_scales, void* v_scales);
+
+/*
+ * Debug: when dev_f32 is non-NULL, every later prefill / decode step also
+ * writes the float32 K (after the rotary embedding) and V that enter the KV
+ * store of every layer into dev_f32, laid out [n_layers, 2, B, T, n_kv_heads,
+ * head_dim] with T the step's token count (P for prefill, 1 for decode);
+ * the buffer must hold n_layers*2*max_batch*max_prompt*n_kv_heads*head_dim
+ * floats.  NULL switches it off.  Disables graph replay while set.
+ */
+fp_status fp_set_debug_kv_dump(fp_layer* layer, void* dev_f32);
+
+/*
+ * Per-kernel timing (the Profiler of Sec. 4.2 measures latency with dummy
+ * requests; this breaks one request's step down by kernel).  Runs one prefill
+ * or one decode step exactly as fp_prefill / fp_decode_step do, but launches
+ * kernel by kernel with a HIP event recorded on `stream` before each launch and
+ * after the last; synchronises, then writes one record per launch into out[]
+ * (at most cap records; *count receives the number written).  State changes as
+ * for the plain call.
+ */
+typedef enum {
+    FP_K_RMSNORM = 0, FP_K_QKV = 1, FP_K_ROPE_KV = 2, FP_K_ATTN = 3, FP_K_O = 4,
+    FP_K_RESID_NORM = 5, FP_K_GATE_UP = 6, FP_K_SWIGLU = 7, FP_K_DOWN = 8, FP_K_POS = 9
+} fp_kernel_kind;
+
+typedef struct {
+    int32_t kind;    /* fp_kernel_kind */
+    int32_t layer;   /* layer index, -1 for step-level kernels */
+    float ms;        /* event-to-event device time of the launch */
+} fp_kernel_time;
+
+fp_status fp_profile_prefill(fp_layer* layer, const void* x, int32_t B, int32_t P, void* y,
+                             void* stream, fp_kernel_time* out, int32_t cap, int32_t* count);
+fp_status fp_profile_decode_step(fp_layer* layer, const void* x, void* y, void* stream,
+                                 fp_kernel_time* out, int32_t cap, int32_t* count);
+
+/* Bytes of device memory held for weights, KV cache and workspace. */
+fp_status fp_memory_bytes(const fp_layer* layer, size_t* weights, size_t* kv, size_t* workspace);
+
+/* Current position (tokens in the cache) and active batch of the handle. */
+fp_status fp_get_position(const fp_layer* layer, int32_t* pos, int32_t* batch);
+
+const char* fp_status_str(fp_status status);
+const char* fp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FP_MI355X_H */

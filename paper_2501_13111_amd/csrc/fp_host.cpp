@@ -1,0 +1,849 @@
+// Host runtime of the fingerprint forward pass: handle, validation, allocation,
+// weight synthesis, the prefill / decode schedules, graph replay of decode steps,
+// export and error reporting.  See include/fp.h for the contract of each call.
+//
+// Dataflow of one hidden layer (the paper names the components -- attention,
+// normalisation, activation -- Sec. 5.1; their Llama-style math is the reading):
+//   prefill, M = B*P tokens:
+//     rmsnorm(x) -> gemm[qkv] -> rope + KV append -> causal attention over the
+//     cache -> gemm[o] + residual -> rmsnorm -> gemm[gate|up] + SwiGLU ->
+//     gemm[down] + residual
+//   decode, M = B tokens at position pos:
+//     skinny[qkv] -> rope + KV append at pos -> split-context attention + merge
+//     -> skinny[o] -> residual + next rmsnorm -> skinny[gate|up] -> SwiGLU ->
+//     skinny[down] -> residual + next layer's rmsnorm
+// All weights of a layer live in three fused matrices: [q; k; v], o, [gate; up],
+// down, each [N, K] row-major (out x in).
+#include "../../include/fp.h"
+#include "fp_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <utility>
+#include <vector>
+
+using namespace fpk;
+
+namespace {
+
+thread_local std::string g_err;
+
+fp_status fail(fp_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+#define HIPCHK(expr)                                                                       \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess)                                                              \
+            return fail(FP_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
+    } while (0)
+
+constexpr uint64_t GAMMA = 0x9E3779B97F4A7C15ull;
+uint64_t mix64(uint64_t z) {
+    z ^= z >> 30; z *= 0xBF58476D1CE4E5B9ull;
+    z ^= z >> 27; z *= 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    return z;
+}
+uint64_t stream_key(uint64_t seed, int32_t layer, int32_t tensor) {
+    const uint64_t id = ((uint64_t)(int64_t)(layer + 1) << 8) | (uint64_t)(uint32_t)tensor;
+    return mix64(mix64(seed) + GAMMA * id);
+}
+
+constexpr int KSMAX = 16;         // max split-K factor of the decode projections
+constexpr int TARGET_WG = 1024;   // decode workgroups per projection the split-K aims for
+
+struct Mat {
+    void* codes = nullptr;        // bf16 / int8 / int4 words (device nibble order)
+    uint16_t* scales = nullptr;
+    uint16_t* zeros = nullptr;
+    int N = 0, K = 0;
+};
+
+struct LayerW {
+    uint16_t* attn_norm = nullptr;
+    uint16_t* mlp_norm = nullptr;
+    Mat qkv, o, gu, down;
+};
+
+// Event marks around each launch of a profiled step.
+struct Prof {
+    std::vector<hipEvent_t> ev;
+    std::vector<int> kind, layer;
+    hipStream_t st = nullptr;
+    bool on = false;
+    void mark(int k, int l) {
+        if (!on) return;
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        (void)hipEventRecord(e, st);
+        ev.push_back(e);
+        kind.push_back(k);
+        layer.push_back(l);
+    }
+    void end() {
+        if (!on) return;
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        (void)hipEventRecord(e, st);
+        ev.push_back(e);
+    }
+    void clear() {
+        for (auto e : ev) (void)hipEventDestroy(e);
+        ev.clear();
+        kind.clear();
+        layer.clear();
+        on = false;
+    }
+};
+
+}  // namespace
+
+struct fp_layer {
+    fp_shape s{};
+    int wq = 0, kvq = 0;
+    uint64_t seed = 0;
+    bool unbacked = false;
+    int act_fmt = ACT_BF16;
+    int q_dim = 0, kv_dim = 0, nqkv = 0;
+    std::vector<LayerW> L;
+    std::vector<void*> kc, vc;
+    std::vector<uint16_t*> ksc, vsc;
+    float* cos_t = nullptr;
+    float* sin_t = nullptr;
+    // workspace
+    uint16_t* act_in = nullptr;   // normalised inputs of qkv / gate|up  [Mmax, H]
+    uint16_t* act_o = nullptr;    // attention output                     [Mmax, q_dim]
+    uint16_t* act_f = nullptr;    // SwiGLU output                        [Mmax, F]
+    uint16_t* hbuf = nullptr;     // h = x + attention projection         [Mmax, H]
+    uint16_t* xbuf = nullptr;     // inter-layer hidden state              [Mmax, H]
+    float* qkv32 = nullptr;       // prefill q|k|v before rotary          [Mmax, Nqkv]
+    float* q32 = nullptr;         // rotated queries                      [Mmax, q_dim]
+    float* part = nullptr;        // decode split-K partials              [KSMAX, Bmax, Ncol]
+    float* attn_ws = nullptr;     // decode attention partials
+    int* d_pos = nullptr;
+    // state
+    int pos = 0, B = 0;
+    bool prefilled = false;
+    bool use_graph = true;
+    float* dump = nullptr;
+    hipStream_t cap_stream = nullptr;
+    std::map<std::pair<const void*, void*>, hipGraphExec_t> graphs;
+    Prof prof;
+    size_t bytes_w = 0, bytes_kv = 0, bytes_ws = 0;
+    std::vector<void*> allocs;
+};
+
+namespace {
+
+fp_status dev_alloc(fp_layer* h, void** p, size_t bytes, size_t* counter) {
+    if (bytes == 0) bytes = 256;
+    hipError_t e = hipMalloc(p, bytes);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        return fail(e == hipErrorOutOfMemory ? FP_ERR_OOM : FP_ERR_HIP, "hipMalloc(%zu) failed: %s",
+                    bytes, hipGetErrorString(e));
+    }
+    h->allocs.push_back(*p);
+    *counter += bytes;
+    return FP_OK;
+}
+
+template <typename T>
+fp_status alloc_t(fp_layer* h, T** p, size_t count, size_t* counter) {
+    void* v = nullptr;
+    fp_status st = dev_alloc(h, &v, count * sizeof(T), counter);
+    *p = (T*)v;
+    return st;
+}
+
+void free_all(fp_layer* h) {
+    for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
+    h->graphs.clear();
+    if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
+    h->cap_stream = nullptr;
+    for (void* p : h->allocs) (void)hipFree(p);
+    h->allocs.clear();
+}
+
+fp_status validate_shape(const fp_shape* s, int wq, int kvq) {
+    if (!s) return fail(FP_ERR_INVALID_ARG, "shape is NULL");
+    if (wq < FP_WQ_BF16 || wq > FP_WQ_INT4_G128) return fail(FP_ERR_INVALID_ARG, "bad weight quant %d", wq);
+    if (kvq < FP_KV_BF16 || kvq > FP_KV_INT8) return fail(FP_ERR_INVALID_ARG, "bad kv quant %d", kvq);
+    if (s->n_layers <= 0 || s->hidden <= 0 || s->n_heads <= 0 || s->n_kv_heads <= 0 ||
+        s->head_dim <= 0 || s->ffn <= 0 || s->max_batch <= 0 || s->max_prompt <= 0 || s->max_seq <= 0)
+        return fail(FP_ERR_INVALID_ARG, "shape fields must be positive");
+    if (s->n_heads % s->n_kv_heads != 0)
+        return fail(FP_ERR_INVALID_ARG, "n_heads %d not a multiple of n_kv_heads %d", s->n_heads, s->n_kv_heads);
+    if (s->head_dim % 2 != 0) return fail(FP_ERR_INVALID_ARG, "head_dim must be even");
+    if (s->max_seq < s->max_prompt) return fail(FP_ERR_INVALID_ARG, "max_seq < max_prompt");
+    if (!(s->rms_eps > 0.f) || !(s->rope_theta > 0.f)) return fail(FP_ERR_INVALID_ARG, "rms_eps and rope_theta must be > 0");
+    const int q_dim = s->n_heads * s->head_dim;
+    const int mult = (wq == FP_WQ_INT4_G128) ? 128 : 16;
+    if (s->hidden % mult || q_dim % mult || s->ffn % mult)
+        return fail(FP_ERR_INVALID_ARG, "hidden (%d), n_heads*head_dim (%d) and ffn (%d) must be multiples of %d",
+                    s->hidden, q_dim, s->ffn, mult);
+    if (s->head_dim != 64 && s->head_dim != 128)
+        return fail(FP_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", s->head_dim);
+    if (!attn_decode_supported(s->head_dim, s->n_heads / s->n_kv_heads))
+        return fail(FP_ERR_UNSUPPORTED, "query group size %d not supported (1, 2, 4, 8)",
+                    s->n_heads / s->n_kv_heads);
+    if (s->max_batch > 64) return fail(FP_ERR_UNSUPPORTED, "max_batch %d > 64", s->max_batch);
+    if ((int64_t)s->max_batch * s->max_prompt > (1 << 24))
+        return fail(FP_ERR_UNSUPPORTED, "max_batch * max_prompt too large");
+    return FP_OK;
+}
+
+size_t act_elems(const fp_layer* h) { return (size_t)h->s.max_batch * h->s.max_prompt; }
+
+// Allocate the storage of a [N, K] weight in format wq.
+fp_status alloc_mat(fp_layer* h, Mat* m, int N, int K) {
+    m->N = N;
+    m->K = K;
+    const size_t nk = (size_t)N * K;
+    fp_status st;
+    if (h->wq == FP_WQ_BF16) return alloc_t(h, (uint16_t**)&m->codes, nk, &h->bytes_w);
+    if (h->wq == FP_WQ_INT8_CHANNEL) {
+        if ((st = alloc_t(h, (int8_t**)&m->codes, nk, &h->bytes_w))) return st;
+        return alloc_t(h, &m->scales, (size_t)N, &h->bytes_w);
+    }
+    if ((st = alloc_t(h, (uint32_t**)&m->codes, nk / 8, &h->bytes_w))) return st;
+    if ((st = alloc_t(h, &m->scales, nk / 128, &h->bytes_w))) return st;
+    return alloc_t(h, &m->zeros, nk / 128, &h->bytes_w);
+}
+
+// Synthesise rows [row0, row0 + n) of matrix m from stream (seed, layer, tensor) and
+// quantise them into place.  tmp holds >= n * K bf16 values.
+fp_status synth_rows(fp_layer* h, Mat* m, int row0, int n, int layer, int tensor, uint16_t* tmp) {
+    const uint64_t key = stream_key(h->seed, layer, tensor);
+    const int K = m->K;
+    const int64_t cnt = (int64_t)n * K;
+    if (h->wq == FP_WQ_BF16) {
+        HIPCHK(launch_fill_bf16((uint16_t*)m->codes + (int64_t)row0 * K, cnt, key, 0.f, 0.02f, 0));
+        return FP_OK;
+    }
+    HIPCHK(launch_fill_bf16(tmp, cnt, key, 0.f, 0.02f, 0));
+    if (h->wq == FP_WQ_INT8_CHANNEL) {
+        HIPCHK(launch_quant_int8(tmp, n, K, (int8_t*)m->codes + (int64_t)row0 * K, m->scales + row0, 0));
+    } else {
+        HIPCHK(launch_quant_int4(tmp, n, K, (uint32_t*)m->codes + (int64_t)row0 * (K / 8),
+                                 m->scales + (int64_t)row0 * (K / 128), m->zeros + (int64_t)row0 * (K / 128), 0));
+    }
+    return FP_OK;
+}
+
+// Split-K factor and k-range for a decode projection.
+void choose_split(int tiles, int K, int wf, int* ks, int* krange) {
+    const int KS = skinny_kstep(wf);
+    const int nsteps = (K + KS - 1) / KS;
+    int k = (TARGET_WG + tiles - 1) / tiles;
+    int kmax = nsteps / 8;             // keep at least two steps per wave
+    if (kmax < 1) kmax = 1;
+    if (k > kmax) k = kmax;
+    if (k > KSMAX) k = KSMAX;
+    if (k < 1) k = 1;
+    const int per = (nsteps + k - 1) / k;
+    *krange = per * KS;
+    *ks = (K + *krange - 1) / *krange;
+}
+
+fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, int* ks_out,
+                     hipStream_t st) {
+    SkinnyArgs a{};
+    a.X = X;
+    a.W = m.codes;
+    a.scales = m.scales;
+    a.zeros = m.zeros;
+    a.M = M;
+    a.N = m.N;
+    a.K = m.K;
+    a.dual_F = dual_F;
+    a.part = h->part;
+    const int tiles = dual_F > 0 ? (dual_F + 15) / 16 : (m.N + 31) / 32;
+    int ks, kr;
+    choose_split(tiles, m.K, h->wq, &ks, &kr);
+    a.krange = kr;
+    HIPCHK(launch_skinny(a, h->wq, ks, st));
+    *ks_out = ks;
+    return FP_OK;
+}
+
+fp_status run_gemm(fp_layer* h, const uint16_t* X, const Mat& m, int M, int epi, float* out32,
+                   uint16_t* out16, const uint16_t* resid, hipStream_t st) {
+    GemmArgs a{};
+    a.X = X;
+    a.W = m.codes;
+    a.scales = m.scales;
+    a.zeros = m.zeros;
+    a.M = M;
+    a.N = m.N;
+    a.K = m.K;
+    a.F = h->s.ffn;
+    a.out32 = out32;
+    a.out16 = out16;
+    a.resid = resid;
+    a.out_fmt = h->act_fmt;
+    HIPCHK(launch_gemm(a, h->wq, epi, st));
+    return FP_OK;
+}
+
+RopeKvArgs rope_args(fp_layer* h, int l, const float* part, int ks, int M, int T, const int* d_pos,
+                     float* dump) {
+    RopeKvArgs r{};
+    r.part = part;
+    r.ks = ks;
+    r.M = M;
+    r.T = T;
+    r.nh = h->s.n_heads;
+    r.nkv = h->s.n_kv_heads;
+    r.d = h->s.head_dim;
+    r.d_pos = d_pos;
+    r.cos_t = h->cos_t;
+    r.sin_t = h->sin_t;
+    r.max_seq = h->s.max_seq;
+    r.qout = h->q32;
+    r.kc = h->kc[l];
+    r.vc = h->vc[l];
+    r.ks_out = h->ksc[l];
+    r.vs_out = h->vsc[l];
+    r.kv_int8 = h->kvq == FP_KV_INT8;
+    r.dump = dump;
+    return r;
+}
+
+fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t* y, hipStream_t st) {
+    const fp_shape& s = h->s;
+    const int M = B * P;
+    const float scale = (float)(1.0 / std::sqrt((double)s.head_dim));
+    fp_status rc;
+    for (int l = 0; l < s.n_layers; ++l) {
+        const LayerW& W = h->L[l];
+        const uint16_t* in = (l == 0) ? x : h->xbuf;
+        uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
+        float* dump = h->dump ? h->dump + (size_t)l * 2 * M * h->kv_dim : nullptr;
+        h->prof.mark(FP_K_RMSNORM, l);
+        HIPCHK(launch_rmsnorm(in, M, s.hidden, W.attn_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+        h->prof.mark(FP_K_QKV, l);
+        if ((rc = run_gemm(h, h->act_in, W.qkv, M, EPI_F32, h->qkv32, nullptr, nullptr, st))) return rc;
+        h->prof.mark(FP_K_ROPE_KV, l);
+        HIPCHK(launch_rope_kv(rope_args(h, l, h->qkv32, 1, M, P, nullptr, dump), st));
+        AttnPreArgs aa{};
+        aa.q = h->q32;
+        aa.kc = h->kc[l];
+        aa.vc = h->vc[l];
+        aa.k_scales = h->ksc[l];
+        aa.v_scales = h->vsc[l];
+        aa.kv_int8 = h->kvq == FP_KV_INT8;
+        aa.P = P;
+        aa.nh = s.n_heads;
+        aa.nkv = s.n_kv_heads;
+        aa.d = s.head_dim;
+        aa.max_seq = s.max_seq;
+        aa.scale = scale;
+        aa.out = h->act_o;
+        aa.out_fmt = h->act_fmt;
+        h->prof.mark(FP_K_ATTN, l);
+        HIPCHK(launch_attn_prefill(aa, B, st));
+        h->prof.mark(FP_K_O, l);
+        if ((rc = run_gemm(h, h->act_o, W.o, M, EPI_RESID, nullptr, h->hbuf, in, st))) return rc;
+        h->prof.mark(FP_K_RMSNORM, l);
+        HIPCHK(launch_rmsnorm(h->hbuf, M, s.hidden, W.mlp_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+        h->prof.mark(FP_K_GATE_UP, l);
+        if ((rc = run_gemm(h, h->act_in, W.gu, M, EPI_SWIGLU, nullptr, h->act_f, nullptr, st))) return rc;
+        h->prof.mark(FP_K_DOWN, l);
+        if ((rc = run_gemm(h, h->act_f, W.down, M, EPI_RESID, nullptr, out, h->hbuf, st))) return rc;
+    }
+    h->prof.mark(FP_K_POS, -1);
+    HIPCHK(launch_set_pos(h->d_pos, P, st));
+    h->prof.end();
+    return FP_OK;
+}
+
+fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
+    const fp_shape& s = h->s;
+    const int B = h->B;
+    const float scale = (float)(1.0 / std::sqrt((double)s.head_dim));
+    fp_status rc;
+    int ks;
+    h->prof.mark(FP_K_RMSNORM, 0);
+    HIPCHK(launch_rmsnorm(x, B, s.hidden, h->L[0].attn_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+    for (int l = 0; l < s.n_layers; ++l) {
+        const LayerW& W = h->L[l];
+        const uint16_t* in = (l == 0) ? x : h->xbuf;
+        uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
+        float* dump = h->dump ? h->dump + (size_t)l * 2 * B * h->kv_dim : nullptr;
+        h->prof.mark(FP_K_QKV, l);
+        if ((rc = run_skinny(h, h->act_in, W.qkv, B, 0, &ks, st))) return rc;
+        h->prof.mark(FP_K_ROPE_KV, l);
+        HIPCHK(launch_rope_kv(rope_args(h, l, h->part, ks, B, 1, h->d_pos, dump), st));
+        AttnDecArgs ad{};
+        ad.q = h->q32;
+        ad.kc = h->kc[l];
+        ad.vc = h->vc[l];
+        ad.k_scales = h->ksc[l];
+        ad.v_scales = h->vsc[l];
+        ad.kv_int8 = h->kvq == FP_KV_INT8;
+        ad.nh = s.n_heads;
+        ad.nkv = s.n_kv_heads;
+        ad.d = s.head_dim;
+        ad.max_seq = s.max_seq;
+        ad.d_pos = h->d_pos;
+        ad.scale = scale;
+        ad.ws = h->attn_ws;
+        ad.out = h->act_o;
+        ad.out_fmt = h->act_fmt;
+        h->prof.mark(FP_K_ATTN, l);
+        HIPCHK(launch_attn_decode(ad, B, st));
+        h->prof.mark(FP_K_O, l);
+        if ((rc = run_skinny(h, h->act_o, W.o, B, 0, &ks, st))) return rc;
+        h->prof.mark(FP_K_RESID_NORM, l);
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, W.mlp_norm, s.rms_eps, h->act_in,
+                                 h->act_fmt, st));
+        h->prof.mark(FP_K_GATE_UP, l);
+        if ((rc = run_skinny(h, h->act_in, W.gu, B, s.ffn, &ks, st))) return rc;
+        h->prof.mark(FP_K_SWIGLU, l);
+        HIPCHK(launch_swiglu(h->part, ks, B, s.ffn, h->act_f, h->act_fmt, st));
+        h->prof.mark(FP_K_DOWN, l);
+        if ((rc = run_skinny(h, h->act_f, W.down, B, 0, &ks, st))) return rc;
+        const uint16_t* gnext = (l + 1 < s.n_layers) ? h->L[l + 1].attn_norm : nullptr;
+        h->prof.mark(FP_K_RESID_NORM, l);
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, gnext, s.rms_eps, h->act_in,
+                                 h->act_fmt, st));
+    }
+    h->prof.mark(FP_K_POS, -1);
+    HIPCHK(launch_inc_pos(h->d_pos, st));
+    h->prof.end();
+    return FP_OK;
+}
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+    const char* pa = (const char*)a;
+    const char* pb = (const char*)b;
+    return pa < pb + nb && pb < pa + na;
+}
+
+}  // namespace
+
+// ============================================================================ C ABI
+extern "C" {
+
+const char* fp_status_str(fp_status s) {
+    switch (s) {
+        case FP_OK: return "FP_OK";
+        case FP_ERR_INVALID_ARG: return "FP_ERR_INVALID_ARG";
+        case FP_ERR_STATE: return "FP_ERR_STATE";
+        case FP_ERR_CAPACITY: return "FP_ERR_CAPACITY";
+        case FP_ERR_OOM: return "FP_ERR_OOM";
+        case FP_ERR_HIP: return "FP_ERR_HIP";
+        case FP_ERR_UNSUPPORTED: return "FP_ERR_UNSUPPORTED";
+    }
+    return "FP_ERR_UNKNOWN";
+}
+
+const char* fp_last_error(void) { return g_err.c_str(); }
+
+static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant kvq, uint64_t seed,
+                             fp_layer** out, bool unbacked) {
+    if (!out) return fail(FP_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    fp_status st = validate_shape(shape, wq, kvq);
+    if (st) return st;
+    fp_layer* h = new fp_layer();
+    h->s = *shape;
+    h->wq = wq;
+    h->kvq = kvq;
+    h->seed = seed;
+    h->unbacked = unbacked;
+    h->act_fmt = (wq == FP_WQ_BF16) ? ACT_BF16 : ACT_F16;
+    const fp_shape& s = h->s;
+    h->q_dim = s.n_heads * s.head_dim;
+    h->kv_dim = s.n_kv_heads * s.head_dim;
+    h->nqkv = h->q_dim + 2 * h->kv_dim;
+    if (unbacked) {
+        *out = h;
+        return FP_OK;
+    }
+
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev == 0) {
+        delete h;
+        return fail(FP_ERR_HIP, "no HIP device available");
+    }
+    int dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+        delete h;
+        return fail(FP_ERR_HIP, "cannot query the current HIP device");
+    }
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+        delete h;
+        return fail(FP_ERR_UNSUPPORTED, "device %s is not gfx950", prop.gcnArchName);
+    }
+
+    auto bail = [&](fp_status code) {
+        free_all(h);
+        delete h;
+        return code;
+    };
+    const int H = s.hidden, F = s.ffn;
+    h->L.resize(s.n_layers);
+    size_t maxrows = 0;
+    for (auto& W : h->L) {
+        if ((st = alloc_t(h, &W.attn_norm, H, &h->bytes_w))) return bail(st);
+        if ((st = alloc_t(h, &W.mlp_norm, H, &h->bytes_w))) return bail(st);
+        if ((st = alloc_mat(h, &W.qkv, h->nqkv, H))) return bail(st);
+        if ((st = alloc_mat(h, &W.o, H, h->q_dim))) return bail(st);
+        if ((st = alloc_mat(h, &W.gu, 2 * F, H))) return bail(st);
+        if ((st = alloc_mat(h, &W.down, H, F))) return bail(st);
+    }
+    maxrows = std::max<size_t>({(size_t)h->q_dim * H, (size_t)H * h->q_dim, (size_t)F * H, (size_t)H * F});
+    // KV cache
+    const size_t kv_elems = (size_t)s.max_batch * s.n_kv_heads * s.max_seq * s.head_dim;
+    const size_t kv_bytes = kv_elems * (kvq == FP_KV_INT8 ? 1 : 2);
+    const size_t sc_elems = (size_t)s.max_batch * s.n_kv_heads * s.max_seq;
+    h->kc.assign(s.n_layers, nullptr);
+    h->vc.assign(s.n_layers, nullptr);
+    h->ksc.assign(s.n_layers, nullptr);
+    h->vsc.assign(s.n_layers, nullptr);
+    for (int l = 0; l < s.n_layers; ++l) {
+        if ((st = dev_alloc(h, &h->kc[l], kv_bytes, &h->bytes_kv))) return bail(st);
+        if ((st = dev_alloc(h, &h->vc[l], kv_bytes, &h->bytes_kv))) return bail(st);
+        if (kvq == FP_KV_INT8) {
+            if ((st = alloc_t(h, &h->ksc[l], sc_elems, &h->bytes_kv))) return bail(st);
+            if ((st = alloc_t(h, &h->vsc[l], sc_elems, &h->bytes_kv))) return bail(st);
+        }
+    }
+    // workspace
+    const size_t Mmax = std::max(act_elems(h), (size_t)s.max_batch);
+    const int ncol = std::max({h->nqkv, H, 2 * F});
+    if ((st = alloc_t(h, &h->act_in, Mmax * H, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->act_o, Mmax * h->q_dim, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->act_f, Mmax * F, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->hbuf, Mmax * H, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->xbuf, Mmax * H, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->qkv32, Mmax * h->nqkv, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->q32, Mmax * h->q_dim, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return bail(st);
+    const size_t nch = attn_decode_chunks(s.max_seq);
+    if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 2), &h->bytes_ws)))
+        return bail(st);
+    if ((st = alloc_t(h, &h->d_pos, 1, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->cos_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->sin_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return bail(st);
+
+    // rotary tables: angle(p, i) = p * theta^(-2i/d) in double, rounded once to float
+    {
+        const int half = s.head_dim / 2;
+        std::vector<float> c((size_t)s.max_seq * half), sn((size_t)s.max_seq * half);
+        for (int i = 0; i < half; ++i) {
+            const double inv = std::pow((double)s.rope_theta, -2.0 * i / s.head_dim);
+            for (int p = 0; p < s.max_seq; ++p) {
+                const double ang = (double)p * inv;
+                c[(size_t)p * half + i] = (float)std::cos(ang);
+                sn[(size_t)p * half + i] = (float)std::sin(ang);
+            }
+        }
+        if (hipMemcpy(h->cos_t, c.data(), c.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+            hipMemcpy(h->sin_t, sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+            return bail(fail(FP_ERR_HIP, "rotary table upload failed"));
+    }
+
+    // weights
+    uint16_t* tmp = nullptr;
+    size_t tmp_bytes = 0;
+    if (wq != FP_WQ_BF16) {
+        if ((st = alloc_t(h, &tmp, maxrows, &tmp_bytes))) return bail(st);
+    }
+    for (int l = 0; l < s.n_layers; ++l) {
+        LayerW& W = h->L[l];
+        auto chk = [&](hipError_t e) { return e == hipSuccess ? FP_OK : fail(FP_ERR_HIP, "weight synthesis: %s", hipGetErrorString(e)); };
+        if ((st = chk(launch_fill_bf16(W.attn_norm, H, stream_key(seed, l, FP_T_ATTN_NORM), 1.f, 0.02f, 0)))) return bail(st);
+        if ((st = chk(launch_fill_bf16(W.mlp_norm, H, stream_key(seed, l, FP_T_MLP_NORM), 1.f, 0.02f, 0)))) return bail(st);
+        if ((st = synth_rows(h, &W.qkv, 0, h->q_dim, l, FP_T_Q, tmp))) return bail(st);
+        if ((st = synth_rows(h, &W.qkv, h->q_dim, h->kv_dim, l, FP_T_K, tmp))) return bail(st);
+        if ((st = synth_rows(h, &W.qkv, h->q_dim + h->kv_dim, h->kv_dim, l, FP_T_V, tmp))) return bail(st);
+        if ((st = synth_rows(h, &W.o, 0, H, l, FP_T_O, tmp))) return bail(st);
+        if ((st = synth_rows(h, &W.gu, 0, F, l, FP_T_GATE, tmp))) return bail(st);
+        if ((st = synth_rows(h, &W.gu, F, F, l, FP_T_UP, tmp))) return bail(st);
+        if ((st = synth_rows(h, &W.down, 0, H, l, FP_T_DOWN, tmp))) return bail(st);
+    }
+    if (hipDeviceSynchronize() != hipSuccess) return bail(fail(FP_ERR_HIP, "weight synthesis failed"));
+    if (tmp) {
+        (void)hipFree(tmp);
+        h->allocs.erase(std::find(h->allocs.begin(), h->allocs.end(), (void*)tmp));
+    }
+    // zero the KV cache so exports of unwritten positions are deterministic
+    for (int l = 0; l < s.n_layers; ++l) {
+        if (hipMemset(h->kc[l], 0, kv_bytes) != hipSuccess || hipMemset(h->vc[l], 0, kv_bytes) != hipSuccess)
+            return bail(fail(FP_ERR_HIP, "kv clear failed"));
+        if (kvq == FP_KV_INT8 && (hipMemset(h->ksc[l], 0, sc_elems * 2) != hipSuccess ||
+                                   hipMemset(h->vsc[l], 0, sc_elems * 2) != hipSuccess))
+            return bail(fail(FP_ERR_HIP, "kv clear failed"));
+    }
+    if (hipStreamCreateWithFlags(&h->cap_stream, hipStreamNonBlocking) != hipSuccess)
+        return bail(fail(FP_ERR_HIP, "stream creation failed"));
+    if (hipDeviceSynchronize() != hipSuccess) return bail(fail(FP_ERR_HIP, "create failed"));
+    *out = h;
+    return FP_OK;
+}
+
+fp_status fp_layer_create(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant kvq, uint64_t seed,
+                          fp_layer** out) {
+    return create_impl(shape, wq, kvq, seed, out, false);
+}
+
+fp_status fp_layer_create_unbacked(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant kvq,
+                                   uint64_t seed, fp_layer** out) {
+    return create_impl(shape, wq, kvq, seed, out, true);
+}
+
+fp_status fp_layer_destroy(fp_layer* h) {
+    if (!h) return FP_OK;
+    if (!h->unbacked) {
+        (void)hipDeviceSynchronize();
+        free_all(h);
+    }
+    delete h;
+    return FP_OK;
+}
+
+fp_status fp_prefill(fp_layer* h, const void* x, int32_t B, int32_t P, void* y, void* stream) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (!x || !y) return fail(FP_ERR_INVALID_ARG, "x and y must be device pointers");
+    if (B < 1 || P < 1) return fail(FP_ERR_INVALID_ARG, "B and P must be >= 1 (got %d, %d)", B, P);
+    if (B > h->s.max_batch) return fail(FP_ERR_CAPACITY, "B %d > max_batch %d", B, h->s.max_batch);
+    if (P > h->s.max_prompt) return fail(FP_ERR_CAPACITY, "P %d > max_prompt %d", P, h->s.max_prompt);
+    const size_t bytes = (size_t)B * P * h->s.hidden * 2;
+    if (overlap(x, bytes, y, bytes)) return fail(FP_ERR_INVALID_ARG, "x and y overlap");
+    if (!h->unbacked) {
+        fp_status st = enqueue_prefill(h, (const uint16_t*)x, B, P, (uint16_t*)y, (hipStream_t)stream);
+        if (st) {
+            h->prefilled = false;
+            return st;
+        }
+    }
+    h->B = B;
+    h->pos = P;
+    h->prefilled = true;
+    return FP_OK;
+}
+
+fp_status fp_decode_step(fp_layer* h, const void* x, void* y, void* stream) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (!x || !y) return fail(FP_ERR_INVALID_ARG, "x and y must be device pointers");
+    if (!h->prefilled) return fail(FP_ERR_STATE, "decode step before prefill");
+    if (h->pos >= h->s.max_seq) return fail(FP_ERR_CAPACITY, "position %d reached max_seq %d", h->pos, h->s.max_seq);
+    const size_t bytes = (size_t)h->B * h->s.hidden * 2;
+    if (overlap(x, bytes, y, bytes)) return fail(FP_ERR_INVALID_ARG, "x and y overlap");
+    if (!h->unbacked) {
+        hipStream_t st = (hipStream_t)stream;
+        fp_status rc;
+        if (h->use_graph && !h->dump) {
+            auto key = std::make_pair(x, y);
+            auto it = h->graphs.find(key);
+            if (it == h->graphs.end()) {
+                hipGraph_t g = nullptr;
+                hipGraphExec_t ge = nullptr;
+                HIPCHK(hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal));
+                rc = enqueue_decode(h, (const uint16_t*)x, (uint16_t*)y, h->cap_stream);
+                hipError_t e = hipStreamEndCapture(h->cap_stream, &g);
+                if (rc) {
+                    if (g) (void)hipGraphDestroy(g);
+                    return rc;
+                }
+                if (e != hipSuccess) return fail(FP_ERR_HIP, "graph capture failed: %s", hipGetErrorString(e));
+                e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+                (void)hipGraphDestroy(g);
+                if (e != hipSuccess) return fail(FP_ERR_HIP, "graph instantiate failed: %s", hipGetErrorString(e));
+                it = h->graphs.emplace(key, ge).first;
+            }
+            HIPCHK(hipGraphLaunch(it->second, st));
+        } else {
+            if ((rc = enqueue_decode(h, (const uint16_t*)x, (uint16_t*)y, st))) return rc;
+        }
+    }
+    h->pos += 1;
+    return FP_OK;
+}
+
+static fp_status collect_profile(fp_layer* h, fp_kernel_time* out, int32_t cap, int32_t* count) {
+    fp_status rc = FP_OK;
+    if (hipStreamSynchronize(h->prof.st) != hipSuccess) rc = fail(FP_ERR_HIP, "profile synchronise failed");
+    int n = 0;
+    for (size_t i = 0; rc == FP_OK && i + 1 < h->prof.ev.size(); ++i) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, h->prof.ev[i], h->prof.ev[i + 1]) != hipSuccess) {
+            rc = fail(FP_ERR_HIP, "event timing failed");
+            break;
+        }
+        if (n < cap) out[n++] = fp_kernel_time{h->prof.kind[i], h->prof.layer[i], ms};
+    }
+    if (count) *count = n;
+    h->prof.clear();
+    return rc;
+}
+
+fp_status fp_profile_prefill(fp_layer* h, const void* x, int32_t B, int32_t P, void* y, void* stream,
+                             fp_kernel_time* out, int32_t cap, int32_t* count) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (!out || cap <= 0) return fail(FP_ERR_INVALID_ARG, "no output records");
+    if (h->unbacked) return fail(FP_ERR_STATE, "handle has no device storage");
+    h->prof.clear();
+    h->prof.on = true;
+    h->prof.st = (hipStream_t)stream;
+    fp_status rc = fp_prefill(h, x, B, P, y, stream);
+    if (rc) {
+        h->prof.clear();
+        return rc;
+    }
+    return collect_profile(h, out, cap, count);
+}
+
+fp_status fp_profile_decode_step(fp_layer* h, const void* x, void* y, void* stream, fp_kernel_time* out,
+                                 int32_t cap, int32_t* count) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (!out || cap <= 0) return fail(FP_ERR_INVALID_ARG, "no output records");
+    if (h->unbacked) return fail(FP_ERR_STATE, "handle has no device storage");
+    const bool g = h->use_graph;
+    h->use_graph = false;            // launch kernel by kernel
+    h->prof.clear();
+    h->prof.on = true;
+    h->prof.st = (hipStream_t)stream;
+    fp_status rc = fp_decode_step(h, x, y, stream);
+    h->use_graph = g;
+    if (rc) {
+        h->prof.clear();
+        return rc;
+    }
+    return collect_profile(h, out, cap, count);
+}
+
+fp_status fp_set_decode_graph(fp_layer* h, int32_t enable) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    h->use_graph = enable != 0;
+    return FP_OK;
+}
+
+fp_status fp_fill_normal(void* dst, int64_t n, uint64_t seed, int32_t layer, int32_t tensor, float mean,
+                         float sigma, void* stream) {
+    if (!dst && n > 0) return fail(FP_ERR_INVALID_ARG, "dst is NULL");
+    if (n < 0) return fail(FP_ERR_INVALID_ARG, "n < 0");
+    if (tensor < 0 || tensor > 255) return fail(FP_ERR_INVALID_ARG, "tensor id out of range");
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev == 0) return fail(FP_ERR_HIP, "no HIP device available");
+    HIPCHK(launch_fill_bf16((uint16_t*)dst, n, stream_key(seed, layer, tensor), mean, sigma, (hipStream_t)stream));
+    return FP_OK;
+}
+
+fp_status fp_export_weight(fp_layer* h, int32_t l, int32_t tensor, void* codes, void* scales, void* zeros) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (l < 0 || l >= h->s.n_layers) return fail(FP_ERR_INVALID_ARG, "layer index %d out of range", l);
+    if (!codes) return fail(FP_ERR_INVALID_ARG, "codes is NULL");
+    if (h->unbacked) return fail(FP_ERR_STATE, "handle has no device storage");
+    const LayerW& W = h->L[l];
+    const int H = h->s.hidden;
+    if (tensor == FP_T_ATTN_NORM || tensor == FP_T_MLP_NORM) {
+        HIPCHK(hipDeviceSynchronize());
+        HIPCHK(hipMemcpy(codes, tensor == FP_T_ATTN_NORM ? W.attn_norm : W.mlp_norm, (size_t)H * 2, hipMemcpyDeviceToHost));
+        return FP_OK;
+    }
+    const Mat* m = nullptr;
+    int row0 = 0, n = 0;
+    switch (tensor) {
+        case FP_T_Q: m = &W.qkv; row0 = 0; n = h->q_dim; break;
+        case FP_T_K: m = &W.qkv; row0 = h->q_dim; n = h->kv_dim; break;
+        case FP_T_V: m = &W.qkv; row0 = h->q_dim + h->kv_dim; n = h->kv_dim; break;
+        case FP_T_O: m = &W.o; row0 = 0; n = H; break;
+        case FP_T_GATE: m = &W.gu; row0 = 0; n = h->s.ffn; break;
+        case FP_T_UP: m = &W.gu; row0 = h->s.ffn; n = h->s.ffn; break;
+        case FP_T_DOWN: m = &W.down; row0 = 0; n = H; break;
+        default: return fail(FP_ERR_INVALID_ARG, "unknown tensor id %d", tensor);
+    }
+    const int K = m->K;
+    HIPCHK(hipDeviceSynchronize());
+    if (h->wq == FP_WQ_BF16) {
+        HIPCHK(hipMemcpy(codes, (const uint16_t*)m->codes + (size_t)row0 * K, (size_t)n * K * 2, hipMemcpyDeviceToHost));
+        return FP_OK;
+    }
+    if (!scales) return fail(FP_ERR_INVALID_ARG, "scales is NULL");
+    if (h->wq == FP_WQ_INT8_CHANNEL) {
+        HIPCHK(hipMemcpy(codes, (const int8_t*)m->codes + (size_t)row0 * K, (size_t)n * K, hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(scales, m->scales + row0, (size_t)n * 2, hipMemcpyDeviceToHost));
+        return FP_OK;
+    }
+    if (!zeros) return fail(FP_ERR_INVALID_ARG, "zeros is NULL");
+    const size_t words = (size_t)n * K / 8;
+    uint32_t* dst = (uint32_t*)codes;
+    HIPCHK(hipMemcpy(dst, (const uint32_t*)m->codes + (size_t)row0 * (K / 8), words * 4, hipMemcpyDeviceToHost));
+    // device nibble order -> canonical (nibble j holds column 8w + j)
+    for (size_t i = 0; i < words; ++i) {
+        const uint32_t wv = dst[i];
+        uint32_t c = 0;
+        for (int p = 0; p < 8; ++p) {
+            const int col = (p < 4) ? 2 * p : 2 * (p - 4) + 1;
+            c |= ((wv >> (4 * p)) & 0xFu) << (4 * col);
+        }
+        dst[i] = c;
+    }
+    HIPCHK(hipMemcpy(scales, m->scales + (size_t)row0 * (K / 128), (size_t)n * (K / 128) * 2, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(zeros, m->zeros + (size_t)row0 * (K / 128), (size_t)n * (K / 128) * 2, hipMemcpyDeviceToHost));
+    return FP_OK;
+}
+
+fp_status fp_export_kv(fp_layer* h, int32_t l, void* k, void* v, void* k_scales, void* v_scales) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (l < 0 || l >= h->s.n_layers) return fail(FP_ERR_INVALID_ARG, "layer index %d out of range", l);
+    if (!k || !v) return fail(FP_ERR_INVALID_ARG, "k and v must be host buffers");
+    if (h->unbacked) return fail(FP_ERR_STATE, "handle has no device storage");
+    if (!h->prefilled) return fail(FP_ERR_STATE, "no prefill yet");
+    const fp_shape& s = h->s;
+    const size_t elems = (size_t)h->B * s.n_kv_heads * s.max_seq * s.head_dim;
+    const size_t esz = h->kvq == FP_KV_INT8 ? 1 : 2;
+    HIPCHK(hipDeviceSynchronize());
+    HIPCHK(hipMemcpy(k, h->kc[l], elems * esz, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(v, h->vc[l], elems * esz, hipMemcpyDeviceToHost));
+    if (h->kvq == FP_KV_INT8) {
+        if (!k_scales || !v_scales) return fail(FP_ERR_INVALID_ARG, "scale buffers are NULL");
+        const size_t n = (size_t)h->B * s.n_kv_heads * s.max_seq;
+        HIPCHK(hipMemcpy(k_scales, h->ksc[l], n * 2, hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(v_scales, h->vsc[l], n * 2, hipMemcpyDeviceToHost));
+    }
+    return FP_OK;
+}
+
+fp_status fp_set_debug_kv_dump(fp_layer* h, void* dev_f32) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    h->dump = (float*)dev_f32;
+    return FP_OK;
+}
+
+fp_status fp_memory_bytes(const fp_layer* h, size_t* weights, size_t* kv, size_t* workspace) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (weights) *weights = h->bytes_w;
+    if (kv) *kv = h->bytes_kv;
+    if (workspace) *workspace = h->bytes_ws;
+    return FP_OK;
+}
+
+fp_status fp_get_position(const fp_layer* h, int32_t* pos, int32_t* batch) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (pos) *pos = h->prefilled ? h->pos : 0;
+    if (batch) *batch = h->prefilled ? h->B : 0;
+    return FP_OK;
+}
+
+}  // extern "C"

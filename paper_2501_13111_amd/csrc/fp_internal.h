@@ -1,0 +1,109 @@
+// Internal interface between the host runtime (fp_host.cpp) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fpk {
+
+enum WFmt { W_BF16 = 0, W_INT8 = 1, W_INT4 = 2 };
+enum Epi { EPI_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+// Activation format of a GEMM's A operand: bf16 for bf16 weights, fp16 for quantised
+// weights (the fp16 copy of a bf16-rounded value is exact in fp16's normal range).
+enum ActFmt { ACT_BF16 = 0, ACT_F16 = 1 };
+
+// Decode skinny GEMM: part[s, m, col] = sum_{k in split s} X[m, k] W[col, k]
+// (times the row scale for int8).  W rows are output columns; dual_F > 0 selects
+// the SwiGLU tiling over the concatenated [gate; up] matrix of 2 * dual_F rows.
+struct SkinnyArgs {
+    const uint16_t* X;        // activations [M, K] (bf16 for bf16 weights, else fp16)
+    const void* W;            // bf16 [N, K] / int8 [N, K] / int4 words [N, K/8] (device order)
+    const uint16_t* scales;   // fp16: int8 [N]; int4 [N, K/128]
+    const uint16_t* zeros;    // fp16 [N, K/128] (int4)
+    int M, N, K;
+    int dual_F;
+    int krange;               // k per split (multiple of the format's K-step)
+    float* part;              // [ks, M, N] fp32
+};
+
+struct GemmArgs {
+    const uint16_t* X;        // activations [M, K]
+    const void* W;
+    const uint16_t* scales;
+    const uint16_t* zeros;
+    int M, N, K, F;           // F: SwiGLU width (N = 2F rows of [gate; up])
+    float* out32;             // EPI_F32: [M, N]
+    uint16_t* out16;          // EPI_RESID: bf16 [M, N]; EPI_SWIGLU: act [M, F]
+    const uint16_t* resid;    // EPI_RESID: bf16 [M, N]
+    int out_fmt;              // EPI_SWIGLU activation format
+};
+
+struct RopeKvArgs {
+    const float* part;        // [ks, M, Nqkv]
+    int ks, M, T, nh, nkv, d;
+    const int* d_pos;         // NULL -> positions start at 0
+    const float* cos_t;
+    const float* sin_t;
+    int max_seq;
+    float* qout;              // [M, nh*d]
+    void* kc;
+    void* vc;
+    uint16_t* ks_out;
+    uint16_t* vs_out;
+    int kv_int8;
+    float* dump;              // NULL or [2, M, nkv, d]
+};
+
+struct AttnDecArgs {
+    const float* q;           // [B, nh*d] rotated queries
+    const void* kc;           // layer cache [B, nkv, max_seq, d]
+    const void* vc;
+    const uint16_t* k_scales; // [B, nkv, max_seq] (int8)
+    const uint16_t* v_scales;
+    int kv_int8, nh, nkv, d, max_seq;
+    const int* d_pos;         // current position (the new token's index)
+    float scale;              // float32(1/sqrt(d))
+    float* ws;                // [B, nh, nchunks, d + 2]
+    uint16_t* out;            // [B, nh*d] activation format out_fmt
+    int out_fmt;
+};
+
+struct AttnPreArgs {
+    const float* q;           // [B*P, nh*d]
+    const void* kc;
+    const void* vc;
+    const uint16_t* k_scales;
+    const uint16_t* v_scales;
+    int kv_int8, P, nh, nkv, d, max_seq;
+    float scale;
+    uint16_t* out;            // [B*P, nh*d]
+    int out_fmt;
+};
+
+hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint64_t key, float mean, float sigma,
+                            hipStream_t st);
+hipError_t launch_quant_int8(const uint16_t* w, int N, int K, int8_t* codes, uint16_t* scales,
+                             hipStream_t st);
+hipError_t launch_quant_int4(const uint16_t* w, int N, int K, uint32_t* codes, uint16_t* scales,
+                             uint16_t* zeros, hipStream_t st);
+
+hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, float eps, uint16_t* out,
+                          int out_fmt, hipStream_t st);
+hipError_t launch_resid_norm(const float* part, int ks, int M, int N, const uint16_t* resid,
+                             uint16_t* out, const uint16_t* g, float eps, uint16_t* nout, int nfmt,
+                             hipStream_t st);
+hipError_t launch_swiglu(const float* part, int ks, int M, int F, uint16_t* a, int afmt,
+                         hipStream_t st);
+hipError_t launch_rope_kv(const RopeKvArgs& a, hipStream_t st);
+hipError_t launch_set_pos(int* d_pos, int v, hipStream_t st);
+hipError_t launch_inc_pos(int* d_pos, hipStream_t st);
+
+int skinny_kstep(int wf);
+hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st);
+hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st);
+
+int attn_decode_chunks(int max_seq);
+bool attn_decode_supported(int d, int group);
+hipError_t launch_attn_decode(const AttnDecArgs& a, int B, hipStream_t st);
+hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st);
+
+}  // namespace fpk
