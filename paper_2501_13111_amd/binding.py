@@ -55,11 +55,12 @@ def lib_path() -> str:
 
 
 def load(path: str | None = None):
-    """Load the built HIP library (raises if it is missing)."""
+    """Load the built HIP library (raises if it is missing).  The environment variable
+    FP_MI355X_LIB selects another build of the same library (e.g. a tuning variant)."""
     global _lib
     if _lib is not None:
         return _lib
-    p = path or LIB_PATH
+    p = path or os.environ.get("FP_MI355X_LIB") or LIB_PATH
     if not os.path.exists(p):
         raise RuntimeError(f"HIP library not built: {p} is missing (run __graft_entry__.build())")
     L = ctypes.CDLL(p)

@@ -31,30 +31,36 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def _compile(src: str, hipcc: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc, *COMMON, "-c", src, "-o", obj]
+def _compile(src: str, hipcc: str, build_dir: str, extra: list) -> str:
+    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+    cmd = [hipcc, *COMMON, *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     return obj
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, out: str | None = None, defines: dict | None = None) -> str:
+    """Compile and link.  ``out`` overrides the library path and ``defines`` adds -D
+    macros (tuning constants such as SKINNY_NS or FP_TARGET_WG)."""
     hipcc = _hipcc()
-    os.makedirs(BUILD_DIR, exist_ok=True)
+    lib = out or LIB
+    extra = [f"-D{k}={v}" for k, v in (defines or {}).items()]
+    build_dir = BUILD_DIR if not extra else os.path.join(BUILD_DIR, "v_" + "_".join(f"{k}{v}" for k, v in sorted(defines.items())))
+    os.makedirs(build_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, hipcc), srcs))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, hipcc, build_dir, extra), srcs))
+    LIB_ = lib
+    tmp = LIB_ + ".tmp"
     cmd = [hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, LIB_)
     if verbose:
-        print("built", LIB)
-    return LIB
+        print("built", LIB_)
+    return LIB_
 
 
 if __name__ == "__main__":

@@ -64,14 +64,18 @@ uint64_t stream_key(uint64_t seed, int32_t layer, int32_t tensor) {
     return mix64(mix64(seed) + GAMMA * id);
 }
 
-constexpr int KSMAX = 16;         // max split-K factor of the decode projections
-constexpr int TARGET_WG = 1024;   // decode workgroups per projection the split-K aims for
+constexpr int KSMAX = 64;         // max split-K factor of the decode projections
+#ifndef FP_TARGET_WG
+#define FP_TARGET_WG 512
+#endif
+constexpr int TARGET_WG = FP_TARGET_WG;   // decode workgroups per projection the split-K aims for
 
 struct Mat {
-    void* codes = nullptr;        // bf16 / int8 / int4 words (device nibble order)
+    void* codes = nullptr;        // fragment-major tiles of bf16 / int8 / int4 (device nibble order)
     uint16_t* scales = nullptr;
     uint16_t* zeros = nullptr;
     int N = 0, K = 0;
+    int kst = 0;                  // K-steps (1 KiB blocks) per 16-row block row
 };
 
 struct LayerW {
@@ -134,7 +138,9 @@ struct fp_layer {
     float* qkv32 = nullptr;       // prefill q|k|v before rotary          [Mmax, Nqkv]
     float* q32 = nullptr;         // rotated queries                      [Mmax, q_dim]
     float* part = nullptr;        // decode split-K partials              [KSMAX, Bmax, Ncol]
+    float* part2 = nullptr;       // gate|up partials (read while down writes part)
     float* attn_ws = nullptr;     // decode attention partials
+    float* ssq = nullptr;         // decode row-norm block sums         [Bmax, nblk]
     int* d_pos = nullptr;
     // state
     int pos = 0, B = 0;
@@ -214,55 +220,68 @@ size_t act_elems(const fp_layer* h) { return (size_t)h->s.max_batch * h->s.max_p
 fp_status alloc_mat(fp_layer* h, Mat* m, int N, int K) {
     m->N = N;
     m->K = K;
+    const int KS = weight_kstep(h->wq);
+    m->kst = (K + KS - 1) / KS;
     const size_t nk = (size_t)N * K;
     fp_status st;
-    if (h->wq == FP_WQ_BF16) return alloc_t(h, (uint16_t**)&m->codes, nk, &h->bytes_w);
-    if (h->wq == FP_WQ_INT8_CHANNEL) {
-        if ((st = alloc_t(h, (int8_t**)&m->codes, nk, &h->bytes_w))) return st;
-        return alloc_t(h, &m->scales, (size_t)N, &h->bytes_w);
-    }
-    if ((st = alloc_t(h, (uint32_t**)&m->codes, nk / 8, &h->bytes_w))) return st;
-    if ((st = alloc_t(h, &m->scales, nk / 128, &h->bytes_w))) return st;
-    return alloc_t(h, &m->zeros, nk / 128, &h->bytes_w);
-}
-
-// Synthesise rows [row0, row0 + n) of matrix m from stream (seed, layer, tensor) and
-// quantise them into place.  tmp holds >= n * K bf16 values.
-fp_status synth_rows(fp_layer* h, Mat* m, int row0, int n, int layer, int tensor, uint16_t* tmp) {
-    const uint64_t key = stream_key(h->seed, layer, tensor);
-    const int K = m->K;
-    const int64_t cnt = (int64_t)n * K;
-    if (h->wq == FP_WQ_BF16) {
-        HIPCHK(launch_fill_bf16((uint16_t*)m->codes + (int64_t)row0 * K, cnt, key, 0.f, 0.02f, 0));
-        return FP_OK;
-    }
-    HIPCHK(launch_fill_bf16(tmp, cnt, key, 0.f, 0.02f, 0));
-    if (h->wq == FP_WQ_INT8_CHANNEL) {
-        HIPCHK(launch_quant_int8(tmp, n, K, (int8_t*)m->codes + (int64_t)row0 * K, m->scales + row0, 0));
-    } else {
-        HIPCHK(launch_quant_int4(tmp, n, K, (uint32_t*)m->codes + (int64_t)row0 * (K / 8),
-                                 m->scales + (int64_t)row0 * (K / 128), m->zeros + (int64_t)row0 * (K / 128), 0));
+    if ((st = dev_alloc(h, &m->codes, (size_t)(N / 16) * m->kst * 1024, &h->bytes_w))) return st;
+    if (h->wq == FP_WQ_INT8_CHANNEL) return alloc_t(h, &m->scales, (size_t)N, &h->bytes_w);
+    if (h->wq == FP_WQ_INT4_G128) {
+        if ((st = alloc_t(h, &m->scales, nk / 128, &h->bytes_w))) return st;
+        return alloc_t(h, &m->zeros, nk / 128, &h->bytes_w);
     }
     return FP_OK;
 }
 
-// Split-K factor and k-range for a decode projection.
-void choose_split(int tiles, int K, int wf, int* ks, int* krange) {
+// Synthesise rows [row0, row0 + n) of matrix m from stream (seed, layer, tensor),
+// quantise them (row-major, in tmpq) and write them into the fragment-major tiles.
+// tmp holds >= n * K bf16 values, tmpq >= n * K bytes.
+fp_status synth_rows(fp_layer* h, Mat* m, int row0, int n, int layer, int tensor, uint16_t* tmp, void* tmpq) {
+    const uint64_t key = stream_key(h->seed, layer, tensor);
+    const int K = m->K;
+    const int64_t cnt = (int64_t)n * K;
+    const int KS = weight_kstep(h->wq), eb = weight_ebits(h->wq);
+    HIPCHK(launch_fill_bf16(tmp, cnt, key, 0.f, 0.02f, 0));
+    const void* src = tmp;
+    if (h->wq == FP_WQ_INT8_CHANNEL) {
+        HIPCHK(launch_quant_int8(tmp, n, K, (int8_t*)tmpq, m->scales + row0, 0));
+        src = tmpq;
+    } else if (h->wq == FP_WQ_INT4_G128) {
+        HIPCHK(launch_quant_int4(tmp, n, K, (uint32_t*)tmpq, m->scales + (int64_t)row0 * (K / 128),
+                                 m->zeros + (int64_t)row0 * (K / 128), 0));
+        src = tmpq;
+    }
+    HIPCHK(launch_tile(src, n, K, eb, KS, m->codes, row0, 0));
+    return FP_OK;
+}
+
+// Split-K factor and k-range for a decode projection: aim for TARGET_WG workgroups,
+// within the LDS bound on the staged activation slice.
+void choose_split(int tiles, int K, int M, int wf, int* ks, int* krange) {
     const int KS = skinny_kstep(wf);
     const int nsteps = (K + KS - 1) / KS;
     int k = (TARGET_WG + tiles - 1) / tiles;
-    int kmax = nsteps / 8;             // keep at least two steps per wave
+    int kmax = nsteps / 4;             // keep at least four K-steps per workgroup
     if (kmax < 1) kmax = 1;
     if (k > kmax) k = kmax;
-    if (k > KSMAX) k = KSMAX;
     if (k < 1) k = 1;
-    const int per = (nsteps + k - 1) / k;
+    int per = (nsteps + k - 1) / k;
+    const int maxsteps = skinny_max_krange(M) / KS;
+    if (per > maxsteps) per = maxsteps;
     *krange = per * KS;
     *ks = (K + *krange - 1) / *krange;
 }
 
-fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, int* ks_out,
-                     hipStream_t st) {
+struct XIn {
+    int xf = XF_COPY;
+    const uint16_t* gain = nullptr;
+    const float* ssq = nullptr;
+    const float* src_part = nullptr;
+    int src_ks = 0;
+};
+
+fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, const XIn& xin,
+                     float* part, int* ks_out, hipStream_t st) {
     SkinnyArgs a{};
     a.X = X;
     a.W = m.codes;
@@ -271,11 +290,19 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     a.M = M;
     a.N = m.N;
     a.K = m.K;
+    a.kst = m.kst;
     a.dual_F = dual_F;
-    a.part = h->part;
-    const int tiles = dual_F > 0 ? (dual_F + 15) / 16 : (m.N + 31) / 32;
+    a.part = part;
+    a.xf = xin.xf;
+    a.gain = xin.gain;
+    a.ssq = xin.ssq;
+    a.ssq_blocks = resid_ssq_blocks(h->s.hidden);
+    a.eps = h->s.rms_eps;
+    a.src_part = xin.src_part;
+    a.src_ks = xin.src_ks;
     int ks, kr;
-    choose_split(tiles, m.K, h->wq, &ks, &kr);
+    choose_split(skinny_tiles(m.N, dual_F), m.K, M, h->wq, &ks, &kr);
+    if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     a.krange = kr;
     HIPCHK(launch_skinny(a, h->wq, ks, st));
     *ks_out = ks;
@@ -292,6 +319,7 @@ fp_status run_gemm(fp_layer* h, const uint16_t* X, const Mat& m, int M, int epi,
     a.M = M;
     a.N = m.N;
     a.K = m.K;
+    a.kst = m.kst;
     a.F = h->s.ffn;
     a.out32 = out32;
     a.out16 = out16;
@@ -379,19 +407,28 @@ fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_
     const float scale = (float)(1.0 / std::sqrt((double)s.head_dim));
     fp_status rc;
     int ks;
+    // sums of squares of the layer-0 input rows (its RMSNorm is applied while the qkv
+    // projection stages its input)
     h->prof.mark(FP_K_RMSNORM, 0);
-    HIPCHK(launch_rmsnorm(x, B, s.hidden, h->L[0].attn_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+    HIPCHK(launch_resid_norm(nullptr, 0, B, s.hidden, x, nullptr, nullptr, s.rms_eps, nullptr, h->act_fmt,
+                             h->ssq, nullptr, st));
     for (int l = 0; l < s.n_layers; ++l) {
         const LayerW& W = h->L[l];
         const uint16_t* in = (l == 0) ? x : h->xbuf;
         uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
         float* dump = h->dump ? h->dump + (size_t)l * 2 * B * h->kv_dim : nullptr;
+        XIn xq;
+        xq.xf = XF_NORM;
+        xq.gain = W.attn_norm;
+        xq.ssq = h->ssq;
         h->prof.mark(FP_K_QKV, l);
-        if ((rc = run_skinny(h, h->act_in, W.qkv, B, 0, &ks, st))) return rc;
-        h->prof.mark(FP_K_ROPE_KV, l);
-        HIPCHK(launch_rope_kv(rope_args(h, l, h->part, ks, B, 1, h->d_pos, dump), st));
+        if ((rc = run_skinny(h, in, W.qkv, B, 0, xq, h->part, &ks, st))) return rc;
         AttnDecArgs ad{};
-        ad.q = h->q32;
+        ad.qkv_part = h->part;
+        ad.ks = ks;
+        ad.cos_t = h->cos_t;
+        ad.sin_t = h->sin_t;
+        ad.dump = dump;
         ad.kc = h->kc[l];
         ad.vc = h->vc[l];
         ad.k_scales = h->ksc[l];
@@ -409,23 +446,28 @@ fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_
         h->prof.mark(FP_K_ATTN, l);
         HIPCHK(launch_attn_decode(ad, B, st));
         h->prof.mark(FP_K_O, l);
-        if ((rc = run_skinny(h, h->act_o, W.o, B, 0, &ks, st))) return rc;
+        if ((rc = run_skinny(h, h->act_o, W.o, B, 0, XIn(), h->part, &ks, st))) return rc;
         h->prof.mark(FP_K_RESID_NORM, l);
-        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, W.mlp_norm, s.rms_eps, h->act_in,
-                                 h->act_fmt, st));
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, nullptr, s.rms_eps, nullptr, h->act_fmt,
+                                 h->ssq, nullptr, st));
+        XIn xg;
+        xg.xf = XF_NORM;
+        xg.gain = W.mlp_norm;
+        xg.ssq = h->ssq;
         h->prof.mark(FP_K_GATE_UP, l);
-        if ((rc = run_skinny(h, h->act_in, W.gu, B, s.ffn, &ks, st))) return rc;
-        h->prof.mark(FP_K_SWIGLU, l);
-        HIPCHK(launch_swiglu(h->part, ks, B, s.ffn, h->act_f, h->act_fmt, st));
+        if ((rc = run_skinny(h, h->hbuf, W.gu, B, s.ffn, xg, h->part2, &ks, st))) return rc;
+        XIn xd;
+        xd.xf = XF_SWIGLU;
+        xd.src_part = h->part2;
+        xd.src_ks = ks;
         h->prof.mark(FP_K_DOWN, l);
-        if ((rc = run_skinny(h, h->act_f, W.down, B, 0, &ks, st))) return rc;
-        const uint16_t* gnext = (l + 1 < s.n_layers) ? h->L[l + 1].attn_norm : nullptr;
+        if ((rc = run_skinny(h, nullptr, W.down, B, 0, xd, h->part, &ks, st))) return rc;
         h->prof.mark(FP_K_RESID_NORM, l);
-        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, gnext, s.rms_eps, h->act_in,
-                                 h->act_fmt, st));
+        // the last layer's epilogue also advances the position
+        int* incp = (l == s.n_layers - 1) ? h->d_pos : nullptr;
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, nullptr, s.rms_eps, nullptr, h->act_fmt,
+                                 h->ssq, incp, st));
     }
-    h->prof.mark(FP_K_POS, -1);
-    HIPCHK(launch_inc_pos(h->d_pos, st));
     h->prof.end();
     return FP_OK;
 }
@@ -538,10 +580,12 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     if ((st = alloc_t(h, &h->qkv32, Mmax * h->nqkv, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->q32, Mmax * h->q_dim, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->part2, (size_t)KSMAX * s.max_batch * 2 * F, &h->bytes_ws))) return bail(st);
     const size_t nch = attn_decode_chunks(s.max_seq);
     if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 2), &h->bytes_ws)))
         return bail(st);
     if ((st = alloc_t(h, &h->d_pos, 1, &h->bytes_ws))) return bail(st);
+    if ((st = alloc_t(h, &h->ssq, (size_t)s.max_batch * resid_ssq_blocks(H), &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->cos_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->sin_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return bail(st);
 
@@ -564,27 +608,27 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
 
     // weights
     uint16_t* tmp = nullptr;
+    void* tmpq = nullptr;
     size_t tmp_bytes = 0;
-    if (wq != FP_WQ_BF16) {
-        if ((st = alloc_t(h, &tmp, maxrows, &tmp_bytes))) return bail(st);
-    }
+    if ((st = alloc_t(h, &tmp, maxrows, &tmp_bytes))) return bail(st);
+    if ((st = dev_alloc(h, &tmpq, maxrows, &tmp_bytes))) return bail(st);
     for (int l = 0; l < s.n_layers; ++l) {
         LayerW& W = h->L[l];
         auto chk = [&](hipError_t e) { return e == hipSuccess ? FP_OK : fail(FP_ERR_HIP, "weight synthesis: %s", hipGetErrorString(e)); };
         if ((st = chk(launch_fill_bf16(W.attn_norm, H, stream_key(seed, l, FP_T_ATTN_NORM), 1.f, 0.02f, 0)))) return bail(st);
         if ((st = chk(launch_fill_bf16(W.mlp_norm, H, stream_key(seed, l, FP_T_MLP_NORM), 1.f, 0.02f, 0)))) return bail(st);
-        if ((st = synth_rows(h, &W.qkv, 0, h->q_dim, l, FP_T_Q, tmp))) return bail(st);
-        if ((st = synth_rows(h, &W.qkv, h->q_dim, h->kv_dim, l, FP_T_K, tmp))) return bail(st);
-        if ((st = synth_rows(h, &W.qkv, h->q_dim + h->kv_dim, h->kv_dim, l, FP_T_V, tmp))) return bail(st);
-        if ((st = synth_rows(h, &W.o, 0, H, l, FP_T_O, tmp))) return bail(st);
-        if ((st = synth_rows(h, &W.gu, 0, F, l, FP_T_GATE, tmp))) return bail(st);
-        if ((st = synth_rows(h, &W.gu, F, F, l, FP_T_UP, tmp))) return bail(st);
-        if ((st = synth_rows(h, &W.down, 0, H, l, FP_T_DOWN, tmp))) return bail(st);
+        if ((st = synth_rows(h, &W.qkv, 0, h->q_dim, l, FP_T_Q, tmp, tmpq))) return bail(st);
+        if ((st = synth_rows(h, &W.qkv, h->q_dim, h->kv_dim, l, FP_T_K, tmp, tmpq))) return bail(st);
+        if ((st = synth_rows(h, &W.qkv, h->q_dim + h->kv_dim, h->kv_dim, l, FP_T_V, tmp, tmpq))) return bail(st);
+        if ((st = synth_rows(h, &W.o, 0, H, l, FP_T_O, tmp, tmpq))) return bail(st);
+        if ((st = synth_rows(h, &W.gu, 0, F, l, FP_T_GATE, tmp, tmpq))) return bail(st);
+        if ((st = synth_rows(h, &W.gu, F, F, l, FP_T_UP, tmp, tmpq))) return bail(st);
+        if ((st = synth_rows(h, &W.down, 0, H, l, FP_T_DOWN, tmp, tmpq))) return bail(st);
     }
     if (hipDeviceSynchronize() != hipSuccess) return bail(fail(FP_ERR_HIP, "weight synthesis failed"));
-    if (tmp) {
-        (void)hipFree(tmp);
-        h->allocs.erase(std::find(h->allocs.begin(), h->allocs.end(), (void*)tmp));
+    for (void* p : {(void*)tmp, tmpq}) {
+        (void)hipFree(p);
+        h->allocs.erase(std::find(h->allocs.begin(), h->allocs.end(), p));
     }
     // zero the KV cache so exports of unwritten positions are deterministic
     for (int l = 0; l < s.n_layers; ++l) {
@@ -775,29 +819,41 @@ fp_status fp_export_weight(fp_layer* h, int32_t l, int32_t tensor, void* codes, 
     }
     const int K = m->K;
     HIPCHK(hipDeviceSynchronize());
-    if (h->wq == FP_WQ_BF16) {
-        HIPCHK(hipMemcpy(codes, (const uint16_t*)m->codes + (size_t)row0 * K, (size_t)n * K * 2, hipMemcpyDeviceToHost));
-        return FP_OK;
-    }
-    if (!scales) return fail(FP_ERR_INVALID_ARG, "scales is NULL");
+    if (h->wq != FP_WQ_BF16 && !scales) return fail(FP_ERR_INVALID_ARG, "scales is NULL");
+    if (h->wq == FP_WQ_INT4_G128 && !zeros) return fail(FP_ERR_INVALID_ARG, "zeros is NULL");
+    // fragment-major tiles -> row-major canonical layout
+    const int KS = weight_kstep(h->wq), eb = weight_ebits(h->wq);
+    const size_t blk_bytes = 1024, nblk = (size_t)(n / 16) * m->kst;
+    std::vector<uint8_t> tiles(nblk * blk_bytes);
+    HIPCHK(hipMemcpy(tiles.data(), (const uint8_t*)m->codes + (size_t)(row0 / 16) * m->kst * blk_bytes,
+                     tiles.size(), hipMemcpyDeviceToHost));
+    const size_t rowbytes = (size_t)K * eb / 8, chunk = 16;
+    uint8_t* dst = (uint8_t*)codes;
+    for (int nt = 0; nt < n / 16; ++nt)
+        for (int st = 0; st < m->kst; ++st)
+            for (int L = 0; L < 64; ++L) {
+                const int r = L & 15, g = L >> 4;
+                const int k0 = st * KS + g * (KS / 4);
+                if (k0 >= K) continue;
+                std::memcpy(dst + (size_t)(16 * nt + r) * rowbytes + (size_t)k0 * eb / 8,
+                            tiles.data() + ((size_t)nt * m->kst + st) * blk_bytes + (size_t)L * chunk, chunk);
+            }
+    if (h->wq == FP_WQ_BF16) return FP_OK;
     if (h->wq == FP_WQ_INT8_CHANNEL) {
-        HIPCHK(hipMemcpy(codes, (const int8_t*)m->codes + (size_t)row0 * K, (size_t)n * K, hipMemcpyDeviceToHost));
         HIPCHK(hipMemcpy(scales, m->scales + row0, (size_t)n * 2, hipMemcpyDeviceToHost));
         return FP_OK;
     }
-    if (!zeros) return fail(FP_ERR_INVALID_ARG, "zeros is NULL");
+    // int4: device nibble order -> canonical (nibble j holds column 8w + j)
+    uint32_t* wds = (uint32_t*)codes;
     const size_t words = (size_t)n * K / 8;
-    uint32_t* dst = (uint32_t*)codes;
-    HIPCHK(hipMemcpy(dst, (const uint32_t*)m->codes + (size_t)row0 * (K / 8), words * 4, hipMemcpyDeviceToHost));
-    // device nibble order -> canonical (nibble j holds column 8w + j)
     for (size_t i = 0; i < words; ++i) {
-        const uint32_t wv = dst[i];
+        const uint32_t wv = wds[i];
         uint32_t c = 0;
         for (int p = 0; p < 8; ++p) {
             const int col = (p < 4) ? 2 * p : 2 * (p - 4) + 1;
             c |= ((wv >> (4 * p)) & 0xFu) << (4 * col);
         }
-        dst[i] = c;
+        wds[i] = c;
     }
     HIPCHK(hipMemcpy(scales, m->scales + (size_t)row0 * (K / 128), (size_t)n * (K / 128) * 2, hipMemcpyDeviceToHost));
     HIPCHK(hipMemcpy(zeros, m->zeros + (size_t)row0 * (K / 128), (size_t)n * (K / 128) * 2, hipMemcpyDeviceToHost));

@@ -11,26 +11,47 @@ enum Epi { EPI_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 // weights (the fp16 copy of a bf16-rounded value is exact in fp16's normal range).
 enum ActFmt { ACT_BF16 = 0, ACT_F16 = 1 };
 
-// Decode skinny GEMM: part[s, m, col] = sum_{k in split s} X[m, k] W[col, k]
+// Weight rows per workgroup of the decode skinny GEMM = 64 * SKINNY_NS.
+#ifndef SKINNY_NS
+#define SKINNY_NS 2
+#endif
+
+// How the decode skinny GEMM forms its A operand while staging it in LDS.
+enum XForm {
+    XF_COPY = 0,     // A = X (activation format already)
+    XF_NORM = 1,     // A = act(bf16(X * r[m] * gain)), X bf16, r from ssq block sums
+    XF_SWIGLU = 2    // A = act(bf16(silu(G) * U)) from gate|up partial sums
+};
+
+// Decode skinny GEMM: part[s, m, col] = sum_{k in split s} A[m, k] W[col, k]
 // (times the row scale for int8).  W rows are output columns; dual_F > 0 selects
 // the SwiGLU tiling over the concatenated [gate; up] matrix of 2 * dual_F rows.
 struct SkinnyArgs {
-    const uint16_t* X;        // activations [M, K] (bf16 for bf16 weights, else fp16)
-    const void* W;            // bf16 [N, K] / int8 [N, K] / int4 words [N, K/8] (device order)
+    const uint16_t* X;        // XF_COPY: act [M, K]; XF_NORM: bf16 [M, K]
+    const void* W;            // fragment-major tiles (bf16 / int8 / int4 in device nibble order)
     const uint16_t* scales;   // fp16: int8 [N]; int4 [N, K/128]
     const uint16_t* zeros;    // fp16 [N, K/128] (int4)
     int M, N, K;
+    int kst;                  // K-steps per 16-row block row of W (ceil(K / KS))
     int dual_F;
     int krange;               // k per split (multiple of the format's K-step)
     float* part;              // [ks, M, N] fp32
+    int xf;                   // XForm
+    const uint16_t* gain;     // XF_NORM: bf16 [K]
+    const float* ssq;         // XF_NORM: [M, ssq_blocks] sums of squares of X rows
+    int ssq_blocks;
+    float eps;
+    const float* src_part;    // XF_SWIGLU: [src_ks, M, 2K] gate|up partial sums
+    int src_ks;
 };
 
 struct GemmArgs {
     const uint16_t* X;        // activations [M, K]
-    const void* W;
+    const void* W;            // fragment-major tiles
     const uint16_t* scales;
     const uint16_t* zeros;
     int M, N, K, F;           // F: SwiGLU width (N = 2F rows of [gate; up])
+    int kst;                  // K-steps per 16-row block row of W
     float* out32;             // EPI_F32: [M, N]
     uint16_t* out16;          // EPI_RESID: bf16 [M, N]; EPI_SWIGLU: act [M, F]
     const uint16_t* resid;    // EPI_RESID: bf16 [M, N]
@@ -54,11 +75,17 @@ struct RopeKvArgs {
 };
 
 struct AttnDecArgs {
-    const float* q;           // [B, nh*d] rotated queries
-    const void* kc;           // layer cache [B, nkv, max_seq, d]
-    const void* vc;
-    const uint16_t* k_scales; // [B, nkv, max_seq] (int8)
-    const uint16_t* v_scales;
+    // q|k|v of the new tokens as split-K partial sums [ks, B, (nh + 2 nkv) d], before the
+    // rotary embedding; the kernel rotates q and k and appends k, v to the cache
+    const float* qkv_part;
+    int ks;
+    const float* cos_t;       // [max_seq, d/2]
+    const float* sin_t;
+    float* dump;              // NULL or [2, B, nkv, d] pre-quantisation K, V
+    void* kc;                 // layer cache [B, nkv, max_seq, d]
+    void* vc;
+    uint16_t* k_scales;       // [B, nkv, max_seq] (int8)
+    uint16_t* v_scales;
     int kv_int8, nh, nkv, d, max_seq;
     const int* d_pos;         // current position (the new token's index)
     float scale;              // float32(1/sqrt(d))
@@ -81,6 +108,10 @@ struct AttnPreArgs {
 
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint64_t key, float mean, float sigma,
                             hipStream_t st);
+// Fragment-major weight layout (see tile_kernel): KS = k per 1 KiB block row-slice.
+inline int weight_kstep(int wf) { return wf == W_BF16 ? 32 : (wf == W_INT8 ? 64 : 128); }
+inline int weight_ebits(int wf) { return wf == W_BF16 ? 16 : (wf == W_INT8 ? 8 : 4); }
+hipError_t launch_tile(const void* src, int n, int K, int ebits, int KS, void* dst, int row0, hipStream_t st);
 hipError_t launch_quant_int8(const uint16_t* w, int N, int K, int8_t* codes, uint16_t* scales,
                              hipStream_t st);
 hipError_t launch_quant_int4(const uint16_t* w, int N, int K, uint32_t* codes, uint16_t* scales,
@@ -88,9 +119,14 @@ hipError_t launch_quant_int4(const uint16_t* w, int N, int K, uint32_t* codes, u
 
 hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, float eps, uint16_t* out,
                           int out_fmt, hipStream_t st);
+// Decode epilogue: out = bf16(resid + sum of ks partials) (skipped when ks == 0: the
+// row is resid itself); then, if g != NULL, nout = act(bf16(row * rsqrt(mean(row^2) + eps) * g)).
+// ssq: scratch of M * resid_ssq_blocks(N) floats.  inc_pos (optional): position counter
+// the kernel increments once after its work.
 hipError_t launch_resid_norm(const float* part, int ks, int M, int N, const uint16_t* resid,
                              uint16_t* out, const uint16_t* g, float eps, uint16_t* nout, int nfmt,
-                             hipStream_t st);
+                             float* ssq, int* inc_pos, hipStream_t st);
+int resid_ssq_blocks(int N);
 hipError_t launch_swiglu(const float* part, int ks, int M, int F, uint16_t* a, int afmt,
                          hipStream_t st);
 hipError_t launch_rope_kv(const RopeKvArgs& a, hipStream_t st);
@@ -98,6 +134,8 @@ hipError_t launch_set_pos(int* d_pos, int v, hipStream_t st);
 hipError_t launch_inc_pos(int* d_pos, hipStream_t st);
 
 int skinny_kstep(int wf);
+int skinny_max_krange(int M);
+int skinny_tiles(int N, int dual_F);
 hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st);
 

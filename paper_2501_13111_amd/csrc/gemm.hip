@@ -13,6 +13,9 @@
 // out = bf16(resid + acc), and SwiGLU a = bf16(silu(gate) * up) where each wave
 // holds gate and up columns of the same f (dual tiles over [gate; up]).
 //
+// Weights are read from the fragment-major layout (1 KiB blocks of 16 rows x one
+// K-step), so each 64-thread group of a tile load reads contiguous memory.
+//
 // Tile 128 x 128 x 64, 4 waves in 2 x 2, each wave 64 x 64 = 4 x 4 MFMA 16x16x32
 // tiles; the next K tile is loaded into registers while the current one is
 // multiplied out of LDS.
@@ -63,38 +66,46 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
             ra[i] = u32x4{0u, 0u, 0u, 0u};
             if (m < a.M && k < a.K) ra[i] = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
         }
+        // B: fragment-major tiles -- each 64-thread group reads one contiguous 1 KiB block
+        // (16 rows x one K-step); chunk L = r + 16 g holds row r, k-slice g of the block.
+        const u32x4* Wt = (const u32x4*)a.W;
         if constexpr (WF == W_BF16) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < 4; ++i) {                  // 8 subtiles x 2 K-steps of 32
                 const int c = tid + 256 * i;
-                const int lr = c >> 3, kc = (c & 7) * 8;
+                const int blk = c >> 6, L = c & 63, ntl = blk >> 1, kst = blk & 1;
+                const int lr = 16 * ntl + (L & 15);
                 bool v;
                 const int n = brow(lr, v);
+                const int kabs = k0 + 32 * kst;
                 rb[i] = u32x4{0u, 0u, 0u, 0u};
-                if (v && k0 + kc < a.K)
-                    rb[i] = *(const u32x4*)((const uint16_t*)a.W + (int64_t)n * a.K + k0 + kc);
+                if (v && kabs + 8 * (L >> 4) < a.K)
+                    rb[i] = Wt[((int64_t)(n >> 4) * a.kst + kabs / 32) * 64 + L];
             }
         } else if constexpr (WF == W_INT8) {
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
+            for (int i = 0; i < 2; ++i) {                  // 8 subtiles x 1 K-step of 64
                 const int c = tid + 256 * i;
-                const int lr = c >> 2, kc = (c & 3) * 16;
+                const int ntl = c >> 6, L = c & 63;
+                const int lr = 16 * ntl + (L & 15);
                 bool v;
                 const int n = brow(lr, v);
                 rb[i] = u32x4{0u, 0u, 0u, 0u};
-                if (v && k0 + kc < a.K)
-                    rb[i] = *(const u32x4*)((const int8_t*)a.W + (int64_t)n * a.K + k0 + kc);
+                if (v && k0 + 16 * (L >> 4) < a.K)
+                    rb[i] = Wt[((int64_t)(n >> 4) * a.kst + k0 / 64) * 64 + L];
             }
-        } else {
-            const int lr = tid >> 1, kc = (tid & 1) * 32;
+        } else {                                           // 8 subtiles x half a K-step of 128
+            const int ntl = tid >> 5, j = tid & 31;
+            const int lr = 16 * ntl + (j & 15);
+            const int gg = j >> 4, g = gg + 2 * ((k0 >> 6) & 1);
             bool v;
             const int n = brow(lr, v);
             rb[0] = u32x4{0u, 0u, 0u, 0u};
             bs_scale = 0.f;
             bs_zero = 0.f;
-            if (v && k0 + kc < a.K) {
-                rb[0] = *(const u32x4*)((const uint32_t*)a.W + (int64_t)n * (a.K / 8) + (k0 + kc) / 8);
-                const int grp = (k0 + kc) / 128;
+            if (v && k0 < a.K) {
+                rb[0] = Wt[((int64_t)(n >> 4) * a.kst + k0 / 128) * 64 + (j & 15) + 16 * g];
+                const int grp = k0 / 128;
                 bs_scale = h2f(a.scales[(int64_t)n * (a.K / 128) + grp]);
                 bs_zero = h2f(a.zeros[(int64_t)n * (a.K / 128) + grp]);
             }
@@ -110,20 +121,22 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int c = tid + 256 * i;
-                *(u32x4*)(Bs + (c >> 3) * GLD + (c & 7) * 8) = rb[i];
+                const int blk = c >> 6, L = c & 63;
+                *(u32x4*)(Bs + (16 * (blk >> 1) + (L & 15)) * GLD + 32 * (blk & 1) + 8 * (L >> 4)) = rb[i];
             }
         } else if constexpr (WF == W_INT8) {
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
                 const int c = tid + 256 * i;
-                uint16_t* dst = Bs + (c >> 2) * GLD + (c & 3) * 16;
+                const int L = c & 63;
+                uint16_t* dst = Bs + (16 * (c >> 6) + (L & 15)) * GLD + 16 * (L >> 4);
                 const u32x2 c0 = i8x4_to_f16x4(rb[i].x), c1 = i8x4_to_f16x4(rb[i].y);
                 const u32x2 c2 = i8x4_to_f16x4(rb[i].z), c3 = i8x4_to_f16x4(rb[i].w);
                 *(u32x4*)(dst) = u32x4{c0.x, c0.y, c1.x, c1.y};
                 *(u32x4*)(dst + 8) = u32x4{c2.x, c2.y, c3.x, c3.y};
             }
         } else {
-            uint16_t* dst = Bs + (tid >> 1) * GLD + (tid & 1) * 32;
+            uint16_t* dst = Bs + (16 * (tid >> 5) + (tid & 15)) * GLD + 32 * ((tid >> 4) & 1);
             const _Float16 bz = (_Float16)(1024.0f + bs_zero);
             const f16x2 bias = {bz, bz};
             const _Float16 sh = (_Float16)bs_scale;

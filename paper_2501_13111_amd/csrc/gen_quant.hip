@@ -98,6 +98,41 @@ __global__ void __launch_bounds__(256) quant_int4_kernel(const uint16_t* __restr
     }
 }
 
+// Row-major [n, K] codes (n % 16 == 0) -> fragment-major tiles of the destination
+// matrix starting at row row0: block (row / 16, k / KS) of 1024 bytes holds, for lane
+// L = r + 16 g, the 16 bytes of row 16 * (row / 16) + r covering k in
+// [KS * step + g * KS / 4, + KS / 4).  Columns beyond K (padding up to a multiple
+// of KS) are zero.  ebits: element size in bits (16, 8 or 4).
+__global__ void __launch_bounds__(256) tile_kernel(const uint8_t* __restrict__ src, int n, int K, int ebits,
+                                                   int KS, uint8_t* __restrict__ dst, int row0) {
+    const int nst = (K + KS - 1) / KS;
+    const int64_t total = (int64_t)(n / 16) * nst * 64;
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= total) return;
+    const int L = (int)(c % 64);
+    const int64_t blk = c / 64;
+    const int step = (int)(blk % nst);
+    const int ntl = (int)(blk / nst);
+    const int r = L & 15, g = L >> 4;
+    const int row = ntl * 16 + r;
+    const int k0 = step * KS + g * (KS / 4);
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (k0 < K) {
+        const int64_t rowbytes = (int64_t)K * ebits / 8;
+        v = *(const u32x4*)(src + row * rowbytes + (int64_t)k0 * ebits / 8);
+    }
+    const int64_t nt = row0 / 16 + ntl;
+    *(u32x4*)(dst + ((nt * nst + step) * 64 + L) * 16) = v;
+}
+
+hipError_t launch_tile(const void* src, int n, int K, int ebits, int KS, void* dst, int row0, hipStream_t st) {
+    const int nst = (K + KS - 1) / KS;
+    const int64_t total = (int64_t)(n / 16) * nst * 64;
+    hipLaunchKernelGGL(tile_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
+                       (const uint8_t*)src, n, K, ebits, KS, (uint8_t*)dst, row0);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint64_t key, float mean, float sigma,
                             hipStream_t st) {
     if (n <= 0) return hipSuccess;

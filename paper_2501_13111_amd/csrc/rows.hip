@@ -35,30 +35,46 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------- residual epilogue
-// out = bf16(resid + sum_s part[s]) for one row; then optionally the next RMSNorm of
-// that row: nout = act(bf16(out * r * g)).  part: [ks, M, N] fp32.
-__global__ void __launch_bounds__(256) resid_norm_kernel(const float* __restrict__ part, int ks, int M,
-                                                          int N, const uint16_t* __restrict__ resid,
-                                                          uint16_t* __restrict__ out,
-                                                          const uint16_t* __restrict__ g, float eps,
-                                                          uint16_t* __restrict__ nout, int nfmt) {
+// Decode rows are few (one per sequence), so the row-wise work is spread over column
+// blocks of RB values: resid_ssq writes out = bf16(resid + sum_s part[s]) for its block
+// and the block's sum of squares; norm_apply then forms r = 1/sqrt(mean + eps) from the
+// row's block sums (fixed order) and writes act(bf16(out * r * g)).  With ks == 0 the
+// first kernel only sums squares of resid (the RMSNorm of a layer input).
+constexpr int RB = 256;
+
+__global__ void __launch_bounds__(256) resid_ssq_kernel(const float* __restrict__ part, int ks, int M,
+                                                         int N, const uint16_t* __restrict__ resid,
+                                                         uint16_t* __restrict__ out,
+                                                         float* __restrict__ ssq, int* __restrict__ d_pos) {
     __shared__ float red[16];
-    extern __shared__ float rowbuf[];
-    const int64_t m = blockIdx.x;
+    const int64_t m = blockIdx.y;
+    const int n0 = blockIdx.x * RB;
     float ss = 0.f;
-    for (int n = threadIdx.x; n < N; n += blockDim.x) {
-        float acc = 0.f;
-        for (int s = 0; s < ks; ++s) acc += part[((int64_t)s * M + m) * N + n];
-        const float v = bfround(bf2f(resid[m * (int64_t)N + n]) + acc);
-        out[m * (int64_t)N + n] = f2bf(v);
-        rowbuf[n] = v;
+    for (int n = n0 + threadIdx.x; n < min(N, n0 + RB); n += blockDim.x) {
+        float v = bf2f(resid[m * (int64_t)N + n]);
+        if (ks > 0) {
+            v = bfround(v + sum_parts(part + m * (int64_t)N + n, ks, (int64_t)M * N));
+            out[m * (int64_t)N + n] = f2bf(v);
+        }
         ss += v * v;
     }
-    if (g == nullptr) return;
     ss = block_sum(ss, red);
+    if (threadIdx.x == 0) ssq[m * gridDim.x + blockIdx.x] = ss;
+    // the step's last kernel advances the decode position (every reader has run)
+    if (d_pos && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *d_pos += 1;
+}
+
+__global__ void __launch_bounds__(256) norm_apply_kernel(const uint16_t* __restrict__ y, int N,
+                                                          const float* __restrict__ ssq, int nblk,
+                                                          const uint16_t* __restrict__ g, float eps,
+                                                          uint16_t* __restrict__ nout, int nfmt) {
+    const int64_t m = blockIdx.y;
+    float ss = 0.f;
+    for (int b = 0; b < nblk; ++b) ss += ssq[m * nblk + b];
     const float r = 1.0f / __fsqrt_rn(ss / (float)N + eps);
-    for (int n = threadIdx.x; n < N; n += blockDim.x)
-        nout[m * (int64_t)N + n] = act_store(bfround(rowbuf[n] * r * bf2f(g[n])), nfmt);
+    const int n0 = blockIdx.x * RB;
+    for (int n = n0 + threadIdx.x; n < min(N, n0 + RB); n += blockDim.x)
+        nout[m * (int64_t)N + n] = act_store(bfround(bf2f(y[m * (int64_t)N + n]) * r * bf2f(g[n])), nfmt);
 }
 
 // ---------------------------------------------------------------- SwiGLU epilogue
@@ -68,12 +84,8 @@ __global__ void __launch_bounds__(256) swiglu_kernel(const float* __restrict__ p
     const int64_t m = blockIdx.y;
     const int f = blockIdx.x * blockDim.x + threadIdx.x;
     if (f >= F) return;
-    float gs = 0.f, us = 0.f;
-    for (int s = 0; s < ks; ++s) {
-        const float* p = part + ((int64_t)s * M + m) * (2 * (int64_t)F);
-        gs += p[f];
-        us += p[F + f];
-    }
+    const float gs = sum_parts(part + m * (2 * (int64_t)F) + f, ks, (int64_t)M * 2 * F);
+    const float us = sum_parts(part + m * (2 * (int64_t)F) + F + f, ks, (int64_t)M * 2 * F);
     a[m * (int64_t)F + f] = act_store(bfround(silu_f(gs) * us), afmt);
 }
 
@@ -102,11 +114,7 @@ __global__ void __launch_bounds__(64) rope_kv_kernel(const float* __restrict__ p
     const int Nqkv = (nh + 2 * nkv) * d;
     const int b = m / T;
     const int pos = (d_pos ? *d_pos : 0) + (m % T);
-    auto load = [&](int col) {
-        float acc = 0.f;
-        for (int s = 0; s < ks; ++s) acc += part[((int64_t)s * M + m) * Nqkv + col];
-        return acc;
-    };
+    auto load = [&](int col) { return sum_parts(part + (int64_t)m * Nqkv + col, ks, (int64_t)M * Nqkv); };
     const float* cr = cos_t + (int64_t)pos * half;
     const float* sr = sin_t + (int64_t)pos * half;
     if (slot < nh) {
@@ -186,11 +194,18 @@ hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, fl
 
 hipError_t launch_resid_norm(const float* part, int ks, int M, int N, const uint16_t* resid,
                              uint16_t* out, const uint16_t* g, float eps, uint16_t* nout, int nfmt,
-                             hipStream_t st) {
-    hipLaunchKernelGGL(resid_norm_kernel, dim3(M), dim3(256), N * sizeof(float), st, part, ks, M, N,
-                       resid, out, g, eps, nout, nfmt);
+                             float* ssq, int* inc_pos, hipStream_t st) {
+    const int nblk = (N + RB - 1) / RB;
+    hipLaunchKernelGGL(resid_ssq_kernel, dim3(nblk, M), dim3(256), 0, st, part, ks, M, N, resid, out, ssq,
+                       inc_pos);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || g == nullptr) return e;
+    const uint16_t* y = ks > 0 ? out : resid;
+    hipLaunchKernelGGL(norm_apply_kernel, dim3(nblk, M), dim3(256), 0, st, y, N, ssq, nblk, g, eps, nout, nfmt);
     return hipGetLastError();
 }
+
+int resid_ssq_blocks(int N) { return (N + RB - 1) / RB; }
 
 hipError_t launch_swiglu(const float* part, int ks, int M, int F, uint16_t* a, int afmt,
                          hipStream_t st) {

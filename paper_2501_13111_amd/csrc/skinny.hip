@@ -1,27 +1,40 @@
-// Decode projections: weight-streaming skinny GEMM  part[s] = X[M, K] . W[N, K]^T
+// Decode projections: weight-streaming skinny GEMM  part[s] = A[M, K] . W[N, K]^T
 // over the split-K range s, for M <= 64 tokens (one per sequence in the batch).
 //
 // Decode is where the fingerprint's per-token time goes (TPOT, paper Sec. 5.3):
 // every step streams all weights once, so the kernel is bound by HBM bandwidth.
 // Weight-only quantisation (Sec. 3.2) shrinks those bytes; the cost the paper
 // points at is converting the codes back to 16-bit values for the arithmetic.
-// Here the codes go straight from a 128-bit load into fp16 MFMA operands with a
-// few integer ops per dword:
-//   bf16   W: 16 B per lane = 8 weights  -> 1 MFMA  (bf16 x bf16)
-//   int8   W: 16 B per lane = 16 weights -> 2 MFMAs (fp16 x exact fp16 codes),
-//             per-row scale applied once at the end
-//   int4   W: 16 B per lane = 32 weights = one 128-group of a row (4 lanes) ->
-//             4 MFMAs on exact (q - z), then acc += s * group sum
+// Here the codes go straight from a 128-bit load into MFMA operands with a few
+// integer ops per dword:
+//   bf16  W: 16 B per lane = 8 weights  -> 1 MFMA  (bf16 x bf16)
+//   int8  W: 16 B per lane = 16 weights -> 2 MFMAs (fp16 x exact fp16 codes); the
+//            row scale is applied once at the end
+//   int4  W: 16 B per lane = 32 weights = a quarter of one 128-group of a row ->
+//            4 MFMAs on fp16((q - z) * s)
 // MFMA 16x16x32 layout: lane l supplies row (l % 16) of A and column (l % 16) of
 // B, each with 8 consecutive k from the lane's k-slice (l / 16); the output lane
-// holds C[4 (l/16) + i][l % 16].  A and B use the same k assignment, so any
-// permutation of k inside a K-step is allowed; the int4 nibble order on the
-// device is chosen so that pairs of nibbles come out as consecutive k.
+// holds C[4 (l/16) + i][l % 16].  A and B use the same k assignment, so the order
+// of k inside a K-step is free; the int4 nibble order on the device makes nibble
+// pairs come out as consecutive k.
 //
-// Workgroup = 4 waves over one 32-row tile (two 16-row subtiles) and one split-K
-// range; the waves interleave K-steps and are summed through LDS.  In "dual"
-// mode (SwiGLU) subtile 0 reads gate rows f and subtile 1 up rows F + f of the
-// concatenated [gate; up] matrix, so one tile covers 16 values of f.
+// Weights are stored fragment-major: the 64 lanes' 16-byte operands of one 16-row
+// subtile and one K-step form a contiguous 1 KiB block, and a row of blocks runs
+// along K, so every wave-wide load reads 1 KiB of contiguous memory and each wave
+// streams long contiguous runs.  The loads are non-temporal: each weight is read once
+// per step.
+//
+// Workgroup = 4 waves; each wave owns NS subtiles of 16 weight rows and streams
+// them over the workgroup's K-range with UNR K-steps of loads in flight (double
+// buffered in registers).  The activation slice A[:, K-range] is staged once in
+// LDS, transformed on the way in:
+//   XF_COPY   A = X                                   (attention output)
+//   XF_NORM   A = bf16(y * rsqrt(mean(y^2) + eps) * g) (RMSNorm of the layer input
+//             or of h; the row's sum of squares comes as block sums)
+//   XF_SWIGLU A = bf16(silu(gate) * up) from the gate|up partial sums
+// so the normalisation and the activation never run as kernels of their own.
+// In dual mode (the [gate; up] matrix) the first NS/2 subtiles of a wave read gate
+// rows f and the others up rows F + f of the same f.
 #include "fp_device.h"
 #include "fp_internal.h"
 
@@ -33,195 +46,245 @@ template <> struct SkinnyTraits<W_BF16> { static constexpr int KS = 32; static c
 template <> struct SkinnyTraits<W_INT8> { static constexpr int KS = 64; static constexpr int NJ = 2; };
 template <> struct SkinnyTraits<W_INT4> { static constexpr int KS = 128; static constexpr int NJ = 4; };
 
-template <int WF, int MT, int UNR>
+constexpr int SK_LDS_ELEMS = 31744;   // u16 elements of the staged activation slice (62 KiB)
+constexpr int SK_PAD = 8;
+
+template <int WF, int MT, int NS, int UNR, int XF>
 __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
     constexpr int KS = SkinnyTraits<WF>::KS;
     constexpr int NJ = SkinnyTraits<WF>::NJ;
-    constexpr int KL = KS / 4;   // k per lane group in one K-step
+    constexpr int KL = KS / 4;                       // k per lane group in one K-step
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
-    __shared__ f32x4 red[3][MT][2][64];
+    extern __shared__ __attribute__((aligned(16))) uint16_t As[];
+    __shared__ float rrow[64];
 
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
-    const int tb = blockIdx.x, sp = blockIdx.y;
+    const int sp = blockIdx.y;
     const int kb = sp * a.krange;
     const int ke = min(a.K, kb + a.krange);
+    const int klen = ke - kb;
+    const int ld = a.krange + SK_PAD;               // LDS row stride (u16)
 
-    int row[2];
-    bool rv[2];
+    // ---- rows of this wave's subtiles
+    int row[NS];
+    bool rv[NS];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int s = 0; s < NS; ++s) {
         if (a.dual_F > 0) {
-            const int f = tb * 16 + r;
+            const int fw = blockIdx.x * (32 * NS) + w * (8 * NS);
+            const int f = fw + 16 * (s % (NS / 2)) + r;
             rv[s] = f < a.dual_F;
-            row[s] = s * a.dual_F + f;
+            row[s] = (s < NS / 2 ? 0 : a.dual_F) + f;
         } else {
-            row[s] = tb * 32 + 16 * s + r;
+            row[s] = blockIdx.x * (64 * NS) + w * (16 * NS) + 16 * s + r;
             rv[s] = row[s] < a.N;
         }
     }
 
-    f32x4 acc[MT][2];
+    // ---- weight loads of one K-step
+    auto load_w = [&](int kk, u32x4* dst) {
 #pragma unroll
-    for (int t = 0; t < MT; ++t)
-#pragma unroll
-        for (int s = 0; s < 2; ++s) acc[t][s] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    bool mv[MT];
-    const uint16_t* xrow[MT];
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-        mv[t] = (16 * t + r) < a.M;
-        xrow[t] = a.X + (int64_t)(mv[t] ? 16 * t + r : 0) * a.K;
-    }
-
-    for (int k0 = kb + w * KS; k0 < ke; k0 += 4 * KS * UNR) {
-        u32x4 wv[UNR][2];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            const int kk = k0 + u * 4 * KS;
-#pragma unroll
-            for (int s = 0; s < 2; ++s) {
-                wv[u][s] = u32x4{0u, 0u, 0u, 0u};
-                if (rv[s] && kk + KL * g < ke) {
-                    if constexpr (WF == W_BF16) {
-                        wv[u][s] = *(const u32x4*)((const uint16_t*)a.W + (int64_t)row[s] * a.K + kk + 8 * g);
-                    } else if constexpr (WF == W_INT8) {
-                        wv[u][s] = *(const u32x4*)((const int8_t*)a.W + (int64_t)row[s] * a.K + kk + 16 * g);
-                    } else {
-                        wv[u][s] = *(const u32x4*)((const uint32_t*)a.W + (int64_t)row[s] * (a.K / 8) + (kk + 32 * g) / 8);
-                    }
-                }
-            }
+        for (int s = 0; s < NS; ++s) {
+            dst[s] = u32x4{0u, 0u, 0u, 0u};
+            if (rv[s] && kk < ke)   // one 1 KiB block per wave: 16 rows x one K-step
+                dst[s] = __builtin_nontemporal_load((const u32x4*)a.W + ((int64_t)(row[s] >> 4) * a.kst + kk / KS) * 64 + lane);
         }
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            const int kk = k0 + u * 4 * KS;
-            if (kk >= ke) break;
-            // B operands (dequantised weights) for the NJ MFMAs of this K-step
-            u32x4 bop[NJ][2];
-            float gscale[2];
-#pragma unroll
-            for (int s = 0; s < 2; ++s) {
-                if constexpr (WF == W_BF16) {
-                    bop[0][s] = wv[u][s];
-                } else if constexpr (WF == W_INT8) {
-                    const u32x2 c0 = i8x4_to_f16x4(wv[u][s].x), c1 = i8x4_to_f16x4(wv[u][s].y);
-                    const u32x2 c2 = i8x4_to_f16x4(wv[u][s].z), c3 = i8x4_to_f16x4(wv[u][s].w);
-                    bop[0][s] = u32x4{c0.x, c0.y, c1.x, c1.y};
-                    bop[1][s] = u32x4{c2.x, c2.y, c3.x, c3.y};
-                } else {
-                    const int grp = kk / 128;
-                    float sc = 0.f, zz = 0.f;
-                    if (rv[s]) {
-                        sc = h2f(a.scales[(int64_t)row[s] * (a.K / 128) + grp]);
-                        zz = h2f(a.zeros[(int64_t)row[s] * (a.K / 128) + grp]);
-                    }
-                    gscale[s] = sc;
-                    const _Float16 bz = (_Float16)(1024.0f + zz);
-                    const f16x2 bias = {bz, bz};
-                    bop[0][s] = i4x8_to_f16x8(wv[u][s].x, bias);
-                    bop[1][s] = i4x8_to_f16x8(wv[u][s].y, bias);
-                    bop[2][s] = i4x8_to_f16x8(wv[u][s].z, bias);
-                    bop[3][s] = i4x8_to_f16x8(wv[u][s].w, bias);
-                }
-            }
-            f32x4 tmp[MT][2];
-            if constexpr (WF == W_INT4) {
-#pragma unroll
-                for (int t = 0; t < MT; ++t)
-#pragma unroll
-                    for (int s = 0; s < 2; ++s) tmp[t][s] = f32x4{0.f, 0.f, 0.f, 0.f};
-            }
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                // k-offset of this MFMA's 8 values for lane group g
-                int koff;
-                if constexpr (WF == W_BF16) koff = kk + 8 * g;
-                else if constexpr (WF == W_INT8) koff = kk + 16 * g + 8 * j;
-                else koff = kk + 32 * g + 8 * j;
-                const bool kin = kk + KL * g < ke;
-#pragma unroll
-                for (int t = 0; t < MT; ++t) {
-                    u32x4 av = u32x4{0u, 0u, 0u, 0u};
-                    if (mv[t] && kin) av = *(const u32x4*)(xrow[t] + koff);
-#pragma unroll
-                    for (int s = 0; s < 2; ++s) {
-                        if constexpr (WF == W_INT4) tmp[t][s] = mfma16<AF>(av, bop[j][s], tmp[t][s]);
-                        else acc[t][s] = mfma16<AF>(av, bop[j][s], acc[t][s]);
-                    }
-                }
-            }
-            if constexpr (WF == W_INT4) {
-#pragma unroll
-                for (int t = 0; t < MT; ++t)
-#pragma unroll
-                    for (int s = 0; s < 2; ++s) acc[t][s] += gscale[s] * tmp[t][s];
-            }
-        }
-    }
+    };
 
-    // sum the four waves' partial sums through LDS
-    if (w > 0) {
+    u32x4 wa[UNR][NS], wb[UNR][NS];
 #pragma unroll
-        for (int t = 0; t < MT; ++t)
+    for (int u = 0; u < UNR; ++u) load_w(kb + u * KS, wa[u]);
+
+    // ---- stage the activation slice (with its transform) into LDS
+    if constexpr (XF == XF_NORM) {
+        if (tid < a.M) {
+            float ss = 0.f;
+            for (int b = 0; b < a.ssq_blocks; ++b) ss += a.ssq[tid * a.ssq_blocks + b];
+            rrow[tid] = 1.0f / __fsqrt_rn(ss / (float)a.K + a.eps);
+        }
+        __syncthreads();
+    }
+    {
+        const int chunks = klen / 8;                 // 8-element chunks per row
+        for (int c = tid; c < a.M * chunks; c += 256) {
+            const int m = c / chunks, kc = (c % chunks) * 8;
+            const int k = kb + kc;
+            uint32_t o[4];
+            if constexpr (XF == XF_COPY) {
+                const u32x4 v = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+                o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+            } else if constexpr (XF == XF_NORM) {
+                const u32x4 v = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+                const u32x4 gg = *(const u32x4*)(a.gain + k);
+                const uint32_t vv[4] = {v.x, v.y, v.z, v.w}, gv[4] = {gg.x, gg.y, gg.z, gg.w};
+                const float rm = rrow[m];
 #pragma unroll
-            for (int s = 0; s < 2; ++s) red[w - 1][t][s][lane] = acc[t][s];
+                for (int j = 0; j < 4; ++j) {
+                    const float e0 = bfround(__uint_as_float(vv[j] << 16) * rm * __uint_as_float(gv[j] << 16));
+                    const float e1 = bfround(__uint_as_float(vv[j] & 0xFFFF0000u) * rm * __uint_as_float(gv[j] & 0xFFFF0000u));
+                    o[j] = (uint32_t)act_store(e0, AF) | ((uint32_t)act_store(e1, AF) << 16);
+                }
+            } else {   // XF_SWIGLU: k indexes f; partials [src_ks, M, 2F]
+                const int F = a.K;
+                float gs[8], us[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) { gs[j] = 0.f; us[j] = 0.f; }
+                for (int s = 0; s < a.src_ks; ++s) {
+                    const float* p = a.src_part + ((int64_t)s * a.M + m) * (2 * (int64_t)F);
+                    const float4 g0 = *(const float4*)(p + k), g1 = *(const float4*)(p + k + 4);
+                    const float4 u0 = *(const float4*)(p + F + k), u1 = *(const float4*)(p + F + k + 4);
+                    gs[0] += g0.x; gs[1] += g0.y; gs[2] += g0.z; gs[3] += g0.w;
+                    gs[4] += g1.x; gs[5] += g1.y; gs[6] += g1.z; gs[7] += g1.w;
+                    us[0] += u0.x; us[1] += u0.y; us[2] += u0.z; us[3] += u0.w;
+                    us[4] += u1.x; us[5] += u1.y; us[6] += u1.z; us[7] += u1.w;
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    o[j] = (uint32_t)act_store(bfround(silu_f(gs[2 * j]) * us[2 * j]), AF) |
+                           ((uint32_t)act_store(bfround(silu_f(gs[2 * j + 1]) * us[2 * j + 1]), AF) << 16);
+            }
+            *(u32x4*)(As + m * ld + kc) = u32x4{o[0], o[1], o[2], o[3]};
+        }
     }
     __syncthreads();
-    if (w != 0) return;
+
+    // ---- stream the weights
+    f32x4 acc[MT][NS];
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
-            acc[t][s] += red[0][t][s][lane] + red[1][t][s][lane] + red[2][t][s][lane];
+        for (int s = 0; s < NS; ++s) acc[t][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bool mv[MT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) mv[t] = (16 * t + r) < a.M;
 
+    auto compute = [&](int kk, const u32x4* wv) {
+        if (kk >= ke) return;
+        const bool kin = kk + KL * g < ke;
+        u32x4 bop[NJ][NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            if constexpr (WF == W_BF16) {
+                bop[0][s] = wv[s];
+            } else if constexpr (WF == W_INT8) {
+                const u32x2 c0 = i8x4_to_f16x4(wv[s].x), c1 = i8x4_to_f16x4(wv[s].y);
+                const u32x2 c2 = i8x4_to_f16x4(wv[s].z), c3 = i8x4_to_f16x4(wv[s].w);
+                bop[0][s] = u32x4{c0.x, c0.y, c1.x, c1.y};
+                bop[1][s] = u32x4{c2.x, c2.y, c3.x, c3.y};
+            } else {
+                const int grp = kk / 128;
+                float sc = 0.f, zz = 0.f;
+                if (rv[s]) {
+                    sc = h2f(a.scales[(int64_t)row[s] * (a.K / 128) + grp]);
+                    zz = h2f(a.zeros[(int64_t)row[s] * (a.K / 128) + grp]);
+                }
+                const _Float16 bz = (_Float16)(1024.0f + zz);
+                const f16x2 bias = {bz, bz};
+                const _Float16 sh = (_Float16)sc;
+                const f16x2 s2 = {sh, sh};
+                const uint32_t wd[4] = {wv[s].x, wv[s].y, wv[s].z, wv[s].w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const u32x4 q = i4x8_to_f16x8(wd[j], bias);
+                    bop[j][s] = u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            int koff;
+            if constexpr (WF == W_BF16) koff = kk + 8 * g;
+            else if constexpr (WF == W_INT8) koff = kk + 16 * g + 8 * j;
+            else koff = kk + 32 * g + 8 * j;
+#pragma unroll
+            for (int t = 0; t < MT; ++t) {
+                u32x4 av = u32x4{0u, 0u, 0u, 0u};
+                if (mv[t] && kin) av = *(const u32x4*)(As + (16 * t + r) * ld + (koff - kb));
+#pragma unroll
+                for (int s = 0; s < NS; ++s) acc[t][s] = mfma16<AF>(av, bop[j][s], acc[t][s]);
+            }
+        }
+    };
+
+    for (int base = kb; base < ke; base += 2 * UNR * KS) {
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) load_w(base + (UNR + u) * KS, wb[u]);
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) compute(base + u * KS, wa[u]);
+        if (base + 2 * UNR * KS < ke) {
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) load_w(base + (2 * UNR + u) * KS, wa[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) compute(base + (UNR + u) * KS, wb[u]);
+    }
+
+    // ---- partial sums of this split
     const int ncols = a.dual_F > 0 ? 2 * a.dual_F : a.N;
     float* out = a.part + (int64_t)sp * a.M * ncols;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int s = 0; s < NS; ++s) {
         if (!rv[s]) continue;
         float rs = 1.f;
         if constexpr (WF == W_INT8) rs = h2f(a.scales[row[s]]);
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
+        for (int t = 0; t < MT; ++t)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int m = 16 * t + 4 * g + i;
                 if (m < a.M) out[(int64_t)m * ncols + row[s]] = acc[t][s][i] * rs;
             }
-        }
     }
 }
 
-template <int WF, int MT>
-static hipError_t launch_mt(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
+template <int WF, int MT, int NS, int XF>
+static hipError_t launch4(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
     constexpr int UNR = (WF == W_INT4) ? 2 : 4;
-    hipLaunchKernelGGL((skinny_kernel<WF, MT, UNR>), grid, dim3(256), 0, st, a);
+    const size_t lds = (size_t)a.M * (a.krange + SK_PAD) * 2;
+    hipLaunchKernelGGL((skinny_kernel<WF, MT, NS, UNR, XF>), grid, dim3(256), lds, st, a);
     return hipGetLastError();
 }
 
-template <int WF>
-static hipError_t launch_wf(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
-    const int mt = (a.M + 15) / 16;
-    switch (mt) {
-        case 1: return launch_mt<WF, 1>(a, grid, st);
-        case 2: return launch_mt<WF, 2>(a, grid, st);
-        case 3: return launch_mt<WF, 3>(a, grid, st);
-        case 4: return launch_mt<WF, 4>(a, grid, st);
+template <int WF, int MT, int NS>
+static hipError_t launch3(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
+    switch (a.xf) {
+        case XF_COPY: return launch4<WF, MT, NS, XF_COPY>(a, grid, st);
+        case XF_NORM: return launch4<WF, MT, NS, XF_NORM>(a, grid, st);
+        case XF_SWIGLU: return launch4<WF, MT, NS, XF_SWIGLU>(a, grid, st);
         default: return hipErrorInvalidValue;
     }
 }
 
-int skinny_kstep(int wf) { return wf == W_BF16 ? 32 : (wf == W_INT8 ? 64 : 128); }
+template <int WF>
+static hipError_t launch2(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
+    switch ((a.M + 15) / 16) {
+        case 1: return launch3<WF, 1, SKINNY_NS>(a, grid, st);
+        case 2: return launch3<WF, 2, SKINNY_NS>(a, grid, st);
+        case 3: return launch3<WF, 3, SKINNY_NS>(a, grid, st);
+        case 4: return launch3<WF, 4, SKINNY_NS>(a, grid, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+int skinny_kstep(int wf) { return weight_kstep(wf); }
+
+int skinny_max_krange(int M) {
+    int kr = SK_LDS_ELEMS / (M > 0 ? M : 1) - SK_PAD;
+    return kr - kr % 128;
+}
+
+int skinny_tiles(int N, int dual_F) {
+    return dual_F > 0 ? (dual_F + 32 * SKINNY_NS - 1) / (32 * SKINNY_NS) : (N + 64 * SKINNY_NS - 1) / (64 * SKINNY_NS);
+}
 
 hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st) {
-    const int tiles = a.dual_F > 0 ? (a.dual_F + 15) / 16 : (a.N + 31) / 32;
-    dim3 grid(tiles, ks);
+    if (a.krange > skinny_max_krange(a.M) || a.krange % skinny_kstep(wf) != 0) return hipErrorInvalidValue;
+    dim3 grid(skinny_tiles(a.N, a.dual_F), ks);
     switch (wf) {
-        case W_BF16: return launch_wf<W_BF16>(a, grid, st);
-        case W_INT8: return launch_wf<W_INT8>(a, grid, st);
-        case W_INT4: return launch_wf<W_INT4>(a, grid, st);
+        case W_BF16: return launch2<W_BF16>(a, grid, st);
+        case W_INT8: return launch2<W_INT8>(a, grid, st);
+        case W_INT4: return launch2<W_INT4>(a, grid, st);
         default: return hipErrorInvalidValue;
     }
 }
