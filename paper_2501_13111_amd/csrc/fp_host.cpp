@@ -301,7 +301,7 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     a.src_part = xin.src_part;
     a.src_ks = xin.src_ks;
     int ks, kr;
-    choose_split(skinny_tiles(m.N, dual_F), m.K, M, h->wq, &ks, &kr);
+    choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, h->wq, &ks, &kr);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     a.krange = kr;
     HIPCHK(launch_skinny(a, h->wq, ks, st));
@@ -409,20 +409,25 @@ fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_
     int ks;
     // sums of squares of the layer-0 input rows (its RMSNorm is applied while the qkv
     // projection stages its input)
+    // RMSNorm of a layer input: for one sequence the projection applies it while staging
+    // its input (from the row's sum of squares); for a batch it is applied once here
+    const bool stage_norm = (B == 1);
     h->prof.mark(FP_K_RMSNORM, 0);
-    HIPCHK(launch_resid_norm(nullptr, 0, B, s.hidden, x, nullptr, nullptr, s.rms_eps, nullptr, h->act_fmt,
-                             h->ssq, nullptr, st));
+    HIPCHK(launch_resid_norm(nullptr, 0, B, s.hidden, x, nullptr, stage_norm ? nullptr : h->L[0].attn_norm,
+                             s.rms_eps, h->act_in, h->act_fmt, h->ssq, nullptr, st));
     for (int l = 0; l < s.n_layers; ++l) {
         const LayerW& W = h->L[l];
         const uint16_t* in = (l == 0) ? x : h->xbuf;
         uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
         float* dump = h->dump ? h->dump + (size_t)l * 2 * B * h->kv_dim : nullptr;
         XIn xq;
-        xq.xf = XF_NORM;
-        xq.gain = W.attn_norm;
-        xq.ssq = h->ssq;
+        if (stage_norm) {
+            xq.xf = XF_NORM;
+            xq.gain = W.attn_norm;
+            xq.ssq = h->ssq;
+        }
         h->prof.mark(FP_K_QKV, l);
-        if ((rc = run_skinny(h, in, W.qkv, B, 0, xq, h->part, &ks, st))) return rc;
+        if ((rc = run_skinny(h, stage_norm ? in : h->act_in, W.qkv, B, 0, xq, h->part, &ks, st))) return rc;
         AttnDecArgs ad{};
         ad.qkv_part = h->part;
         ad.ks = ks;
@@ -440,6 +445,9 @@ fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_
         ad.max_seq = s.max_seq;
         ad.d_pos = h->d_pos;
         ad.scale = scale;
+        int nsplit;
+        attn_decode_split(s.max_seq, B, s.n_kv_heads, s.n_heads / s.n_kv_heads, &nsplit, &ad.keys_per_split);
+        ad.batch = B;
         ad.ws = h->attn_ws;
         ad.out = h->act_o;
         ad.out_fmt = h->act_fmt;
@@ -448,24 +456,38 @@ fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_
         h->prof.mark(FP_K_O, l);
         if ((rc = run_skinny(h, h->act_o, W.o, B, 0, XIn(), h->part, &ks, st))) return rc;
         h->prof.mark(FP_K_RESID_NORM, l);
-        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, nullptr, s.rms_eps, nullptr, h->act_fmt,
-                                 h->ssq, nullptr, st));
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, stage_norm ? nullptr : W.mlp_norm,
+                                 s.rms_eps, h->act_in, h->act_fmt, h->ssq, nullptr, st));
         XIn xg;
-        xg.xf = XF_NORM;
-        xg.gain = W.mlp_norm;
-        xg.ssq = h->ssq;
+        if (stage_norm) {
+            xg.xf = XF_NORM;
+            xg.gain = W.mlp_norm;
+            xg.ssq = h->ssq;
+        }
         h->prof.mark(FP_K_GATE_UP, l);
-        if ((rc = run_skinny(h, h->hbuf, W.gu, B, s.ffn, xg, h->part2, &ks, st))) return rc;
+        if ((rc = run_skinny(h, stage_norm ? h->hbuf : h->act_in, W.gu, B, s.ffn, xg, h->part2, &ks, st))) return rc;
+        // SwiGLU: for one sequence the down projection forms it while staging its input;
+        // for a batch every down workgroup would re-read B rows of partials, so it is
+        // formed once instead
         XIn xd;
-        xd.xf = XF_SWIGLU;
-        xd.src_part = h->part2;
-        xd.src_ks = ks;
+        const uint16_t* dX = nullptr;
+        if (B == 1) {
+            xd.xf = XF_SWIGLU;
+            xd.src_part = h->part2;
+            xd.src_ks = ks;
+        } else {
+            h->prof.mark(FP_K_SWIGLU, l);
+            HIPCHK(launch_swiglu(h->part2, ks, B, s.ffn, h->act_f, h->act_fmt, st));
+            dX = h->act_f;
+        }
         h->prof.mark(FP_K_DOWN, l);
-        if ((rc = run_skinny(h, nullptr, W.down, B, 0, xd, h->part, &ks, st))) return rc;
+        if ((rc = run_skinny(h, dX, W.down, B, 0, xd, h->part, &ks, st))) return rc;
         h->prof.mark(FP_K_RESID_NORM, l);
         // the last layer's epilogue also advances the position
-        int* incp = (l == s.n_layers - 1) ? h->d_pos : nullptr;
-        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, nullptr, s.rms_eps, nullptr, h->act_fmt,
+        const bool last = (l == s.n_layers - 1);
+        int* incp = last ? h->d_pos : nullptr;
+        const uint16_t* gnext = (!last && !stage_norm) ? h->L[l + 1].attn_norm : nullptr;
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, gnext, s.rms_eps, h->act_in, h->act_fmt,
                                  h->ssq, incp, st));
     }
     h->prof.end();

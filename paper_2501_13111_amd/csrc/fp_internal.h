@@ -89,7 +89,9 @@ struct AttnDecArgs {
     int kv_int8, nh, nkv, d, max_seq;
     const int* d_pos;         // current position (the new token's index)
     float scale;              // float32(1/sqrt(d))
-    float* ws;                // [B, nh, nchunks, d + 2]
+    int keys_per_split;       // context keys per workgroup (multiple of 64)
+    int batch;                // B
+    float* ws;                // [B, nh, nsplit, d + 2] partials when nsplit > 1
     uint16_t* out;            // [B, nh*d] activation format out_fmt
     int out_fmt;
 };
@@ -135,11 +137,12 @@ hipError_t launch_inc_pos(int* d_pos, hipStream_t st);
 
 int skinny_kstep(int wf);
 int skinny_max_krange(int M);
-int skinny_tiles(int N, int dual_F);
+int skinny_tiles(int N, int dual_F, int M);
 hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st);
 
 int attn_decode_chunks(int max_seq);
+void attn_decode_split(int max_seq, int B, int nkv, int group, int* nsplit, int* keys_per_split);
 bool attn_decode_supported(int d, int group);
 hipError_t launch_attn_decode(const AttnDecArgs& a, int B, hipStream_t st);
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st);

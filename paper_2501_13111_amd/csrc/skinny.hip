@@ -256,13 +256,17 @@ static hipError_t launch3(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
     }
 }
 
+// subtiles per wave: batches stream more rows per workgroup so the staged activation
+// slice is shared by more weights
+static int skinny_ns(int M) { return M > 16 ? 4 : SKINNY_NS; }
+
 template <int WF>
 static hipError_t launch2(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
     switch ((a.M + 15) / 16) {
         case 1: return launch3<WF, 1, SKINNY_NS>(a, grid, st);
-        case 2: return launch3<WF, 2, SKINNY_NS>(a, grid, st);
-        case 3: return launch3<WF, 3, SKINNY_NS>(a, grid, st);
-        case 4: return launch3<WF, 4, SKINNY_NS>(a, grid, st);
+        case 2: return launch3<WF, 2, 4>(a, grid, st);
+        case 3: return launch3<WF, 3, 4>(a, grid, st);
+        case 4: return launch3<WF, 4, 4>(a, grid, st);
         default: return hipErrorInvalidValue;
     }
 }
@@ -274,13 +278,14 @@ int skinny_max_krange(int M) {
     return kr - kr % 128;
 }
 
-int skinny_tiles(int N, int dual_F) {
-    return dual_F > 0 ? (dual_F + 32 * SKINNY_NS - 1) / (32 * SKINNY_NS) : (N + 64 * SKINNY_NS - 1) / (64 * SKINNY_NS);
+int skinny_tiles(int N, int dual_F, int M) {
+    const int ns = skinny_ns(M);
+    return dual_F > 0 ? (dual_F + 32 * ns - 1) / (32 * ns) : (N + 64 * ns - 1) / (64 * ns);
 }
 
 hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st) {
     if (a.krange > skinny_max_krange(a.M) || a.krange % skinny_kstep(wf) != 0) return hipErrorInvalidValue;
-    dim3 grid(skinny_tiles(a.N, a.dual_F), ks);
+    dim3 grid(skinny_tiles(a.N, a.dual_F, a.M), ks);
     switch (wf) {
         case W_BF16: return launch2<W_BF16>(a, grid, st);
         case W_INT8: return launch2<W_INT8>(a, grid, st);
