@@ -266,7 +266,7 @@ __global__ void __launch_bounds__(256) attn_decode_kernel(AttnDecArgs a) {
         if (nsplit == 1) {
             a.out[((int64_t)b * a.nh + hg) * D + dd] = act_store(bfround(sum / l_run[h]), a.out_fmt);
         } else {
-            float* dst = a.ws + (((int64_t)b * a.nh + hg) * nsplit + sp) * (D + 2);
+            float* dst = a.ws + (((int64_t)b * a.nh + hg) * nsplit + sp) * (D + 4);
             dst[dd] = sum;
             if (dd == 0) { dst[D] = m_run[h]; dst[D + 1] = l_run[h]; }
         }
@@ -540,7 +540,7 @@ __global__ void __launch_bounds__(256) attn_decode_wave_kernel(AttnDecArgs a, in
                 if (nsplit == 1) {
                     a.out[((int64_t)b * a.nh + hg) * D + dd] = act_store(bfround(o[h][e] / l_run[h]), a.out_fmt);
                 } else {
-                    float* dst = a.ws + (((int64_t)b * a.nh + hg) * nsplit + sp) * (D + 2);
+                    float* dst = a.ws + (((int64_t)b * a.nh + hg) * nsplit + sp) * (D + 4);
                     dst[dd] = o[h][e];
                     if (dd == 0) { dst[D] = m_run[h]; dst[D + 1] = l_run[h]; }
                 }
@@ -555,14 +555,14 @@ __global__ void __launch_bounds__(D) attn_merge_kernel(AttnDecArgs a, int nch) {
     const int h = blockIdx.x, b = blockIdx.y, i = threadIdx.x;
     const int len = *a.d_pos + 1;
     const int nv = (len + a.keys_per_split - 1) / a.keys_per_split;
-    const float* src = a.ws + ((int64_t)b * a.nh + h) * nch * (D + 2);
+    const float* src = a.ws + ((int64_t)b * a.nh + h) * nch * (D + 4);
     float m = -INFINITY;
-    for (int c = 0; c < nv; ++c) m = fmaxf(m, src[c * (D + 2) + D]);
+    for (int c = 0; c < nv; ++c) m = fmaxf(m, src[c * (D + 4) + D]);
     float l = 0.f, o = 0.f;
     for (int c = 0; c < nv; ++c) {
-        const float e = __expf(src[c * (D + 2) + D] - m);
-        l += src[c * (D + 2) + D + 1] * e;
-        o += src[c * (D + 2) + i] * e;
+        const float e = __expf(src[c * (D + 4) + D] - m);
+        l += src[c * (D + 4) + D + 1] * e;
+        o += src[c * (D + 4) + i] * e;
     }
     a.out[((int64_t)b * a.nh + h) * D + i] = act_store(bfround(o / l), a.out_fmt);
 }
@@ -594,7 +594,7 @@ static hipError_t launch_dgk(const AttnDecArgs& a, int B, int nsplit, hipStream_
         hipLaunchKernelGGL((attn_decode_kernel<D, G, KV8>), dim3(nsplit, a.nkv, B), dim3(256), 0, st, a);
     }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || nsplit == 1) return e;
+    if (e != hipSuccess || nsplit == 1 || a.skip_merge) return e;
     hipLaunchKernelGGL(attn_merge_kernel<D>, dim3(a.nh, B), dim3(D), 0, st, a, nsplit);
     return hipGetLastError();
 }

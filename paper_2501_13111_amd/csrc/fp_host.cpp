@@ -276,8 +276,10 @@ struct XIn {
     int xf = XF_COPY;
     const uint16_t* gain = nullptr;
     const float* ssq = nullptr;
+    int ssq_blocks = 0;
     const float* src_part = nullptr;
     int src_ks = 0;
+    int att_nsplit = 0, att_kps = 0;
 };
 
 fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, const XIn& xin,
@@ -296,10 +298,15 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     a.xf = xin.xf;
     a.gain = xin.gain;
     a.ssq = xin.ssq;
-    a.ssq_blocks = resid_ssq_blocks(h->s.hidden);
+    a.ssq_blocks = xin.ssq_blocks;
     a.eps = h->s.rms_eps;
     a.src_part = xin.src_part;
     a.src_ks = xin.src_ks;
+    a.att_ws = h->attn_ws;
+    a.att_nsplit = xin.att_nsplit;
+    a.att_kps = xin.att_kps;
+    a.head_dim = h->s.head_dim;
+    a.d_pos = h->d_pos;
     int ks, kr;
     choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, h->wq, &ks, &kr);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
@@ -401,97 +408,135 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
     return FP_OK;
 }
 
-fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
+AttnDecArgs attn_args(fp_layer* h, int l, int ks, int B, float* dump) {
+    const fp_shape& s = h->s;
+    AttnDecArgs ad{};
+    ad.qkv_part = h->part;
+    ad.ks = ks;
+    ad.cos_t = h->cos_t;
+    ad.sin_t = h->sin_t;
+    ad.dump = dump;
+    ad.kc = h->kc[l];
+    ad.vc = h->vc[l];
+    ad.k_scales = h->ksc[l];
+    ad.v_scales = h->vsc[l];
+    ad.kv_int8 = h->kvq == FP_KV_INT8;
+    ad.nh = s.n_heads;
+    ad.nkv = s.n_kv_heads;
+    ad.d = s.head_dim;
+    ad.max_seq = s.max_seq;
+    ad.d_pos = h->d_pos;
+    ad.scale = (float)(1.0 / std::sqrt((double)s.head_dim));
+    int nsplit;
+    attn_decode_split(s.max_seq, B, s.n_kv_heads, s.n_heads / s.n_kv_heads, &nsplit, &ad.keys_per_split);
+    ad.batch = B;
+    ad.ws = h->attn_ws;
+    ad.out = h->act_o;
+    ad.out_fmt = h->act_fmt;
+    return ad;
+}
+
+// One sequence: the RMSNorms and the SwiGLU are applied while the projections stage
+// their inputs (layer 0 sums the squares of its input row itself), attention rotates
+// and appends the new K / V itself, and a light kernel per residual add reduces the
+// split-K partials and the row's sum of squares.
+fp_status enqueue_decode_single(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
     const fp_shape& s = h->s;
     const int B = h->B;
-    const float scale = (float)(1.0 / std::sqrt((double)s.head_dim));
+    const int ssq_blocks = resid_ssq_blocks(s.hidden);
     fp_status rc;
     int ks;
-    // sums of squares of the layer-0 input rows (its RMSNorm is applied while the qkv
-    // projection stages its input)
-    // RMSNorm of a layer input: for one sequence the projection applies it while staging
-    // its input (from the row's sum of squares); for a batch it is applied once here
-    const bool stage_norm = (B == 1);
-    h->prof.mark(FP_K_RMSNORM, 0);
-    HIPCHK(launch_resid_norm(nullptr, 0, B, s.hidden, x, nullptr, stage_norm ? nullptr : h->L[0].attn_norm,
-                             s.rms_eps, h->act_in, h->act_fmt, h->ssq, nullptr, st));
     for (int l = 0; l < s.n_layers; ++l) {
         const LayerW& W = h->L[l];
         const uint16_t* in = (l == 0) ? x : h->xbuf;
         uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
         float* dump = h->dump ? h->dump + (size_t)l * 2 * B * h->kv_dim : nullptr;
         XIn xq;
-        if (stage_norm) {
-            xq.xf = XF_NORM;
-            xq.gain = W.attn_norm;
-            xq.ssq = h->ssq;
-        }
+        xq.xf = XF_NORM;
+        xq.gain = W.attn_norm;
+        xq.ssq = (l == 0) ? nullptr : h->ssq;    // layer 0: the projection sums the squares itself
+        xq.ssq_blocks = ssq_blocks;
         h->prof.mark(FP_K_QKV, l);
-        if ((rc = run_skinny(h, stage_norm ? in : h->act_in, W.qkv, B, 0, xq, h->part, &ks, st))) return rc;
-        AttnDecArgs ad{};
-        ad.qkv_part = h->part;
-        ad.ks = ks;
-        ad.cos_t = h->cos_t;
-        ad.sin_t = h->sin_t;
-        ad.dump = dump;
-        ad.kc = h->kc[l];
-        ad.vc = h->vc[l];
-        ad.k_scales = h->ksc[l];
-        ad.v_scales = h->vsc[l];
-        ad.kv_int8 = h->kvq == FP_KV_INT8;
-        ad.nh = s.n_heads;
-        ad.nkv = s.n_kv_heads;
-        ad.d = s.head_dim;
-        ad.max_seq = s.max_seq;
-        ad.d_pos = h->d_pos;
-        ad.scale = scale;
-        int nsplit;
-        attn_decode_split(s.max_seq, B, s.n_kv_heads, s.n_heads / s.n_kv_heads, &nsplit, &ad.keys_per_split);
-        ad.batch = B;
-        ad.ws = h->attn_ws;
-        ad.out = h->act_o;
-        ad.out_fmt = h->act_fmt;
+        if ((rc = run_skinny(h, in, W.qkv, B, 0, xq, h->part, &ks, st))) return rc;
+        AttnDecArgs ad = attn_args(h, l, ks, B, dump);
+        const int nsplit = (s.max_seq + ad.keys_per_split - 1) / ad.keys_per_split;
+        XIn xo;
+        if (nsplit > 1) {               // the o projection merges the context splits
+            ad.skip_merge = 1;
+            xo.xf = XF_MERGE;
+            xo.att_nsplit = nsplit;
+            xo.att_kps = ad.keys_per_split;
+        }
         h->prof.mark(FP_K_ATTN, l);
         HIPCHK(launch_attn_decode(ad, B, st));
         h->prof.mark(FP_K_O, l);
-        if ((rc = run_skinny(h, h->act_o, W.o, B, 0, XIn(), h->part, &ks, st))) return rc;
+        if ((rc = run_skinny(h, h->act_o, W.o, B, 0, xo, h->part, &ks, st))) return rc;
         h->prof.mark(FP_K_RESID_NORM, l);
-        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, stage_norm ? nullptr : W.mlp_norm,
-                                 s.rms_eps, h->act_in, h->act_fmt, h->ssq, nullptr, st));
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, nullptr, s.rms_eps, nullptr, h->act_fmt,
+                                 h->ssq, nullptr, st));
         XIn xg;
-        if (stage_norm) {
-            xg.xf = XF_NORM;
-            xg.gain = W.mlp_norm;
-            xg.ssq = h->ssq;
-        }
+        xg.xf = XF_NORM;
+        xg.gain = W.mlp_norm;
+        xg.ssq = h->ssq;
+        xg.ssq_blocks = ssq_blocks;
         h->prof.mark(FP_K_GATE_UP, l);
-        if ((rc = run_skinny(h, stage_norm ? h->hbuf : h->act_in, W.gu, B, s.ffn, xg, h->part2, &ks, st))) return rc;
-        // SwiGLU: for one sequence the down projection forms it while staging its input;
-        // for a batch every down workgroup would re-read B rows of partials, so it is
-        // formed once instead
+        if ((rc = run_skinny(h, h->hbuf, W.gu, B, s.ffn, xg, h->part2, &ks, st))) return rc;
         XIn xd;
-        const uint16_t* dX = nullptr;
-        if (B == 1) {
-            xd.xf = XF_SWIGLU;
-            xd.src_part = h->part2;
-            xd.src_ks = ks;
-        } else {
-            h->prof.mark(FP_K_SWIGLU, l);
-            HIPCHK(launch_swiglu(h->part2, ks, B, s.ffn, h->act_f, h->act_fmt, st));
-            dX = h->act_f;
-        }
+        xd.xf = XF_SWIGLU;
+        xd.src_part = h->part2;
+        xd.src_ks = ks;
         h->prof.mark(FP_K_DOWN, l);
-        if ((rc = run_skinny(h, dX, W.down, B, 0, xd, h->part, &ks, st))) return rc;
+        if ((rc = run_skinny(h, nullptr, W.down, B, 0, xd, h->part, &ks, st))) return rc;
+        // the last residual kernel also advances the position (every reader has run)
         h->prof.mark(FP_K_RESID_NORM, l);
-        // the last layer's epilogue also advances the position
-        const bool last = (l == s.n_layers - 1);
-        int* incp = last ? h->d_pos : nullptr;
-        const uint16_t* gnext = (!last && !stage_norm) ? h->L[l + 1].attn_norm : nullptr;
-        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, gnext, s.rms_eps, h->act_in, h->act_fmt,
-                                 h->ssq, incp, st));
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, nullptr, s.rms_eps, nullptr, h->act_fmt,
+                                 h->ssq, (l == s.n_layers - 1) ? h->d_pos : nullptr, st));
     }
     h->prof.end();
     return FP_OK;
+}
+
+// A batch: the RMSNorm of each projection input and the SwiGLU are formed once
+// (every workgroup re-forming them from B rows would cost more than the weights).
+fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
+    const fp_shape& s = h->s;
+    const int B = h->B;
+    fp_status rc;
+    int ks;
+    h->prof.mark(FP_K_RMSNORM, 0);
+    HIPCHK(launch_resid_norm(nullptr, 0, B, s.hidden, x, nullptr, h->L[0].attn_norm, s.rms_eps, h->act_in,
+                             h->act_fmt, h->ssq, nullptr, st));
+    for (int l = 0; l < s.n_layers; ++l) {
+        const LayerW& W = h->L[l];
+        const uint16_t* in = (l == 0) ? x : h->xbuf;
+        uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
+        float* dump = h->dump ? h->dump + (size_t)l * 2 * B * h->kv_dim : nullptr;
+        h->prof.mark(FP_K_QKV, l);
+        if ((rc = run_skinny(h, h->act_in, W.qkv, B, 0, XIn(), h->part, &ks, st))) return rc;
+        h->prof.mark(FP_K_ATTN, l);
+        HIPCHK(launch_attn_decode(attn_args(h, l, ks, B, dump), B, st));
+        h->prof.mark(FP_K_O, l);
+        if ((rc = run_skinny(h, h->act_o, W.o, B, 0, XIn(), h->part, &ks, st))) return rc;
+        h->prof.mark(FP_K_RESID_NORM, l);
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, W.mlp_norm, s.rms_eps, h->act_in,
+                                 h->act_fmt, h->ssq, nullptr, st));
+        h->prof.mark(FP_K_GATE_UP, l);
+        if ((rc = run_skinny(h, h->act_in, W.gu, B, s.ffn, XIn(), h->part2, &ks, st))) return rc;
+        h->prof.mark(FP_K_SWIGLU, l);
+        HIPCHK(launch_swiglu(h->part2, ks, B, s.ffn, h->act_f, h->act_fmt, st));
+        h->prof.mark(FP_K_DOWN, l);
+        if ((rc = run_skinny(h, h->act_f, W.down, B, 0, XIn(), h->part, &ks, st))) return rc;
+        const bool last = (l == s.n_layers - 1);
+        h->prof.mark(FP_K_RESID_NORM, l);
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, last ? nullptr : h->L[l + 1].attn_norm,
+                                 s.rms_eps, h->act_in, h->act_fmt, h->ssq, last ? h->d_pos : nullptr, st));
+    }
+    h->prof.end();
+    return FP_OK;
+}
+
+fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
+    return h->B == 1 ? enqueue_decode_single(h, x, y, st) : enqueue_decode_batch(h, x, y, st);
 }
 
 bool overlap(const void* a, size_t na, const void* b, size_t nb) {
@@ -604,7 +649,7 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->part2, (size_t)KSMAX * s.max_batch * 2 * F, &h->bytes_ws))) return bail(st);
     const size_t nch = attn_decode_chunks(s.max_seq);
-    if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 2), &h->bytes_ws)))
+    if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 4), &h->bytes_ws)))
         return bail(st);
     if ((st = alloc_t(h, &h->d_pos, 1, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->ssq, (size_t)s.max_batch * resid_ssq_blocks(H), &h->bytes_ws))) return bail(st);

@@ -20,7 +20,8 @@ enum ActFmt { ACT_BF16 = 0, ACT_F16 = 1 };
 enum XForm {
     XF_COPY = 0,     // A = X (activation format already)
     XF_NORM = 1,     // A = act(bf16(X * r[m] * gain)), X bf16, r from ssq block sums
-    XF_SWIGLU = 2    // A = act(bf16(silu(G) * U)) from gate|up partial sums
+    XF_SWIGLU = 2,   // A = act(bf16(silu(G) * U)) from gate|up partial sums
+    XF_MERGE = 3     // A = attention output merged from its context-split partials
 };
 
 // Decode skinny GEMM: part[s, m, col] = sum_{k in split s} A[m, k] W[col, k]
@@ -38,11 +39,15 @@ struct SkinnyArgs {
     float* part;              // [ks, M, N] fp32
     int xf;                   // XForm
     const uint16_t* gain;     // XF_NORM: bf16 [K]
-    const float* ssq;         // XF_NORM: [M, ssq_blocks] sums of squares of X rows
+    const float* ssq;         // XF_NORM: [M, ssq_blocks] sums of squares of X rows; NULL: the
+                              // workgroup sums the squares of its rows itself
     int ssq_blocks;
     float eps;
     const float* src_part;    // XF_SWIGLU: [src_ks, M, 2K] gate|up partial sums
     int src_ks;
+    const float* att_ws;      // XF_MERGE: [M, K / head_dim, att_nsplit, head_dim + 4]
+    int att_nsplit, att_kps, head_dim;
+    const int* d_pos;         // XF_MERGE: position of the newest token
 };
 
 struct GemmArgs {
@@ -91,7 +96,8 @@ struct AttnDecArgs {
     float scale;              // float32(1/sqrt(d))
     int keys_per_split;       // context keys per workgroup (multiple of 64)
     int batch;                // B
-    float* ws;                // [B, nh, nsplit, d + 2] partials when nsplit > 1
+    int skip_merge;           // leave split partials in ws (the consumer merges them)
+    float* ws;                // [B, nh, nsplit, d + 4] partials when nsplit > 1 (m at d, l at d + 1)
     uint16_t* out;            // [B, nh*d] activation format out_fmt
     int out_fmt;
 };

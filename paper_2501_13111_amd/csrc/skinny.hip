@@ -32,7 +32,10 @@
 //   XF_NORM   A = bf16(y * rsqrt(mean(y^2) + eps) * g) (RMSNorm of the layer input
 //             or of h; the row's sum of squares comes as block sums)
 //   XF_SWIGLU A = bf16(silu(gate) * up) from the gate|up partial sums
-// so the normalisation and the activation never run as kernels of their own.
+//   XF_MERGE  A = attention output, merged from its context splits by the exact
+//             log-sum-exp identity
+// so the normalisation, the activation and the merge never run as kernels of
+// their own.
 // In dual mode (the [gate; up] matrix) the first NS/2 subtiles of a wave read gate
 // rows f and the others up rows F + f of the same f.
 #include "fp_device.h"
@@ -98,10 +101,28 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 
     // ---- stage the activation slice (with its transform) into LDS
     if constexpr (XF == XF_NORM) {
-        if (tid < a.M) {
-            float ss = 0.f;
-            for (int b = 0; b < a.ssq_blocks; ++b) ss += a.ssq[tid * a.ssq_blocks + b];
-            rrow[tid] = 1.0f / __fsqrt_rn(ss / (float)a.K + a.eps);
+        if (a.ssq != nullptr) {
+            if (tid < a.M) {
+                float ss = 0.f;
+                for (int b = 0; b < a.ssq_blocks; ++b) ss += a.ssq[tid * a.ssq_blocks + b];
+                rrow[tid] = 1.0f / __fsqrt_rn(ss / (float)a.K + a.eps);
+            }
+        } else {   // small batches: sum the squares of the whole rows here
+            __shared__ float red[16];
+            for (int m = 0; m < a.M; ++m) {
+                float ss = 0.f;
+                for (int k = tid * 8; k < a.K; k += 256 * 8) {
+                    const u32x4 v = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+                    const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float e0 = __uint_as_float(vv[j] << 16), e1 = __uint_as_float(vv[j] & 0xFFFF0000u);
+                        ss += e0 * e0 + e1 * e1;
+                    }
+                }
+                ss = block_sum(ss, red);
+                if (tid == 0) rrow[m] = 1.0f / __fsqrt_rn(ss / (float)a.K + a.eps);
+            }
         }
         __syncthreads();
     }
@@ -125,6 +146,29 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
                     const float e1 = bfround(__uint_as_float(vv[j] & 0xFFFF0000u) * rm * __uint_as_float(gv[j] & 0xFFFF0000u));
                     o[j] = (uint32_t)act_store(e0, AF) | ((uint32_t)act_store(e1, AF) << 16);
                 }
+            } else if constexpr (XF == XF_MERGE) {
+                // log-sum-exp merge of the context splits of head k / head_dim
+                const int D = a.head_dim, nhd = a.K / D;
+                const int h = k / D, dd = k % D;
+                const int nv = (*a.d_pos + a.att_kps) / a.att_kps;     // splits holding keys
+                const float* src = a.att_ws + ((int64_t)m * nhd + h) * a.att_nsplit * (D + 4);
+                float mx = -INFINITY;
+                for (int sp2 = 0; sp2 < nv; ++sp2) mx = fmaxf(mx, src[sp2 * (D + 4) + D]);
+                float L = 0.f, ov[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) ov[j] = 0.f;
+                for (int sp2 = 0; sp2 < nv; ++sp2) {
+                    const float* q = src + sp2 * (D + 4);
+                    const float e = __expf(q[D] - mx);
+                    L += q[D + 1] * e;
+                    const float4 o0 = *(const float4*)(q + dd), o1 = *(const float4*)(q + dd + 4);
+                    ov[0] += o0.x * e; ov[1] += o0.y * e; ov[2] += o0.z * e; ov[3] += o0.w * e;
+                    ov[4] += o1.x * e; ov[5] += o1.y * e; ov[6] += o1.z * e; ov[7] += o1.w * e;
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    o[j] = (uint32_t)act_store(bfround(ov[2 * j] / L), AF) |
+                           ((uint32_t)act_store(bfround(ov[2 * j + 1] / L), AF) << 16);
             } else {   // XF_SWIGLU: k indexes f; partials [src_ks, M, 2F]
                 const int F = a.K;
                 float gs[8], us[8];
@@ -252,6 +296,7 @@ static hipError_t launch3(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
         case XF_COPY: return launch4<WF, MT, NS, XF_COPY>(a, grid, st);
         case XF_NORM: return launch4<WF, MT, NS, XF_NORM>(a, grid, st);
         case XF_SWIGLU: return launch4<WF, MT, NS, XF_SWIGLU>(a, grid, st);
+        case XF_MERGE: return launch4<WF, MT, NS, XF_MERGE>(a, grid, st);
         default: return hipErrorInvalidValue;
     }
 }
