@@ -32,6 +32,32 @@ KIND = {0: "rmsnorm", 1: "qkv", 2: "rope_kv", 3: "attn", 4: "o", 5: "resid_norm"
         7: "swiglu", 8: "down", 9: "pos"}
 PROJ = {"qkv", "o", "gate_up", "down"}
 
+# HBM bytes per decode-projection launch of the weight-streaming kernel, from two
+# rocprofv3 --pmc passes (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0, the factors a 1 GiB device
+# copy gives), averaged over the qkv / o / gate_up / down launches.  Valid only for the
+# kernel sources they were taken on (hash of skinny.hip, fp_device.h, fp_internal.h);
+# the summary and the commands are in profiles/skinny_kernel_llama2-7b-bf16.md.
+SKINNY_TRAFFIC = {"llama2-7b-bf16": {"src": "65b73fbc67b7399b", "bytes_per_launch": 102474485}}
+SKINNY_SRC = ("skinny.hip", "fp_device.h", "fp_internal.h")
+
+
+def skinny_src_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in SKINNY_SRC:
+        with open(os.path.join(ROOT, "paper_2501_13111_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def skinny_traffic(config):
+    """Measured bytes per launch, or None when not measured for this workload or the
+    kernel sources changed since the counters were taken."""
+    t = SKINNY_TRAFFIC.get(config)
+    if t is None or t["src"] != skinny_src_hash():
+        return None
+    return t["bytes_per_launch"]
+
 
 def cfg_of(name):
     from oracle.layer import CONFIGS
@@ -79,7 +105,9 @@ def prefill_flops(s, B, P):
 
 
 def profile_decode(fp, x, y, stream_ptr):
-    """One eager decode step with HIP events around every launch (on the bench stream)."""
+    """One eager decode step, timed per launch on the bench stream: the library stamps a
+    start / stop HIP event pair from each kernel's own dispatch (hipExtLaunchKernel), so an
+    interval is that kernel's execution."""
     import ctypes
     from paper_2501_13111_amd import binding
 
@@ -225,17 +253,16 @@ def main():
         for kind, layer, ms in prof:
             by_kind.setdefault(kind, []).append(ms)
     dom = max(by_kind, key=lambda k: sum(by_kind[k]))
-    if dom in PROJ or True:
-        # the projections share one kernel (the weight-streaming skinny GEMM): report it as one
-        proj_ms = [ms for prof in dec_profs for kind, _, ms in prof if kind in PROJ]
-        proj_b = [proj_bytes(kind, s, wq, B) for prof in dec_profs for kind, _, _ in prof if kind in PROJ]
-        achieved = sum(proj_b) / (sum(proj_ms) / 1e3) / 1e9
-        roof = {"kernel": "skinny_kernel (decode weight-streaming projections qkv/o/gate_up/down)",
-                "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "avg_launch_us": round(1e3 * statistics.fmean(proj_ms), 3),
-                "bytes_per_launch_avg": int(statistics.fmean(proj_b)),
-                "dominant_by_time": dom}
+    # the projections share one kernel (the weight-streaming skinny GEMM): report it as one
+    proj_ms = [ms for prof in dec_profs for kind, _, ms in prof if kind in PROJ]
+    proj_b = [proj_bytes(kind, s, wq, B) for prof in dec_profs for kind, _, _ in prof if kind in PROJ]
+    achieved = sum(proj_b) / (sum(proj_ms) / 1e3) / 1e9
+    roof = {"kernel": "skinny_kernel (decode weight-streaming projections qkv/o/gate_up/down)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": skinny_traffic(args.config),
+            "avg_launch_us": round(1e3 * statistics.fmean(proj_ms), 3),
+            "bytes_per_launch_avg": int(statistics.fmean(proj_b)),
+            "dominant_by_time": dom}
     pre_ms_total = sum(ms for _, _, ms in pre_prof)
     pre_gemm_ms = sum(ms for kind, _, ms in pre_prof if kind in PROJ)
     pflops = prefill_flops(s, B, Pp)

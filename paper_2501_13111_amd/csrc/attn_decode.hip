@@ -589,13 +589,13 @@ template <int D, int G, bool KV8>
 static hipError_t launch_dgk(const AttnDecArgs& a, int B, int nsplit, hipStream_t st) {
     if constexpr (G <= 2) {
         const int items = B * a.nkv * nsplit;
-        hipLaunchKernelGGL((attn_decode_wave_kernel<D, G, KV8>), dim3((items + 3) / 4), dim3(256), 0, st, a, nsplit);
+        FP_LAUNCH((attn_decode_wave_kernel<D, G, KV8>), dim3((items + 3) / 4), dim3(256), 0, st, a, nsplit);
     } else {
-        hipLaunchKernelGGL((attn_decode_kernel<D, G, KV8>), dim3(nsplit, a.nkv, B), dim3(256), 0, st, a);
+        FP_LAUNCH((attn_decode_kernel<D, G, KV8>), dim3(nsplit, a.nkv, B), dim3(256), 0, st, a);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || nsplit == 1 || a.skip_merge) return e;
-    hipLaunchKernelGGL(attn_merge_kernel<D>, dim3(a.nh, B), dim3(D), 0, st, a, nsplit);
+    FP_LAUNCH(attn_merge_kernel<D>, dim3(a.nh, B), dim3(D), 0, st, a, nsplit);
     return hipGetLastError();
 }
 

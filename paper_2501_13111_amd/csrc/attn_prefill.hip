@@ -200,8 +200,8 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st) {
     const int nqt = (a.P + 63) / 64;
     dim3 grid(nqt, a.nh, B);
-    if (a.d == 128) hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, dim3(256), 0, st, a);
-    else if (a.d == 64) hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, dim3(256), 0, st, a);
+    if (a.d == 128) FP_LAUNCH(attn_prefill_kernel<128>, grid, dim3(256), 0, st, a);
+    else if (a.d == 64) FP_LAUNCH(attn_prefill_kernel<64>, grid, dim3(256), 0, st, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }

@@ -31,6 +31,8 @@
 
 using namespace fpk;
 
+thread_local LaunchTimer fpk::g_launch_timer;
+
 namespace {
 
 thread_local std::string g_err;
@@ -84,34 +86,39 @@ struct LayerW {
     Mat qkv, o, gu, down;
 };
 
-// Event marks around each launch of a profiled step.
+// Kernel-timed intervals of a profiled step: mark() opens an interval of the given kind,
+// and the launches enqueued until the next mark() or end() stamp its start / stop
+// events from their own dispatches (FP_LAUNCH).
 struct Prof {
-    std::vector<hipEvent_t> ev;
+    std::vector<hipEvent_t> t0, t1;
     std::vector<int> kind, layer;
     hipStream_t st = nullptr;
     bool on = false;
     void mark(int k, int l) {
         if (!on) return;
-        hipEvent_t e;
-        if (hipEventCreate(&e) != hipSuccess) return;
-        (void)hipEventRecord(e, st);
-        ev.push_back(e);
+        hipEvent_t a = nullptr, b = nullptr;
+        if (hipEventCreate(&a) != hipSuccess) return;
+        if (hipEventCreate(&b) != hipSuccess) {
+            (void)hipEventDestroy(a);
+            return;
+        }
+        t0.push_back(a);
+        t1.push_back(b);
         kind.push_back(k);
         layer.push_back(l);
+        g_launch_timer.start = a;
+        g_launch_timer.stop = b;
     }
-    void end() {
-        if (!on) return;
-        hipEvent_t e;
-        if (hipEventCreate(&e) != hipSuccess) return;
-        (void)hipEventRecord(e, st);
-        ev.push_back(e);
-    }
+    void end() { g_launch_timer = LaunchTimer{}; }
     void clear() {
-        for (auto e : ev) (void)hipEventDestroy(e);
-        ev.clear();
+        for (auto e : t0) (void)hipEventDestroy(e);
+        for (auto e : t1) (void)hipEventDestroy(e);
+        t0.clear();
+        t1.clear();
         kind.clear();
         layer.clear();
         on = false;
+        g_launch_timer = LaunchTimer{};
     }
 };
 
@@ -795,9 +802,9 @@ static fp_status collect_profile(fp_layer* h, fp_kernel_time* out, int32_t cap, 
     fp_status rc = FP_OK;
     if (hipStreamSynchronize(h->prof.st) != hipSuccess) rc = fail(FP_ERR_HIP, "profile synchronise failed");
     int n = 0;
-    for (size_t i = 0; rc == FP_OK && i + 1 < h->prof.ev.size(); ++i) {
+    for (size_t i = 0; rc == FP_OK && i < h->prof.t0.size(); ++i) {
         float ms = 0.f;
-        if (hipEventElapsedTime(&ms, h->prof.ev[i], h->prof.ev[i + 1]) != hipSuccess) {
+        if (hipEventElapsedTime(&ms, h->prof.t0[i], h->prof.t1[i]) != hipSuccess) {
             rc = fail(FP_ERR_HIP, "event timing failed");
             break;
         }

@@ -1,9 +1,32 @@
 // Internal interface between the host runtime (fp_host.cpp) and the kernels.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace fpk {
+
+// Per-kernel timing of a profiled step.  While a timer is armed on the calling thread,
+// each launch stamps the stop event with its own end of execution, and the first launch
+// after arming stamps the start event with its own start (hipExtLaunchKernel takes both
+// from the dispatch itself), so an interval covers kernel execution only, not the
+// queue gaps around it.
+struct LaunchTimer {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+extern thread_local LaunchTimer g_launch_timer;
+
+#define FP_LAUNCH(kern, grid, block, shmem, st, ...)                                           \
+    do {                                                                                       \
+        if (::fpk::g_launch_timer.stop) {                                                      \
+            hipExtLaunchKernelGGL(kern, grid, block, shmem, st, ::fpk::g_launch_timer.start,   \
+                                  ::fpk::g_launch_timer.stop, 0, __VA_ARGS__);                 \
+            ::fpk::g_launch_timer.start = nullptr;                                             \
+        } else {                                                                               \
+            hipLaunchKernelGGL(kern, grid, block, shmem, st, __VA_ARGS__);                     \
+        }                                                                                      \
+    } while (0)
 
 enum WFmt { W_BF16 = 0, W_INT8 = 1, W_INT4 = 2 };
 enum Epi { EPI_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };

@@ -231,9 +231,9 @@ static hipError_t launch_w(const GemmArgs& a, int epi, hipStream_t st) {
     const int nt = (epi == EPI_SWIGLU) ? (a.F + 63) / 64 : (a.N + GBN - 1) / GBN;
     dim3 grid(nt, (a.M + GBM - 1) / GBM);
     switch (epi) {
-        case EPI_F32: hipLaunchKernelGGL((gemm_kernel<WF, EPI_F32>), grid, dim3(256), 0, st, a); break;
-        case EPI_RESID: hipLaunchKernelGGL((gemm_kernel<WF, EPI_RESID>), grid, dim3(256), 0, st, a); break;
-        case EPI_SWIGLU: hipLaunchKernelGGL((gemm_kernel<WF, EPI_SWIGLU>), grid, dim3(256), 0, st, a); break;
+        case EPI_F32: FP_LAUNCH((gemm_kernel<WF, EPI_F32>), grid, dim3(256), 0, st, a); break;
+        case EPI_RESID: FP_LAUNCH((gemm_kernel<WF, EPI_RESID>), grid, dim3(256), 0, st, a); break;
+        case EPI_SWIGLU: FP_LAUNCH((gemm_kernel<WF, EPI_SWIGLU>), grid, dim3(256), 0, st, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -128,7 +128,7 @@ __global__ void __launch_bounds__(256) tile_kernel(const uint8_t* __restrict__ s
 hipError_t launch_tile(const void* src, int n, int K, int ebits, int KS, void* dst, int row0, hipStream_t st) {
     const int nst = (K + KS - 1) / KS;
     const int64_t total = (int64_t)(n / 16) * nst * 64;
-    hipLaunchKernelGGL(tile_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
+    FP_LAUNCH(tile_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
                        (const uint8_t*)src, n, K, ebits, KS, (uint8_t*)dst, row0);
     return hipGetLastError();
 }
@@ -138,14 +138,14 @@ hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint64_t key, float mean, 
     if (n <= 0) return hipSuccess;
     int64_t blocks = (n + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(fill_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, st, dst, n, key, mean,
+    FP_LAUNCH(fill_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, st, dst, n, key, mean,
                        sigma);
     return hipGetLastError();
 }
 
 hipError_t launch_quant_int8(const uint16_t* w, int N, int K, int8_t* codes, uint16_t* scales,
                              hipStream_t st) {
-    hipLaunchKernelGGL(quant_int8_rows_kernel, dim3(N), dim3(256), 0, st, w, K, codes, scales);
+    FP_LAUNCH(quant_int8_rows_kernel, dim3(N), dim3(256), 0, st, w, K, codes, scales);
     return hipGetLastError();
 }
 
@@ -153,7 +153,7 @@ hipError_t launch_quant_int4(const uint16_t* w, int N, int K, uint32_t* codes, u
                              uint16_t* zeros, hipStream_t st) {
     const int64_t groups = (int64_t)N * (K / 128);
     const int64_t blocks = (groups + 3) / 4;
-    hipLaunchKernelGGL(quant_int4_kernel, dim3((unsigned)blocks), dim3(256), 0, st, w, N, K, codes,
+    FP_LAUNCH(quant_int4_kernel, dim3((unsigned)blocks), dim3(256), 0, st, w, N, K, codes,
                        scales, zeros);
     return hipGetLastError();
 }

@@ -188,7 +188,7 @@ __global__ void inc_pos_kernel(int* d_pos) { *d_pos += 1; }
 // ---------------------------------------------------------------- launchers
 hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, float eps, uint16_t* out,
                           int out_fmt, hipStream_t st) {
-    hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, st, x, H, g, eps, out, out_fmt);
+    FP_LAUNCH(rmsnorm_kernel, dim3(M), dim3(256), 0, st, x, H, g, eps, out, out_fmt);
     return hipGetLastError();
 }
 
@@ -196,12 +196,12 @@ hipError_t launch_resid_norm(const float* part, int ks, int M, int N, const uint
                              uint16_t* out, const uint16_t* g, float eps, uint16_t* nout, int nfmt,
                              float* ssq, int* inc_pos, hipStream_t st) {
     const int nblk = (N + RB - 1) / RB;
-    hipLaunchKernelGGL(resid_ssq_kernel, dim3(nblk, M), dim3(256), 0, st, part, ks, M, N, resid, out, ssq,
+    FP_LAUNCH(resid_ssq_kernel, dim3(nblk, M), dim3(256), 0, st, part, ks, M, N, resid, out, ssq,
                        inc_pos);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || g == nullptr) return e;
     const uint16_t* y = ks > 0 ? out : resid;
-    hipLaunchKernelGGL(norm_apply_kernel, dim3(nblk, M), dim3(256), 0, st, y, N, ssq, nblk, g, eps, nout, nfmt);
+    FP_LAUNCH(norm_apply_kernel, dim3(nblk, M), dim3(256), 0, st, y, N, ssq, nblk, g, eps, nout, nfmt);
     return hipGetLastError();
 }
 
@@ -209,25 +209,25 @@ int resid_ssq_blocks(int N) { return (N + RB - 1) / RB; }
 
 hipError_t launch_swiglu(const float* part, int ks, int M, int F, uint16_t* a, int afmt,
                          hipStream_t st) {
-    hipLaunchKernelGGL(swiglu_kernel, dim3((F + 255) / 256, M), dim3(256), 0, st, part, ks, M, F, a,
+    FP_LAUNCH(swiglu_kernel, dim3((F + 255) / 256, M), dim3(256), 0, st, part, ks, M, F, a,
                        afmt);
     return hipGetLastError();
 }
 
 hipError_t launch_rope_kv(const RopeKvArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL(rope_kv_kernel, dim3(a.M, a.nh + a.nkv), dim3(64), 0, st, a.part, a.ks, a.M,
+    FP_LAUNCH(rope_kv_kernel, dim3(a.M, a.nh + a.nkv), dim3(64), 0, st, a.part, a.ks, a.M,
                        a.T, a.nh, a.nkv, a.d, a.d_pos, a.cos_t, a.sin_t, a.max_seq, a.qout, a.kc,
                        a.vc, a.ks_out, a.vs_out, a.kv_int8, a.dump);
     return hipGetLastError();
 }
 
 hipError_t launch_set_pos(int* d_pos, int v, hipStream_t st) {
-    hipLaunchKernelGGL(set_pos_kernel, dim3(1), dim3(1), 0, st, d_pos, v);
+    FP_LAUNCH(set_pos_kernel, dim3(1), dim3(1), 0, st, d_pos, v);
     return hipGetLastError();
 }
 
 hipError_t launch_inc_pos(int* d_pos, hipStream_t st) {
-    hipLaunchKernelGGL(inc_pos_kernel, dim3(1), dim3(1), 0, st, d_pos);
+    FP_LAUNCH(inc_pos_kernel, dim3(1), dim3(1), 0, st, d_pos);
     return hipGetLastError();
 }
 

@@ -286,7 +286,7 @@ template <int WF, int MT, int NS, int XF>
 static hipError_t launch4(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
     constexpr int UNR = (WF == W_INT4) ? 2 : 4;
     const size_t lds = (size_t)a.M * (a.krange + SK_PAD) * 2;
-    hipLaunchKernelGGL((skinny_kernel<WF, MT, NS, UNR, XF>), grid, dim3(256), lds, st, a);
+    FP_LAUNCH((skinny_kernel<WF, MT, NS, UNR, XF>), grid, dim3(256), lds, st, a);
     return hipGetLastError();
 }
 
