@@ -168,6 +168,17 @@ fp_status fp_export_kv(fp_layer* layer, int32_t l, void* k, void* v, void* k_sca
 fp_status fp_set_debug_kv_dump(fp_layer* layer, void* dev_f32);
 
 /*
+ * Debug: when dev_bf16 is non-NULL, every later prefill / decode step also
+ * copies each layer's output (the bf16 hidden states it hands to the next
+ * layer, Sec. 5.1's stack of decoder layers) into dev_bf16, laid out
+ * [n_layers, B, T, hidden] with T as above; the buffer must hold
+ * n_layers*max_batch*max_prompt*hidden bf16 values and stay valid while set.
+ * Lets a test compare each layer against a reference fed that layer's own
+ * input.  NULL switches it off.  Disables graph replay while set.
+ */
+fp_status fp_set_debug_layer_dump(fp_layer* layer, void* dev_bf16);
+
+/*
  * Per-kernel timing (the Profiler of Sec. 4.2 measures latency with dummy
  * requests; this breaks one request's step down by kernel).  Runs one prefill
  * or one decode step exactly as fp_prefill / fp_decode_step do, but launches

@@ -277,6 +277,21 @@ class Fingerprint:
         self.pos = P
         return x
 
+    def prefill_layers(self, xs):
+        """Layer-by-layer teacher forcing of a prefill: layer l runs on xs[l] (a given
+        input [B, P, H] of that layer, e.g. another implementation's own) instead of on
+        layer l-1's output here.  Returns the per-layer outputs; the cache afterwards
+        holds what each layer stored from its given input."""
+        xs = [np.asarray(x, dtype=F32) for x in xs]
+        assert len(xs) == self.s.n_layers
+        B, P, H = xs[0].shape
+        assert H == self.s.hidden and P <= self.s.max_seq
+        self._reset_cache(B)
+        pos = np.arange(P)
+        ys = [self._layer(l, xs[l], pos) for l in range(self.s.n_layers)]
+        self.pos = P
+        return ys
+
     def decode(self, x):
         """One decode step: x [B, H] (the previous output fed back) -> y [B, H]."""
         assert self.pos is not None and self.pos < self.s.max_seq

@@ -76,6 +76,7 @@ def load(path: str | None = None):
         "fp_export_weight": [vp, i32, i32, vp, vp, vp],
         "fp_export_kv": [vp, i32, vp, vp, vp, vp],
         "fp_set_debug_kv_dump": [vp, vp],
+        "fp_set_debug_layer_dump": [vp, vp],
         "fp_memory_bytes": [vp, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
                             ctypes.POINTER(ctypes.c_size_t)],
         "fp_get_position": [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)],
@@ -193,6 +194,10 @@ class Fingerprint:
     def set_debug_kv_dump(self, buf=None):
         p = None if buf is None else _dev_ptr(buf, dtype_bits=32, name="dump")
         _check(load().fp_set_debug_kv_dump(self._h, p), "fp_set_debug_kv_dump")
+
+    def set_debug_layer_dump(self, buf=None):
+        p = None if buf is None else _dev_ptr(buf, dtype_bits=16, name="dump")
+        _check(load().fp_set_debug_layer_dump(self._h, p), "fp_set_debug_layer_dump")
 
     # inspection ----------------------------------------------------------
     def position(self):

@@ -154,6 +154,7 @@ struct fp_layer {
     bool prefilled = false;
     bool use_graph = true;
     float* dump = nullptr;
+    uint16_t* ldump = nullptr;      // per-layer outputs [n_layers, B, T, hidden] (debug)
     hipStream_t cap_stream = nullptr;
     std::map<std::pair<const void*, void*>, hipGraphExec_t> graphs;
     Prof prof;
@@ -408,6 +409,8 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
         if ((rc = run_gemm(h, h->act_in, W.gu, M, EPI_SWIGLU, nullptr, h->act_f, nullptr, st))) return rc;
         h->prof.mark(FP_K_DOWN, l);
         if ((rc = run_gemm(h, h->act_f, W.down, M, EPI_RESID, nullptr, out, h->hbuf, st))) return rc;
+        if (h->ldump) HIPCHK(hipMemcpyAsync(h->ldump + (size_t)l * M * s.hidden, out, (size_t)M * s.hidden * 2,
+                                            hipMemcpyDeviceToDevice, st));
     }
     h->prof.mark(FP_K_POS, -1);
     HIPCHK(launch_set_pos(h->d_pos, P, st));
@@ -498,6 +501,8 @@ fp_status enqueue_decode_single(fp_layer* h, const uint16_t* x, uint16_t* y, hip
         h->prof.mark(FP_K_RESID_NORM, l);
         HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, nullptr, s.rms_eps, nullptr, h->act_fmt,
                                  h->ssq, (l == s.n_layers - 1) ? h->d_pos : nullptr, st));
+        if (h->ldump) HIPCHK(hipMemcpyAsync(h->ldump + (size_t)l * B * s.hidden, out, (size_t)B * s.hidden * 2,
+                                            hipMemcpyDeviceToDevice, st));
     }
     h->prof.end();
     return FP_OK;
@@ -537,6 +542,8 @@ fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipS
         h->prof.mark(FP_K_RESID_NORM, l);
         HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, last ? nullptr : h->L[l + 1].attn_norm,
                                  s.rms_eps, h->act_in, h->act_fmt, h->ssq, last ? h->d_pos : nullptr, st));
+        if (h->ldump) HIPCHK(hipMemcpyAsync(h->ldump + (size_t)l * B * s.hidden, out, (size_t)B * s.hidden * 2,
+                                            hipMemcpyDeviceToDevice, st));
     }
     h->prof.end();
     return FP_OK;
@@ -770,7 +777,7 @@ fp_status fp_decode_step(fp_layer* h, const void* x, void* y, void* stream) {
     if (!h->unbacked) {
         hipStream_t st = (hipStream_t)stream;
         fp_status rc;
-        if (h->use_graph && !h->dump) {
+        if (h->use_graph && !h->dump && !h->ldump) {
             auto key = std::make_pair(x, y);
             auto it = h->graphs.find(key);
             if (it == h->graphs.end()) {
@@ -958,6 +965,12 @@ fp_status fp_export_kv(fp_layer* h, int32_t l, void* k, void* v, void* k_scales,
 fp_status fp_set_debug_kv_dump(fp_layer* h, void* dev_f32) {
     if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
     h->dump = (float*)dev_f32;
+    return FP_OK;
+}
+
+fp_status fp_set_debug_layer_dump(fp_layer* h, void* dev_bf16) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    h->ldump = (uint16_t*)dev_bf16;
     return FP_OK;
 }
 

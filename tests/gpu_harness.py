@@ -52,16 +52,20 @@ def np_to_bf16(a: np.ndarray, device="cuda"):
 
 @dataclasses.dataclass
 class ParityResult:
-    prefill_err: float
+    prefill_err: float              # end to end (all layers chained on each side)
     decode_errs: list
     prefill_err2: float = 0.0
     decode_errs2: list = dataclasses.field(default_factory=list)
+    layer_errs: list = dataclasses.field(default_factory=list)   # prefill, layer-wise teacher-forced
 
 
 def run_parity(shape, wq, kvq, B, P, S, rows=None, seed=0, graph=True, acc=np.float64,
-               oracle=None, fp=None):
+               oracle=None, fp=None, layerwise=False):
     """Prefill + S teacher-forced decode steps on the GPU and the oracle; compares
-    sequences ``rows`` (all by default).  Returns ParityResult."""
+    sequences ``rows`` (all by default).  With ``layerwise`` the GPU also dumps every
+    layer's prefill output and the oracle runs each layer on the GPU's own input of
+    that layer (``layer_errs``); decode then continues from that oracle cache.
+    Returns ParityResult."""
     import torch
     from paper_2501_13111_amd import Fingerprint, fill_normal
 
@@ -74,14 +78,28 @@ def run_parity(shape, wq, kvq, B, P, S, rows=None, seed=0, graph=True, acc=np.fl
     x = torch.empty(B * P * H, dtype=torch.bfloat16, device="cuda")
     fill_normal(x, seed, -1, fpgen.T_INPUT, 0.0, 1.0)
     y = torch.empty_like(x)
+    dump = None
+    if layerwise:
+        dump = torch.empty(shape.n_layers, B, P, H, dtype=torch.bfloat16, device="cuda")
+        fp.set_debug_layer_dump(dump)
     fp.prefill(x, y, B, P)
     torch.cuda.synchronize()
+    if layerwise:
+        fp.set_debug_layer_dump(None)
 
     orc = oracle or OracleFingerprint(shape, wq, kvq, seed, acc=acc)
     xo = np.concatenate([fpgen.prompt(seed, B, P, H, b_start=r, b_count=1) for r in rows])
     yo = orc.prefill(xo)
     yg = bf16_to_np(y).reshape(B, P, H)
     res = ParityResult(rel_inf(yg[rows], yo), [], rel_2(yg[rows], yo), [])
+    if layerwise:
+        ridx = torch.tensor(rows, device="cuda")
+        gl = [bf16_to_np(dump[l].index_select(0, ridx)).reshape(len(rows), P, H) for l in range(shape.n_layers)]
+        del dump
+        assert np.array_equal(gl[-1], yg[rows])
+        ys = orc.prefill_layers([xo] + gl[:-1])
+        res.layer_errs = [rel_inf(g, r) for g, r in zip(gl, ys)]
+        yo = ys[-1]
 
     ins = [torch.empty(B, H, dtype=torch.bfloat16, device="cuda") for _ in range(2)]
     outs = [torch.empty(B, H, dtype=torch.bfloat16, device="cuda") for _ in range(2)]

@@ -67,7 +67,8 @@ def test_weight_codes_bit_exact(wq):
 
 
 def _report(name, res):
-    log(f"{name}: prefill {res.prefill_err:.3e} (l2 {res.prefill_err2:.3e}) decode max "
+    log(f"{name}: prefill {res.prefill_err:.3e} (l2 {res.prefill_err2:.3e}) per layer "
+        f"{[f'{e:.2e}' for e in res.layer_errs]} decode max "
         f"{max(res.decode_errs) if res.decode_errs else 0:.3e}")
 
 
@@ -99,9 +100,10 @@ CASES = [
 def test_parity_reduced(case):
     name, shape, wq, kvq, B, P, S = case
     log(f"case {name}: {shape} {wq}/{kvq} B={B} P={P} S={S}")
-    res = run_parity(shape, wq, kvq, B, P, S)
+    res = run_parity(shape, wq, kvq, B, P, S, layerwise=shape.n_layers > 1)
     _report(name, res)
     assert res.prefill_err <= TOL
+    assert all(e <= TOL for e in res.layer_errs)
     assert max(res.decode_errs) <= TOL
 
 

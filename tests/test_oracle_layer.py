@@ -212,6 +212,28 @@ def test_teacher_forcing_hook_reproduces_free_run():
     assert all(np.array_equal(a, b) for a, b in zip(ys, ysb))
 
 
+@pytest.mark.parametrize("kvq", ["bf16", "int8"])
+def test_layerwise_prefill_reproduces_chain(kvq):
+    """Fed its own chain's layer inputs, the layer-by-layer prefill is the chained
+    prefill, and decode continues from the same cache."""
+    import dataclasses
+    s = SMALL
+    x = _prompt(2, 8, s.hidden)
+    one = Fingerprint(dataclasses.replace(s, n_layers=1), "bf16", kvq)   # layer 0 alone
+    y0 = one.prefill(x)
+    fp = Fingerprint(s, "bf16", kvq)
+    assert s.n_layers == 2
+    y = fp.prefill(x)
+    d = fp.decode(y[:, -1])
+    fp2 = Fingerprint(s, "bf16", kvq)
+    ys = fp2.prefill_layers([x, y0])
+    assert np.array_equal(ys[0], y0) and np.array_equal(ys[1], y)
+    assert np.array_equal(fp2.decode(y[:, -1]), d)
+    # a different input to layer 1 changes only layer 1's output
+    ys3 = Fingerprint(s, "bf16", kvq).prefill_layers([x, y0 * 0.5])
+    assert np.array_equal(ys3[0], y0) and not np.array_equal(ys3[1], y)
+
+
 def test_configs_are_the_five_workloads():
     assert set(CONFIGS) == {"tiny", "llama2-7b-bf16", "llama2-7b-int8", "llama2-13b-int4",
                             "llama2-70b-tp8-int4"}
