@@ -84,6 +84,7 @@ struct GemmArgs {
     uint16_t* out16;          // EPI_RESID: bf16 [M, N]; EPI_SWIGLU: act [M, F]
     const uint16_t* resid;    // EPI_RESID: bf16 [M, N]
     int out_fmt;              // EPI_SWIGLU activation format
+    int tiles_m, tiles_n;     // set by the launcher
 };
 
 struct RopeKvArgs {

@@ -5,7 +5,8 @@
 // Prefill (the fingerprint's time to first token, paper Sec. 5.3) runs every
 // prompt token through the projections at once, so it is a dense contraction
 // and belongs on the matrix cores.  Weight-only quantised tiles (Sec. 3.2) are
-// converted to 16-bit once per workgroup tile, amortised over its 128 rows:
+// converted to 16-bit on the way into LDS (small tiling) or per MFMA fragment
+// after the LDS read (large tiling, where LDS holds the packed codes):
 //   bf16 W: copied; A operand bf16                   (bf16 MFMA)
 //   int8 W: codes -> exact fp16; per-row scale in the epilogue    (fp16 MFMA)
 //   int4 W: fp16((q - z) * s), one rounding per weight            (fp16 MFMA)
@@ -16,9 +17,15 @@
 // Weights are read from the fragment-major layout (1 KiB blocks of 16 rows x one
 // K-step), so each 64-thread group of a tile load reads contiguous memory.
 //
-// Tile 128 x 128 x 64, 4 waves in 2 x 2, each wave 64 x 64 = 4 x 4 MFMA 16x16x32
-// tiles; the next K tile is loaded into registers while the current one is
-// multiplied out of LDS.
+// Two tilings:
+//  * small problems (few 256 x 256 tiles): 128 x 128 x 64 tiles, 4 waves in 2 x 2,
+//    each 64 x 64 = 4 x 4 MFMA 16x16x32 tiles; the next K tile is loaded into
+//    registers (and dequantised) while the current one is multiplied out of LDS;
+//  * large problems: 256 x 256 tiles, 8 waves in 2 x 4, each 128 x 64, operands
+//    copied global -> LDS by the LDS-DMA path, two LDS stages.
+// Both map workgroups to tiles XCD-aware: workgroups are dealt to the 8 XCDs
+// round-robin, and each XCD takes a contiguous range of a grouped raster so its
+// L2 sees the same A row tiles and weight column tiles again.
 #include "fp_device.h"
 #include "fp_internal.h"
 
@@ -30,14 +37,29 @@ constexpr int GLD = GBK + GPAD;   // LDS row (u16)
 template <int WF, int EPI>
 __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
-    __shared__ __attribute__((aligned(16))) uint16_t As[GBM * GLD];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[GBN * GLD];
+    __shared__ __attribute__((aligned(16))) uint16_t Asb[2][GBM * GLD];
+    __shared__ __attribute__((aligned(16))) uint16_t Bsb[2][GBN * GLD];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int wm = w >> 1, wn = w & 1;
-    const int m0 = blockIdx.y * GBM;
-    const int nb = blockIdx.x;
+    // tile of this workgroup: XCD-aware, grouped raster.  Workgroups are dealt to the
+    // 8 XCDs round-robin; each XCD takes a contiguous range of the grouped tile order
+    // so that its L2 sees the same A row tiles and B column tiles again.
+    int mt, nb;
+    {
+        const int T = a.tiles_m * a.tiles_n, bid = blockIdx.x;
+        const int x = bid & 7, j = bid >> 3, q = T >> 3, rm = T & 7;
+        const int t = x * q + (x < rm ? x : rm) + j;
+        const int GM = 8;
+        const int grp = t / (GM * a.tiles_n);
+        const int gm0 = grp * GM;
+        const int gsz = min(GM, a.tiles_m - gm0);
+        const int tt = t - grp * GM * a.tiles_n;
+        mt = gm0 + tt % gsz;
+        nb = tt / gsz;
+    }
+    const int m0 = mt * GBM;
 
     // global row of B-tile row lr (plain: n0 + lr; dual: gate / up rows of 64 f's)
     auto brow = [&](int lr, bool& valid) -> int {
@@ -111,7 +133,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
             }
         }
     };
-    auto store_tile = [&]() {
+    auto store_tile = [&](uint16_t* As, uint16_t* Bs) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int c = tid + 256 * i;
@@ -159,9 +181,11 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
 
     const int nk = (a.K + GBK - 1) / GBK;
     load_tile(0);
-    store_tile();
+    store_tile(Asb[0], Bsb[0]);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
+        const uint16_t* As = Asb[kt & 1];
+        const uint16_t* Bs = Bsb[kt & 1];
         if (kt + 1 < nk) load_tile((kt + 1) * GBK);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
@@ -177,11 +201,8 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = mfma16<AF>(af[i], bf[j], acc[i][j]);
         }
+        if (kt + 1 < nk) store_tile(Asb[(kt + 1) & 1], Bsb[(kt + 1) & 1]);
         __syncthreads();
-        if (kt + 1 < nk) {
-            store_tile();
-            __syncthreads();
-        }
     }
 
     // ---- epilogue
@@ -228,24 +249,280 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
 
 template <int WF>
 static hipError_t launch_w(const GemmArgs& a, int epi, hipStream_t st) {
-    const int nt = (epi == EPI_SWIGLU) ? (a.F + 63) / 64 : (a.N + GBN - 1) / GBN;
-    dim3 grid(nt, (a.M + GBM - 1) / GBM);
+    GemmArgs b = a;
+    b.tiles_n = (epi == EPI_SWIGLU) ? (a.F + 63) / 64 : (a.N + GBN - 1) / GBN;
+    b.tiles_m = (a.M + GBM - 1) / GBM;
+    dim3 grid(b.tiles_n * b.tiles_m);
     switch (epi) {
-        case EPI_F32: FP_LAUNCH((gemm_kernel<WF, EPI_F32>), grid, dim3(256), 0, st, a); break;
-        case EPI_RESID: FP_LAUNCH((gemm_kernel<WF, EPI_RESID>), grid, dim3(256), 0, st, a); break;
-        case EPI_SWIGLU: FP_LAUNCH((gemm_kernel<WF, EPI_SWIGLU>), grid, dim3(256), 0, st, a); break;
+        case EPI_F32: FP_LAUNCH((gemm_kernel<WF, EPI_F32>), grid, dim3(256), 0, st, b); break;
+        case EPI_RESID: FP_LAUNCH((gemm_kernel<WF, EPI_RESID>), grid, dim3(256), 0, st, b); break;
+        case EPI_SWIGLU: FP_LAUNCH((gemm_kernel<WF, EPI_SWIGLU>), grid, dim3(256), 0, st, b); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st) {
+hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st) {
     switch (wf) {
         case W_BF16: return launch_w<W_BF16>(a, epi, st);
         case W_INT8: return launch_w<W_INT8>(a, epi, st);
         case W_INT4: return launch_w<W_INT4>(a, epi, st);
         default: return hipErrorInvalidValue;
     }
+}
+
+
+// ---------------------------------------------------------------------------
+// Large prefill GEMMs: 256 x 256 tiles, 8 waves of 128 x 64 (8 x 4 MFMA tiles),
+// operands copied global -> LDS by the LDS-DMA path (global_load_lds, 16 B per
+// lane), two LDS stages.  A rows are stored with an XOR swizzle of their 16-byte
+// chunks so that MFMA fragment reads are free of bank conflicts; weight blocks
+// keep their fragment-major order, so a fragment is one contiguous 1 KiB read.
+// Quantised weights stay packed in LDS and are converted to fp16 per fragment.
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+__device__ u32x4 g_zero16;       // source of the zero fill for out-of-range chunks
+
+constexpr int BT = 256;
+template <int WF>
+struct BigT {
+    static constexpr int TK = (WF == W_INT4) ? 128 : 64;                             // k per stage
+    static constexpr int KSW = (WF == W_BF16) ? 32 : (WF == W_INT8 ? 64 : 128);     // weight K-step
+    static constexpr int NBLK = TK / KSW;                                            // blocks per row-block per stage
+    static constexpr int A_BYTES = BT * TK * 2;
+    static constexpr int B_BYTES = 16 * NBLK * 1024;
+    static constexpr int STAGE = A_BYTES + B_BYTES;
+    static constexpr int CPR = TK / 8;                                               // 16-byte chunks per A row
+    static constexpr int NSUB = TK / 32;                                             // MFMA k-steps per stage
+};
+
+template <int CPR>
+__device__ __forceinline__ int a_swz(int row) { return CPR == 8 ? ((row >> 1) & 7) : (row & 15); }
+
+template <int WF, int EPI>
+__global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
+    using T = BigT<WF>;
+    constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
+    constexpr bool DUAL = EPI == EPI_SWIGLU;
+    __shared__ __attribute__((aligned(1024))) char smem[2 * T::STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int wm = w >> 2, wn = w & 3;      // 2 x 4 waves, each 128 x 64
+    int mt, nt;
+    {
+        const int Tn = a.tiles_m * a.tiles_n, bid = blockIdx.x;
+        const int x = bid & 7, j = bid >> 3, q = Tn >> 3, rm = Tn & 7;
+        const int t = x * q + (x < rm ? x : rm) + j;
+        const int GM = 8;
+        const int grp = t / (GM * a.tiles_n);
+        const int gm0 = grp * GM;
+        const int gsz = min(GM, a.tiles_m - gm0);
+        const int tt = t - grp * GM * a.tiles_n;
+        mt = gm0 + tt % gsz;
+        nt = tt / gsz;
+    }
+    const int m0 = mt * BT;
+    const int nrb = DUAL ? a.F / 16 : (a.N + 15) / 16;    // valid (gate) row-blocks
+
+    // global row-block of LDS row-block rb
+    auto grow_block = [&](int rb, bool& v) -> int {
+        if constexpr (DUAL) {
+            const int fb = nt * 8 + (rb & 7);
+            v = fb < nrb;
+            return rb < 8 ? fb : nrb + fb;
+        } else {
+            const int b = nt * 16 + rb;
+            v = b < nrb;
+            return b;
+        }
+    };
+    // LDS row-block of this wave's column tile j
+    auto col_rb = [&](int j) -> int {
+        if constexpr (DUAL) return j < 2 ? wn * 2 + j : 8 + wn * 2 + (j - 2);
+        else return wn * 4 + j;
+    };
+
+    float nsc[4], nzz[4], csc[4], czz[4];
+    auto issue = [&](int stage, int k0) {
+        char* sA = smem + stage * T::STAGE;
+        char* sB = sA + T::A_BYTES;
+        constexpr int NA = BT * T::CPR / 512;
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int p = (i * 8 + w) * 64 + lane;
+            const int row = p / T::CPR, slot = p % T::CPR;
+            const int chunk = slot ^ a_swz<T::CPR>(row);
+            const int m = m0 + row, k = k0 + chunk * 8;
+            const void* src = (m < a.M && k < a.K) ? (const void*)(a.X + (int64_t)m * a.K + k) : (const void*)&g_zero16;
+            __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(sA + (i * 8 + w) * 1024), 16, 0, 0);
+        }
+        constexpr int NB = 16 * T::NBLK / 8;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int blk = i * 8 + w;
+            const int rb = blk / T::NBLK, kb = blk % T::NBLK;
+            bool v;
+            const int gb = grow_block(rb, v);
+            const int kblk = k0 / T::KSW + kb;
+            v = v && kblk < a.kst;
+            const void* src = v ? (const void*)((const char*)a.W + (((int64_t)gb * a.kst + kblk) * 64 + lane) * 16)
+                                : (const void*)&g_zero16;
+            __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(sB + blk * 1024), 16, 0, 0);
+        }
+        if constexpr (WF == W_INT4) {
+            const int grp = k0 / 128, ng = a.K / 128;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                bool v;
+                const int gb = grow_block(col_rb(j), v);
+                nsc[j] = 0.f;
+                nzz[j] = 0.f;
+                if (v) {
+                    const int64_t n = (int64_t)gb * 16 + r;
+                    nsc[j] = h2f(a.scales[n * ng + grp]);
+                    nzz[j] = h2f(a.zeros[n * ng + grp]);
+                }
+            }
+        }
+    };
+
+    f32x4 acc[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](int stage) {
+        const char* sA = smem + stage * T::STAGE;
+        const char* sB = sA + T::A_BYTES;
+        u32x4 raw[4];
+        if constexpr (WF != W_BF16) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) raw[j] = *(const u32x4*)(sB + col_rb(j) * 1024 + lane * 16);
+        }
+#pragma unroll
+        for (int s = 0; s < T::NSUB; ++s) {
+            u32x4 af[8], bop[4];
+            int chunk;
+            if constexpr (WF == W_BF16) chunk = 4 * s + g;
+            else if constexpr (WF == W_INT8) chunk = 2 * g + s;
+            else chunk = 4 * g + s;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int row = wm * 128 + 16 * i + r;
+                af[i] = *(const u32x4*)(sA + row * (T::CPR * 16) + ((chunk ^ a_swz<T::CPR>(row)) * 16));
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if constexpr (WF == W_BF16) {
+                    bop[j] = *(const u32x4*)(sB + (col_rb(j) * 2 + s) * 1024 + lane * 16);
+                } else if constexpr (WF == W_INT8) {
+                    const uint32_t lo = s ? raw[j].z : raw[j].x, hi = s ? raw[j].w : raw[j].y;
+                    const u32x2 c0 = i8x4_to_f16x4(lo), c1 = i8x4_to_f16x4(hi);
+                    bop[j] = u32x4{c0.x, c0.y, c1.x, c1.y};
+                } else {
+                    const uint32_t wd = s == 0 ? raw[j].x : (s == 1 ? raw[j].y : (s == 2 ? raw[j].z : raw[j].w));
+                    const _Float16 bz = (_Float16)(1024.0f + czz[j]);
+                    const f16x2 bias = {bz, bz};
+                    const _Float16 sh = (_Float16)csc[j];
+                    const f16x2 s2 = {sh, sh};
+                    const u32x4 q = i4x8_to_f16x8(wd, bias);
+                    bop[j] = u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = mfma16<AF>(af[i], bop[j], acc[i][j]);
+        }
+    };
+
+    const int nk = (a.K + T::TK - 1) / T::TK;
+    issue(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        if constexpr (WF == W_INT4) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) { csc[j] = nsc[j]; czz[j] = nzz[j]; }
+        }
+        if (kt + 1 < nk) issue((kt + 1) & 1, (kt + 1) * T::TK);
+        compute(kt & 1);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    }
+
+    // ---- epilogue
+    if constexpr (DUAL) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int f = nt * 128 + wn * 32 + 16 * j + r;
+            if (f >= a.F) continue;
+            float sg = 1.f, su = 1.f;
+            if constexpr (WF == W_INT8) {
+                sg = h2f(a.scales[f]);
+                su = h2f(a.scales[a.F + f]);
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int m = m0 + wm * 128 + 16 * i + 4 * g + e;
+                    if (m >= a.M) continue;
+                    const float gv = acc[i][j][e] * sg, uv = acc[i][j + 2][e] * su;
+                    a.out16[(int64_t)m * a.F + f] = act_store(bfround(silu_f(gv) * uv), a.out_fmt);
+                }
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = nt * 256 + wn * 64 + 16 * j + r;
+            if (n >= a.N) continue;
+            float sn = 1.f;
+            if constexpr (WF == W_INT8) sn = h2f(a.scales[n]);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int m = m0 + wm * 128 + 16 * i + 4 * g + e;
+                    if (m >= a.M) continue;
+                    const float v = acc[i][j][e] * sn;
+                    if constexpr (EPI == EPI_F32) a.out32[(int64_t)m * a.N + n] = v;
+                    else a.out16[(int64_t)m * a.N + n] = f2bf(bf2f(a.resid[(int64_t)m * a.N + n]) + v);
+                }
+        }
+    }
+}
+
+template <int WF>
+static hipError_t launch_big(const GemmArgs& a, int epi, hipStream_t st) {
+    GemmArgs b = a;
+    b.tiles_n = (epi == EPI_SWIGLU) ? (a.F + 127) / 128 : (a.N + BT - 1) / BT;
+    b.tiles_m = (a.M + BT - 1) / BT;
+    dim3 grid(b.tiles_n * b.tiles_m);
+    switch (epi) {
+        case EPI_F32: FP_LAUNCH((gemm_big_kernel<WF, EPI_F32>), grid, dim3(512), 0, st, b); break;
+        case EPI_RESID: FP_LAUNCH((gemm_big_kernel<WF, EPI_RESID>), grid, dim3(512), 0, st, b); break;
+        case EPI_SWIGLU: FP_LAUNCH((gemm_big_kernel<WF, EPI_SWIGLU>), grid, dim3(512), 0, st, b); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_big(const GemmArgs& a, int wf, int epi, hipStream_t st) {
+    switch (wf) {
+        case W_BF16: return launch_big<W_BF16>(a, epi, st);
+        case W_INT8: return launch_big<W_INT8>(a, epi, st);
+        case W_INT4: return launch_big<W_INT4>(a, epi, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st) {
+    const int tiles = ((a.M + BT - 1) / BT) * ((epi == EPI_SWIGLU) ? (a.F + 127) / 128 : (a.N + BT - 1) / BT);
+    if (tiles >= 128) return launch_gemm_big(a, wf, epi, st);
+    return launch_gemm_small(a, wf, epi, st);
 }
 
 }  // namespace fpk
