@@ -268,6 +268,9 @@ def main():
     pflops = prefill_flops(s, B, Pp)
     proj_flops = s.n_layers * 2 * B * Pp * sum(N * K for N, K in proj_dims(s).values())
     kinds_us = {k: round(1e3 * statistics.fmean(v), 2) for k, v in sorted(by_kind.items())}
+    pre_kinds = {}
+    for kind, _, ms in pre_prof:
+        pre_kinds[kind] = pre_kinds.get(kind, 0.0) + ms
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1,
@@ -289,6 +292,7 @@ def main():
         "tokens_per_s_incl_prefill": round(B * S * args.steps / (sum(prefill_ms) / 1e3 + dec_total_s), 2),
         "roofline": roof,
         "decode_kernel_us": kinds_us,
+        "prefill_kernel_ms": {k: round(v, 4) for k, v in sorted(pre_kinds.items())},
     }
     fp.close()
     if not args.no_cpu_baseline:

@@ -5,11 +5,14 @@
 //
 // Flash-style on bf16 MFMA 16x16x32, written in the transposed form
 //     S^T = K Q^T          (A = key rows from LDS, B = the wave's 16 queries)
-//     O^T += V^T P^T       (A = value columns from a transposed LDS tile,
-//                           B = the probabilities already in the lanes)
+//     O^T += V^T P^T       (A = value columns, B = the probabilities already in
+//                           the lanes)
 // so the probabilities never leave registers: after S^T, lane (q, g) holds the
 // scores of keys 16t + 4g + i for its query column q, which are exactly the 8
-// k-values it must supply as B for a 32-key MFMA step (subtiles t, t+1).
+// k-values it must supply as B for a 32-key MFMA step (subtiles t, t+1).  The
+// value cache is stored transposed in 32-position blocks whose slots follow that
+// order (vt_slot), so the value tile is copied into LDS as it is and each A
+// fragment is one contiguous 16-byte LDS read.
 // Online softmax per query column (max / sum across the 4 lane groups by
 // shuffles).  int8 caches: codes are exact in bf16; s_k scales the scores and
 // s_v the probabilities.  Workgroup = 4 waves x 16 queries of one head; key
@@ -62,31 +65,47 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
     for (int dd = 0; dd < D / 16; ++dd) oacc[dd] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    const int64_t crow0 = ((int64_t)b * a.nkv + kvh) * a.max_seq;   // cache row of position 0
+    const int64_t crow0 = ((int64_t)b * a.nkv + kvh) * a.kv_stride; // key row of position 0
+    const int64_t vblk0 = ((int64_t)b * a.nkv + kvh) * a.nblk;      // value block of position 0
     const int kend = min(a.P, p0 + 64);
     const int ntiles = (kend + KT - 1) / KT;
     for (int kt = 0; kt < ntiles; ++kt) {
         __syncthreads();
-        // ---- stage K (row-major) and V (transposed) tiles, bf16
+        // ---- stage the K tile (row-major) and the two value blocks of the tile, bf16
         if (a.kv_int8) {
-            constexpr int CPR = D / 16;            // 16-code chunks per row
+            constexpr int CPR = D / 16;            // 16-code chunks per key row
             for (int c = tid; c < KT * CPR; c += 256) {
                 const int key = c / CPR, dc = (c % CPR) * 16;
                 const int kpos = kt * KT + key;
-                u32x4 kr = u32x4{0u, 0u, 0u, 0u}, vr = u32x4{0u, 0u, 0u, 0u};
-                if (kpos < a.P) {
-                    kr = *(const u32x4*)((const int8_t*)a.kc + (crow0 + kpos) * D + dc);
-                    vr = *(const u32x4*)((const int8_t*)a.vc + (crow0 + kpos) * D + dc);
-                }
+                u32x4 kr = u32x4{0u, 0u, 0u, 0u};
+                if (kpos < a.P) kr = *(const u32x4*)((const int8_t*)a.kc + (crow0 + kpos) * D + dc);
                 const uint32_t kw[4] = {kr.x, kr.y, kr.z, kr.w};
-                const uint32_t vw[4] = {vr.x, vr.y, vr.z, vr.w};
+                uint32_t o[8];
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const float kf = (float)(int8_t)((kw[e >> 2] >> (8 * (e & 3))) & 0xFF);
-                    const float vf = (float)(int8_t)((vw[e >> 2] >> (8 * (e & 3))) & 0xFF);
-                    Ks[key * KP + dc + e] = (uint16_t)(__float_as_uint(kf) >> 16);   // exact
-                    Vt[(dc + e) * VP + key] = (uint16_t)(__float_as_uint(vf) >> 16);
+                for (int e = 0; e < 8; ++e) {     // codes are exact in bf16
+                    const float f0 = (float)(int8_t)((kw[e >> 1] >> (16 * (e & 1))) & 0xFF);
+                    const float f1 = (float)(int8_t)((kw[e >> 1] >> (16 * (e & 1) + 8)) & 0xFF);
+                    o[e] = (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xFFFF0000u);
                 }
+                *(u32x4*)(Ks + key * KP + dc) = u32x4{o[0], o[1], o[2], o[3]};
+                *(u32x4*)(Ks + key * KP + dc + 8) = u32x4{o[4], o[5], o[6], o[7]};
+            }
+            for (int c = tid; c < 2 * D * 2; c += 256) {   // 2 blocks x D dims x 2 chunks of 16 codes
+                const int half = c & 1, dd = (c >> 1) % D, blk = c / (2 * D);
+                const int gb = 2 * kt + blk;
+                u32x4 vr = u32x4{0u, 0u, 0u, 0u};
+                if (gb < a.nblk) vr = *(const u32x4*)((const int8_t*)a.vc + ((vblk0 + gb) * D + dd) * VT_BLK + 16 * half);
+                const uint32_t vw[4] = {vr.x, vr.y, vr.z, vr.w};
+                uint32_t o[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float f0 = (float)(int8_t)((vw[e >> 1] >> (16 * (e & 1))) & 0xFF);
+                    const float f1 = (float)(int8_t)((vw[e >> 1] >> (16 * (e & 1) + 8)) & 0xFF);
+                    o[e] = (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xFFFF0000u);
+                }
+                uint16_t* dst = Vt + dd * VP + 32 * blk + 16 * half;
+                *(u32x4*)(dst) = u32x4{o[0], o[1], o[2], o[3]};
+                *(u32x4*)(dst + 8) = u32x4{o[4], o[5], o[6], o[7]};
             }
             if (tid < KT) {
                 const int kpos = kt * KT + tid;
@@ -94,20 +113,20 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
                 vsc[tid] = kpos < a.P ? h2f(a.v_scales[crow0 + kpos]) : 0.f;
             }
         } else {
-            constexpr int CPR = D / 8;             // 8-value chunks per row
+            constexpr int CPR = D / 8;             // 8-value chunks per key row
             for (int c = tid; c < KT * CPR; c += 256) {
                 const int key = c / CPR, dc = (c % CPR) * 8;
                 const int kpos = kt * KT + key;
-                u32x4 kr = u32x4{0u, 0u, 0u, 0u}, vr = u32x4{0u, 0u, 0u, 0u};
-                if (kpos < a.P) {
-                    kr = *(const u32x4*)((const uint16_t*)a.kc + (crow0 + kpos) * D + dc);
-                    vr = *(const u32x4*)((const uint16_t*)a.vc + (crow0 + kpos) * D + dc);
-                }
+                u32x4 kr = u32x4{0u, 0u, 0u, 0u};
+                if (kpos < a.P) kr = *(const u32x4*)((const uint16_t*)a.kc + (crow0 + kpos) * D + dc);
                 *(u32x4*)(Ks + key * KP + dc) = kr;
-                const uint32_t vw[4] = {vr.x, vr.y, vr.z, vr.w};
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    Vt[(dc + e) * VP + key] = (uint16_t)((vw[e >> 1] >> (16 * (e & 1))) & 0xFFFF);
+            }
+            for (int c = tid; c < 2 * D * 4; c += 256) {   // 2 blocks x D dims x 4 chunks of 8 values
+                const int q4 = c & 3, dd = (c >> 2) % D, blk = c / (4 * D);
+                const int gb = 2 * kt + blk;
+                u32x4 vr = u32x4{0u, 0u, 0u, 0u};
+                if (gb < a.nblk) vr = *(const u32x4*)((const uint16_t*)a.vc + ((vblk0 + gb) * D + dd) * VT_BLK + 8 * q4);
+                *(u32x4*)(Vt + dd * VP + 32 * blk + 8 * q4) = vr;
             }
         }
         __syncthreads();
@@ -176,10 +195,8 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
             const u32x4 pfrag = u32x4{pb[0], pb[1], pb[2], pb[3]};
 #pragma unroll
             for (int dd = 0; dd < D / 16; ++dd) {
-                const uint16_t* vrow = Vt + (16 * dd + r) * VP + 32 * k2 + 4 * g;
-                const u32x2 lo = *(const u32x2*)(vrow);
-                const u32x2 hi = *(const u32x2*)(vrow + 16);
-                oacc[dd] = mfma_bf16(u32x4{lo.x, lo.y, hi.x, hi.y}, pfrag, oacc[dd]);
+                const u32x4 vf = *(const u32x4*)(Vt + (16 * dd + r) * VP + 32 * k2 + 8 * g);
+                oacc[dd] = mfma_bf16(vf, pfrag, oacc[dd]);
             }
         }
     }

@@ -135,19 +135,18 @@ __device__ __forceinline__ uint32_t mul_h2(uint32_t v, f16x2 s) {
     return __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, v) * s);
 }
 
-// Sum of ks partial sums p[0], p[stride], ..., added in increasing order with p[0], p[stride], ... in increasing order, four loads in flight
+// Sum of ks partial sums p[0], p[stride], ..., added in increasing order; the loads
+// are issued in batches of eight (the partials were written by the previous kernel,
+// so each batch costs one memory round trip).
 __device__ __forceinline__ float sum_parts(const float* __restrict__ p, int ks, int64_t stride) {
     float acc = 0.f;
-    int s = 0;
-    for (; s + 4 <= ks; s += 4) {
-        const float a0 = p[s * stride], a1 = p[(s + 1) * stride];
-        const float a2 = p[(s + 2) * stride], a3 = p[(s + 3) * stride];
-        acc += a0;
-        acc += a1;
-        acc += a2;
-        acc += a3;
+    for (int s = 0; s < ks; s += 8) {
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = (s + i < ks) ? p[(s + i) * stride] : 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc += v[i];
     }
-    for (; s < ks; ++s) acc += p[s * stride];
     return acc;
 }
 

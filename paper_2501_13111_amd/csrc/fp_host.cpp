@@ -214,7 +214,7 @@ fp_status validate_shape(const fp_shape* s, int wq, int kvq) {
     if (s->head_dim != 64 && s->head_dim != 128)
         return fail(FP_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", s->head_dim);
     if (!attn_decode_supported(s->head_dim, s->n_heads / s->n_kv_heads))
-        return fail(FP_ERR_UNSUPPORTED, "query group size %d not supported (1, 2, 4, 8)",
+        return fail(FP_ERR_UNSUPPORTED, "query group size %d not supported (1 to 16)",
                     s->n_heads / s->n_kv_heads);
     if (s->max_batch > 64) return fail(FP_ERR_UNSUPPORTED, "max_batch %d > 64", s->max_batch);
     if ((int64_t)s->max_batch * s->max_prompt > (1 << 24))
@@ -324,6 +324,43 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     return FP_OK;
 }
 
+// Batched decode projection: the workgroup walks its k-range in staged chunks, so the
+// split-K factor only has to fill the GPU (about TARGET_WG_B workgroups) and stays small,
+// which keeps the partial sums (ks * M * N floats) well below the weight bytes.
+#ifndef FP_TARGET_WG_B
+#define FP_TARGET_WG_B 320
+#endif
+fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, float* part,
+                           int* ks_out, hipStream_t st) {
+    SkinnyArgs a{};
+    a.X = X;
+    a.W = m.codes;
+    a.scales = m.scales;
+    a.zeros = m.zeros;
+    a.M = M;
+    a.N = m.N;
+    a.K = m.K;
+    a.kst = m.kst;
+    a.dual_F = dual_F;
+    a.part = part;
+    a.xf = XF_COPY;
+    const int KC = skinny_batch_chunk();
+    const int nch = (m.K + KC - 1) / KC;
+    const int tiles = skinny_batch_tiles(m.N, dual_F, h->wq);
+    int ks = (FP_TARGET_WG_B + tiles - 1) / tiles;
+    int kmax = nch / 4;                  // at least four chunks per workgroup
+    if (kmax < 1) kmax = 1;
+    if (ks > kmax) ks = kmax;
+    if (ks < 1) ks = 1;
+    const int per = (nch + ks - 1) / ks;
+    a.krange = per * KC;
+    ks = (nch + per - 1) / per;
+    if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
+    HIPCHK(launch_skinny_batch(a, h->wq, ks, st));
+    *ks_out = ks;
+    return FP_OK;
+}
+
 fp_status run_gemm(fp_layer* h, const uint16_t* X, const Mat& m, int M, int epi, float* out32,
                    uint16_t* out16, const uint16_t* resid, hipStream_t st) {
     GemmArgs a{};
@@ -358,6 +395,8 @@ RopeKvArgs rope_args(fp_layer* h, int l, const float* part, int ks, int M, int T
     r.cos_t = h->cos_t;
     r.sin_t = h->sin_t;
     r.max_seq = h->s.max_seq;
+    r.nblk = vt_blocks(h->s.max_seq);
+    r.kv_stride = kv_row_stride(h->s.max_seq);
     r.qout = h->q32;
     r.kc = h->kc[l];
     r.vc = h->vc[l];
@@ -396,6 +435,8 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
         aa.nkv = s.n_kv_heads;
         aa.d = s.head_dim;
         aa.max_seq = s.max_seq;
+        aa.nblk = vt_blocks(s.max_seq);
+        aa.kv_stride = kv_row_stride(s.max_seq);
         aa.scale = scale;
         aa.out = h->act_o;
         aa.out_fmt = h->act_fmt;
@@ -435,11 +476,14 @@ AttnDecArgs attn_args(fp_layer* h, int l, int ks, int B, float* dump) {
     ad.nkv = s.n_kv_heads;
     ad.d = s.head_dim;
     ad.max_seq = s.max_seq;
+    ad.nblk = vt_blocks(s.max_seq);
+    ad.kv_stride = kv_row_stride(s.max_seq);
     ad.d_pos = h->d_pos;
     ad.scale = (float)(1.0 / std::sqrt((double)s.head_dim));
     int nsplit;
     attn_decode_split(s.max_seq, B, s.n_kv_heads, s.n_heads / s.n_kv_heads, &nsplit, &ad.keys_per_split);
     ad.batch = B;
+    ad.q16 = (uint16_t*)h->q32;
     ad.ws = h->attn_ws;
     ad.out = h->act_o;
     ad.out_fmt = h->act_fmt;
@@ -469,13 +513,13 @@ fp_status enqueue_decode_single(fp_layer* h, const uint16_t* x, uint16_t* y, hip
         h->prof.mark(FP_K_QKV, l);
         if ((rc = run_skinny(h, in, W.qkv, B, 0, xq, h->part, &ks, st))) return rc;
         AttnDecArgs ad = attn_args(h, l, ks, B, dump);
-        const int nsplit = (s.max_seq + ad.keys_per_split - 1) / ad.keys_per_split;
+        const int nsw = attn_decode_partials((s.max_seq + ad.keys_per_split - 1) / ad.keys_per_split);
         XIn xo;
-        if (nsplit > 1) {               // the o projection merges the context splits
+        if (nsw > 1) {                  // the o projection merges the attention partials
             ad.skip_merge = 1;
             xo.xf = XF_MERGE;
-            xo.att_nsplit = nsplit;
-            xo.att_kps = ad.keys_per_split;
+            xo.att_nsplit = nsw;
+            xo.att_kps = 4 * ad.keys_per_split;
         }
         h->prof.mark(FP_K_ATTN, l);
         HIPCHK(launch_attn_decode(ad, B, st));
@@ -524,20 +568,20 @@ fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipS
         uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
         float* dump = h->dump ? h->dump + (size_t)l * 2 * B * h->kv_dim : nullptr;
         h->prof.mark(FP_K_QKV, l);
-        if ((rc = run_skinny(h, h->act_in, W.qkv, B, 0, XIn(), h->part, &ks, st))) return rc;
+        if ((rc = run_skinny_batch(h, h->act_in, W.qkv, B, 0, h->part, &ks, st))) return rc;
         h->prof.mark(FP_K_ATTN, l);
         HIPCHK(launch_attn_decode(attn_args(h, l, ks, B, dump), B, st));
         h->prof.mark(FP_K_O, l);
-        if ((rc = run_skinny(h, h->act_o, W.o, B, 0, XIn(), h->part, &ks, st))) return rc;
+        if ((rc = run_skinny_batch(h, h->act_o, W.o, B, 0, h->part, &ks, st))) return rc;
         h->prof.mark(FP_K_RESID_NORM, l);
         HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, in, h->hbuf, W.mlp_norm, s.rms_eps, h->act_in,
                                  h->act_fmt, h->ssq, nullptr, st));
         h->prof.mark(FP_K_GATE_UP, l);
-        if ((rc = run_skinny(h, h->act_in, W.gu, B, s.ffn, XIn(), h->part2, &ks, st))) return rc;
+        if ((rc = run_skinny_batch(h, h->act_in, W.gu, B, s.ffn, h->part2, &ks, st))) return rc;
         h->prof.mark(FP_K_SWIGLU, l);
         HIPCHK(launch_swiglu(h->part2, ks, B, s.ffn, h->act_f, h->act_fmt, st));
         h->prof.mark(FP_K_DOWN, l);
-        if ((rc = run_skinny(h, h->act_f, W.down, B, 0, XIn(), h->part, &ks, st))) return rc;
+        if ((rc = run_skinny_batch(h, h->act_f, W.down, B, 0, h->part, &ks, st))) return rc;
         const bool last = (l == s.n_layers - 1);
         h->prof.mark(FP_K_RESID_NORM, l);
         HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, last ? nullptr : h->L[l + 1].attn_norm,
@@ -635,16 +679,20 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     }
     maxrows = std::max<size_t>({(size_t)h->q_dim * H, (size_t)H * h->q_dim, (size_t)F * H, (size_t)H * F});
     // KV cache
-    const size_t kv_elems = (size_t)s.max_batch * s.n_kv_heads * s.max_seq * s.head_dim;
-    const size_t kv_bytes = kv_elems * (kvq == FP_KV_INT8 ? 1 : 2);
-    const size_t sc_elems = (size_t)s.max_batch * s.n_kv_heads * s.max_seq;
+    // keys [Bmax, nkv, kv_stride, d]; values in transposed blocks [Bmax, nkv, nblk, d, VT_BLK];
+    // int8 scales [Bmax, nkv, kv_stride]
+    const size_t esz = kvq == FP_KV_INT8 ? 1 : 2;
+    const size_t kvs = (size_t)kv_row_stride(s.max_seq);
+    const size_t kv_bytes = (size_t)s.max_batch * s.n_kv_heads * kvs * s.head_dim * esz;
+    const size_t v_bytes = (size_t)s.max_batch * s.n_kv_heads * vt_blocks(s.max_seq) * VT_BLK * s.head_dim * esz;
+    const size_t sc_elems = (size_t)s.max_batch * s.n_kv_heads * kvs;
     h->kc.assign(s.n_layers, nullptr);
     h->vc.assign(s.n_layers, nullptr);
     h->ksc.assign(s.n_layers, nullptr);
     h->vsc.assign(s.n_layers, nullptr);
     for (int l = 0; l < s.n_layers; ++l) {
         if ((st = dev_alloc(h, &h->kc[l], kv_bytes, &h->bytes_kv))) return bail(st);
-        if ((st = dev_alloc(h, &h->vc[l], kv_bytes, &h->bytes_kv))) return bail(st);
+        if ((st = dev_alloc(h, &h->vc[l], v_bytes, &h->bytes_kv))) return bail(st);
         if (kvq == FP_KV_INT8) {
             if ((st = alloc_t(h, &h->ksc[l], sc_elems, &h->bytes_kv))) return bail(st);
             if ((st = alloc_t(h, &h->vsc[l], sc_elems, &h->bytes_kv))) return bail(st);
@@ -662,7 +710,7 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     if ((st = alloc_t(h, &h->q32, Mmax * h->q_dim, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->part2, (size_t)KSMAX * s.max_batch * 2 * F, &h->bytes_ws))) return bail(st);
-    const size_t nch = attn_decode_chunks(s.max_seq);
+    const size_t nch = attn_decode_max_splits(s.max_seq);
     if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 4), &h->bytes_ws)))
         return bail(st);
     if ((st = alloc_t(h, &h->d_pos, 1, &h->bytes_ws))) return bail(st);
@@ -713,7 +761,7 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     }
     // zero the KV cache so exports of unwritten positions are deterministic
     for (int l = 0; l < s.n_layers; ++l) {
-        if (hipMemset(h->kc[l], 0, kv_bytes) != hipSuccess || hipMemset(h->vc[l], 0, kv_bytes) != hipSuccess)
+        if (hipMemset(h->kc[l], 0, kv_bytes) != hipSuccess || hipMemset(h->vc[l], 0, v_bytes) != hipSuccess)
             return bail(fail(FP_ERR_HIP, "kv clear failed"));
         if (kvq == FP_KV_INT8 && (hipMemset(h->ksc[l], 0, sc_elems * 2) != hipSuccess ||
                                    hipMemset(h->vsc[l], 0, sc_elems * 2) != hipSuccess))
@@ -948,16 +996,29 @@ fp_status fp_export_kv(fp_layer* h, int32_t l, void* k, void* v, void* k_scales,
     if (h->unbacked) return fail(FP_ERR_STATE, "handle has no device storage");
     if (!h->prefilled) return fail(FP_ERR_STATE, "no prefill yet");
     const fp_shape& s = h->s;
-    const size_t elems = (size_t)h->B * s.n_kv_heads * s.max_seq * s.head_dim;
     const size_t esz = h->kvq == FP_KV_INT8 ? 1 : 2;
+    const int D = s.head_dim, nblk = vt_blocks(s.max_seq);
+    const size_t kvs = (size_t)kv_row_stride(s.max_seq), nbh = (size_t)h->B * s.n_kv_heads;
     HIPCHK(hipDeviceSynchronize());
-    HIPCHK(hipMemcpy(k, h->kc[l], elems * esz, hipMemcpyDeviceToHost));
-    HIPCHK(hipMemcpy(v, h->vc[l], elems * esz, hipMemcpyDeviceToHost));
+    // keys: rows of kv_stride -> [B, nkv, max_seq, d]
+    HIPCHK(hipMemcpy2D(k, (size_t)s.max_seq * D * esz, h->kc[l], kvs * D * esz, (size_t)s.max_seq * D * esz, nbh,
+                       hipMemcpyDeviceToHost));
+    // values: transposed blocks -> [B, nkv, max_seq, d]
+    std::vector<uint8_t> vt((size_t)h->B * s.n_kv_heads * nblk * VT_BLK * D * esz);
+    HIPCHK(hipMemcpy(vt.data(), h->vc[l], vt.size(), hipMemcpyDeviceToHost));
+    uint8_t* vd = (uint8_t*)v;
+    for (size_t bh = 0; bh < (size_t)h->B * s.n_kv_heads; ++bh)
+        for (int p = 0; p < s.max_seq; ++p)
+            for (int dd = 0; dd < D; ++dd) {
+                const size_t src = ((bh * nblk + p / VT_BLK) * D + dd) * VT_BLK + vt_slot(p % VT_BLK);
+                std::memcpy(vd + ((bh * s.max_seq + p) * D + dd) * esz, vt.data() + src * esz, esz);
+            }
     if (h->kvq == FP_KV_INT8) {
         if (!k_scales || !v_scales) return fail(FP_ERR_INVALID_ARG, "scale buffers are NULL");
-        const size_t n = (size_t)h->B * s.n_kv_heads * s.max_seq;
-        HIPCHK(hipMemcpy(k_scales, h->ksc[l], n * 2, hipMemcpyDeviceToHost));
-        HIPCHK(hipMemcpy(v_scales, h->vsc[l], n * 2, hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy2D(k_scales, (size_t)s.max_seq * 2, h->ksc[l], kvs * 2, (size_t)s.max_seq * 2, nbh,
+                           hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy2D(v_scales, (size_t)s.max_seq * 2, h->vsc[l], kvs * 2, (size_t)s.max_seq * 2, nbh,
+                           hipMemcpyDeviceToHost));
     }
     return FP_OK;
 }

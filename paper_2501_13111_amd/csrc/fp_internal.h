@@ -87,13 +87,27 @@ struct GemmArgs {
     int tiles_m, tiles_n;     // set by the launcher
 };
 
+// Value cache layout: blocks of VT_BLK positions per (sequence, kv head), each stored
+// transposed as [head_dim][VT_BLK]; inside a block, position kb sits in slot
+// vt_slot(kb), the order in which the decode and prefill attention kernels supply
+// probabilities as the B operand of a 32-key MFMA step (lane group g holds keys
+// 4g..4g+3 and 16+4g..16+4g+3).  Key cache: [B, nkv, max_seq, head_dim] row-major.
+constexpr int VT_BLK = 32;
+__host__ __device__ inline int vt_slot(int kb) { return 8 * ((kb & 15) >> 2) + 4 * (kb >> 4) + (kb & 3); }
+inline int vt_blocks(int max_seq) { return (max_seq + VT_BLK - 1) / VT_BLK; }
+// Rows of the key cache (and of the int8 scales) per (sequence, kv head): max_seq
+// rounded up to whole VT_BLK blocks, so every 32-key chunk of a context can be loaded
+// without a bounds test (rows past the current length are masked, never used).
+inline int kv_row_stride(int max_seq) { return vt_blocks(max_seq) * VT_BLK; }
+
 struct RopeKvArgs {
     const float* part;        // [ks, M, Nqkv]
     int ks, M, T, nh, nkv, d;
     const int* d_pos;         // NULL -> positions start at 0
     const float* cos_t;
     const float* sin_t;
-    int max_seq;
+    int max_seq, nblk;        // nblk: value blocks per (sequence, kv head)
+    int kv_stride;            // key / scale rows per (sequence, kv head)
     float* qout;              // [M, nh*d]
     void* kc;
     void* vc;
@@ -115,13 +129,15 @@ struct AttnDecArgs {
     void* vc;
     uint16_t* k_scales;       // [B, nkv, max_seq] (int8)
     uint16_t* v_scales;
-    int kv_int8, nh, nkv, d, max_seq;
+    int kv_int8, nh, nkv, d, max_seq, nblk;
+    int kv_stride;            // key / scale rows per (sequence, kv head)
     const int* d_pos;         // current position (the new token's index)
     float scale;              // float32(1/sqrt(d))
-    int keys_per_split;       // context keys per workgroup (multiple of 64)
+    int keys_per_split;       // context keys per split (multiple of VT_BLK)
     int batch;                // B
     int skip_merge;           // leave split partials in ws (the consumer merges them)
-    float* ws;                // [B, nh, nsplit, d + 4] partials when nsplit > 1 (m at d, l at d + 1)
+    uint16_t* q16;            // [B, nh, d] rotated queries in the MFMA operand format (workspace)
+    float* ws;                // [B, nh, nsw, d + 4] workgroup partials when nsw > 1 (m at d, l at d + 1)
     uint16_t* out;            // [B, nh*d] activation format out_fmt
     int out_fmt;
 };
@@ -132,7 +148,8 @@ struct AttnPreArgs {
     const void* vc;
     const uint16_t* k_scales;
     const uint16_t* v_scales;
-    int kv_int8, P, nh, nkv, d, max_seq;
+    int kv_int8, P, nh, nkv, d, max_seq, nblk;
+    int kv_stride;            // key / scale rows per (sequence, kv head)
     float scale;
     uint16_t* out;            // [B*P, nh*d]
     int out_fmt;
@@ -169,9 +186,16 @@ int skinny_kstep(int wf);
 int skinny_max_krange(int M);
 int skinny_tiles(int N, int dual_F, int M);
 hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st);
+// Batched decode projections (XF_COPY, M <= 64): k-range walked in staged chunks of
+// skinny_batch_chunk() values; krange a multiple of it, ks * krange >= K.
+constexpr int skinny_batch_ns(int wf) { return wf == W_BF16 ? 2 : 4; }   // 16-row subtiles per wave
+int skinny_batch_tiles(int N, int dual_F, int wf);
+int skinny_batch_chunk();
+hipError_t launch_skinny_batch(const SkinnyArgs& a, int wf, int ks, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st);
 
-int attn_decode_chunks(int max_seq);
+int attn_decode_max_splits(int max_seq);
+int attn_decode_partials(int nsplit);
 void attn_decode_split(int max_seq, int B, int nkv, int group, int* nsplit, int* keys_per_split);
 bool attn_decode_supported(int d, int group);
 hipError_t launch_attn_decode(const AttnDecArgs& a, int B, hipStream_t st);

@@ -9,6 +9,8 @@
 //   rotary embedding: rotate-half pairs (i, i + d/2) with fp32 cos/sin tables
 //   KV append: bf16, or int8 with s = fp16(absmax/127), code = rint(v/s) per
 //   (sequence, position, kv head) -- the INT8 KV cache of Sec. 3.2.
+#include <algorithm>
+
 #include "fp_device.h"
 #include "fp_internal.h"
 
@@ -89,96 +91,111 @@ __global__ void __launch_bounds__(256) swiglu_kernel(const float* __restrict__ p
     a[m * (int64_t)F + f] = act_store(bfround(silu_f(gs) * us), afmt);
 }
 
-// ---------------------------------------------------------------- rotary + KV append
-// One 64-lane workgroup per (token row m, head slot).  Head slots 0..nh-1 are query
-// heads, nh..nh+nkv-1 are kv heads (K and V).  qkv = sum of ks partials [ks, M, Nqkv]
-// (columns: q heads, then k heads, then v heads).  Token m is sequence m / T at
-// position pos0 + m % T, where pos0 = *d_pos (decode) or 0 (prefill).
-// Writes rotated q (fp32, [M, nh*d]); stores K / V in the cache
-// [B, nkv, max_seq, d] as bf16 or int8 + fp16 scale [B, nkv, max_seq].
+// ---------------------------------------------------------------- rotary + KV append (prefill)
+// qkv: the projection output [M, Nqkv] fp32 (columns: q heads, then k heads, then v
+// heads); token m is sequence m / T at position m % T.
+// Rotated queries: fp32 [M, nh*d], one thread per rotation pair (i, i + d/2).
 #pragma clang fp contract(off)
-__global__ void __launch_bounds__(64) rope_kv_kernel(const float* __restrict__ part, int ks, int M,
-                                                      int T, int nh, int nkv, int d,
-                                                      const int* __restrict__ d_pos,
-                                                      const float* __restrict__ cos_t,
-                                                      const float* __restrict__ sin_t, int max_seq,
-                                                      float* __restrict__ qout, void* __restrict__ kc,
-                                                      void* __restrict__ vc,
-                                                      uint16_t* __restrict__ ks_out,
-                                                      uint16_t* __restrict__ vs_out, int kv_int8,
-                                                      float* __restrict__ dump) {
-    const int m = blockIdx.x;
-    const int slot = blockIdx.y;
-    const int lane = threadIdx.x;
+__global__ void __launch_bounds__(256) rope_q_kernel(const float* __restrict__ qkv, int M, int T, int nh,
+                                                      int nkv, int d, const float* __restrict__ cos_t,
+                                                      const float* __restrict__ sin_t, float* __restrict__ qout) {
     const int half = d / 2;
     const int Nqkv = (nh + 2 * nkv) * d;
-    const int b = m / T;
-    const int pos = (d_pos ? *d_pos : 0) + (m % T);
-    auto load = [&](int col) { return sum_parts(part + (int64_t)m * Nqkv + col, ks, (int64_t)M * Nqkv); };
-    const float* cr = cos_t + (int64_t)pos * half;
-    const float* sr = sin_t + (int64_t)pos * half;
-    if (slot < nh) {
-        const int base = slot * d;
-        for (int i = lane; i < half; i += 64) {
-            const float u = load(base + i), v = load(base + half + i);
-            const float c = cr[i], s = sr[i];
-            qout[(int64_t)m * nh * d + base + i] = __fsub_rn(__fmul_rn(u, c), __fmul_rn(v, s));
-            qout[(int64_t)m * nh * d + base + half + i] = __fadd_rn(__fmul_rn(v, c), __fmul_rn(u, s));
+    const int64_t n = (int64_t)M * nh * half;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+        const int j = (int)(i % half);
+        const int64_t mh = i / half;
+        const int h = (int)(mh % nh);
+        const int64_t m = mh / nh;
+        const int pos = (int)(m % T);
+        const float* p = qkv + m * Nqkv + (int64_t)h * d;
+        const float u = p[j], v = p[j + half];
+        const float c = cos_t[(int64_t)pos * half + j], s = sin_t[(int64_t)pos * half + j];
+        float* q = qout + m * nh * d + (int64_t)h * d;
+        q[j] = __fsub_rn(__fmul_rn(u, c), __fmul_rn(v, s));
+        q[j + half] = __fadd_rn(__fmul_rn(v, c), __fmul_rn(u, s));
+    }
+}
+
+// K / V of one block of VT_BLK prompt positions of one (sequence, kv head): rotated K
+// rows go to the key cache; V is transposed in LDS into the value-block layout
+// ([d][VT_BLK], slot vt_slot(kb)) and written out as one contiguous block.  int8:
+// s = fp16(absmax/127), code = rint(v/s) per (position, kv head), separately for K
+// and V.  Slots past the prompt are cleared.  Lane j handles dims j and j + d/2
+// (d <= 128); wave w handles positions w, w + 4, ... of the block.
+template <bool KV8>
+__global__ void __launch_bounds__(256) kv_append_kernel(const float* __restrict__ qkv, int M, int T, int nh,
+                                                         int nkv, int d, const float* __restrict__ cos_t,
+                                                         const float* __restrict__ sin_t, int kv_stride, int nblk,
+                                                         void* __restrict__ kc, void* __restrict__ vc,
+                                                         uint16_t* __restrict__ ks_out,
+                                                         uint16_t* __restrict__ vs_out, float* __restrict__ dump) {
+    __shared__ __attribute__((aligned(16))) uint16_t vt[128 * VT_BLK];
+    uint8_t* vt8 = (uint8_t*)vt;
+    const int pb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int half = d / 2;
+    const int Nqkv = (nh + 2 * nkv) * d;
+    const int kcol = nh * d + kvh * d, vcol = nh * d + nkv * d + kvh * d;
+    const int64_t crow0 = ((int64_t)b * nkv + kvh) * kv_stride;
+    const int j = lane;
+    for (int kb = w; kb < VT_BLK; kb += 4) {
+        const int pos = pb * VT_BLK + kb;
+        const int slot = vt_slot(kb);
+        if (pos >= T) {
+            if (j < half) {
+                if constexpr (KV8) { vt8[j * VT_BLK + slot] = 0; vt8[(j + half) * VT_BLK + slot] = 0; }
+                else { vt[j * VT_BLK + slot] = 0; vt[(j + half) * VT_BLK + slot] = 0; }
+            }
+            continue;
         }
-        return;
-    }
-    const int kvh = slot - nh;
-    const int kbase = nh * d + kvh * d, vbase = nh * d + nkv * d + kvh * d;
-    const int64_t cidx = (((int64_t)b * nkv + kvh) * max_seq + pos);   // (b, kvh, pos)
-    // each lane holds up to 4 rotated k and 4 v values (d <= 256)
-    float kr[4], vr[4];
-    int cnt = 0;
-    for (int i = lane; i < half; i += 64, ++cnt) {
-        const float u = load(kbase + i), v = load(kbase + half + i);
-        const float c = cr[i], s = sr[i];
-        kr[2 * cnt] = __fsub_rn(__fmul_rn(u, c), __fmul_rn(v, s));
-        kr[2 * cnt + 1] = __fadd_rn(__fmul_rn(v, c), __fmul_rn(u, s));
-        vr[2 * cnt] = load(vbase + i);
-        vr[2 * cnt + 1] = load(vbase + half + i);
-    }
-    if (dump) {
-        // [2, M, nkv, d] slice of this step: dump[0] = K, dump[1] = V
-        float* dk = dump + ((int64_t)m * nkv + kvh) * d;
-        float* dv = dump + (int64_t)M * nkv * d + ((int64_t)m * nkv + kvh) * d;
-        int c2 = 0;
-        for (int i = lane; i < half; i += 64, ++c2) {
-            dk[i] = kr[2 * c2]; dk[half + i] = kr[2 * c2 + 1];
-            dv[i] = vr[2 * c2]; dv[half + i] = vr[2 * c2 + 1];
+        const int64_t m = (int64_t)b * T + pos;
+        const float* p = qkv + m * Nqkv;
+        float k0 = 0.f, k1 = 0.f, v0 = 0.f, v1 = 0.f;
+        if (j < half) {
+            const float u = p[kcol + j], x = p[kcol + j + half];
+            const float c = cos_t[(int64_t)pos * half + j], s = sin_t[(int64_t)pos * half + j];
+            k0 = __fsub_rn(__fmul_rn(u, c), __fmul_rn(x, s));
+            k1 = __fadd_rn(__fmul_rn(x, c), __fmul_rn(u, s));
+            v0 = p[vcol + j];
+            v1 = p[vcol + j + half];
+            if (dump) {   // [2, M, nkv, d]: dump[0] = K, dump[1] = V
+                float* dk = dump + (m * nkv + kvh) * d;
+                float* dv = dump + (int64_t)M * nkv * d + (m * nkv + kvh) * d;
+                dk[j] = k0; dk[j + half] = k1;
+                dv[j] = v0; dv[j + half] = v1;
+            }
+        }
+        if constexpr (!KV8) {
+            if (j < half) {
+                uint16_t* kd = (uint16_t*)kc + (crow0 + pos) * d;
+                kd[j] = f2bf(k0); kd[j + half] = f2bf(k1);
+                vt[j * VT_BLK + slot] = f2bf(v0);
+                vt[(j + half) * VT_BLK + slot] = f2bf(v1);
+            }
+        } else {
+            const float ka = wave_max(fmaxf(fabsf(k0), fabsf(k1)));
+            const float va = wave_max(fmaxf(fabsf(v0), fabsf(v1)));
+            const uint16_t ksh = f2h(__fdiv_rn(ka, 127.0f)), vsh = f2h(__fdiv_rn(va, 127.0f));
+            const float ksf = h2f(ksh), vsf = h2f(vsh);
+            auto q8 = [](float v, float s) -> int8_t {
+                if (s == 0.f) return 0;
+                return (int8_t)(int)fminf(fmaxf(rintf(__fdiv_rn(v, s)), -127.f), 127.f);
+            };
+            if (j < half) {
+                int8_t* kd = (int8_t*)kc + (crow0 + pos) * d;
+                kd[j] = q8(k0, ksf); kd[j + half] = q8(k1, ksf);
+                vt8[j * VT_BLK + slot] = (uint8_t)q8(v0, vsf);
+                vt8[(j + half) * VT_BLK + slot] = (uint8_t)q8(v1, vsf);
+            }
+            if (j == 0) { ks_out[crow0 + pos] = ksh; vs_out[crow0 + pos] = vsh; }
         }
     }
-    if (!kv_int8) {
-        uint16_t* kd = (uint16_t*)kc + cidx * d;
-        uint16_t* vd = (uint16_t*)vc + cidx * d;
-        int c2 = 0;
-        for (int i = lane; i < half; i += 64, ++c2) {
-            kd[i] = f2bf(kr[2 * c2]); kd[half + i] = f2bf(kr[2 * c2 + 1]);
-            vd[i] = f2bf(vr[2 * c2]); vd[half + i] = f2bf(vr[2 * c2 + 1]);
-        }
-        return;
-    }
-    float ka = 0.f, va = 0.f;
-    for (int j = 0; j < 2 * cnt; ++j) { ka = fmaxf(ka, fabsf(kr[j])); va = fmaxf(va, fabsf(vr[j])); }
-    ka = wave_max(ka);
-    va = wave_max(va);
-    const uint16_t ksh = f2h(__fdiv_rn(ka, 127.0f)), vsh = f2h(__fdiv_rn(va, 127.0f));
-    const float ksf = h2f(ksh), vsf = h2f(vsh);
-    auto q8 = [](float v, float s) -> int8_t {
-        if (s == 0.f) return 0;
-        return (int8_t)(int)fminf(fmaxf(rintf(__fdiv_rn(v, s)), -127.f), 127.f);
-    };
-    int8_t* kd = (int8_t*)kc + cidx * d;
-    int8_t* vd = (int8_t*)vc + cidx * d;
-    int c2 = 0;
-    for (int i = lane; i < half; i += 64, ++c2) {
-        kd[i] = q8(kr[2 * c2], ksf); kd[half + i] = q8(kr[2 * c2 + 1], ksf);
-        vd[i] = q8(vr[2 * c2], vsf); vd[half + i] = q8(vr[2 * c2 + 1], vsf);
-    }
-    if (lane == 0) { ks_out[cidx] = ksh; vs_out[cidx] = vsh; }
+    __syncthreads();
+    const int esz = KV8 ? 1 : 2;
+    const int nchunk = d * VT_BLK * esz / 16;
+    u32x4* dst = (u32x4*)((char*)vc + (((int64_t)b * nkv + kvh) * nblk + pb) * d * VT_BLK * esz);
+    for (int c = threadIdx.x; c < nchunk; c += 256) dst[c] = ((const u32x4*)vt)[c];
 }
 #pragma clang fp contract(on)
 
@@ -215,9 +232,20 @@ hipError_t launch_swiglu(const float* part, int ks, int M, int F, uint16_t* a, i
 }
 
 hipError_t launch_rope_kv(const RopeKvArgs& a, hipStream_t st) {
-    FP_LAUNCH(rope_kv_kernel, dim3(a.M, a.nh + a.nkv), dim3(64), 0, st, a.part, a.ks, a.M,
-                       a.T, a.nh, a.nkv, a.d, a.d_pos, a.cos_t, a.sin_t, a.max_seq, a.qout, a.kc,
-                       a.vc, a.ks_out, a.vs_out, a.kv_int8, a.dump);
+    if (a.ks != 1 || a.d_pos != nullptr || a.d > 128 || a.M % a.T != 0) return hipErrorInvalidValue;
+    const int64_t pairs = (int64_t)a.M * a.nh * (a.d / 2);
+    const int nb = (int)std::min<int64_t>((pairs + 255) / 256, 8192);
+    FP_LAUNCH(rope_q_kernel, dim3(nb), dim3(256), 0, st, a.part, a.M, a.T, a.nh, a.nkv, a.d, a.cos_t, a.sin_t,
+              a.qout);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid((a.T + VT_BLK - 1) / VT_BLK, a.nkv, a.M / a.T);
+    if (a.kv_int8)
+        FP_LAUNCH(kv_append_kernel<true>, grid, dim3(256), 0, st, a.part, a.M, a.T, a.nh, a.nkv, a.d, a.cos_t,
+                  a.sin_t, a.kv_stride, a.nblk, a.kc, a.vc, a.ks_out, a.vs_out, a.dump);
+    else
+        FP_LAUNCH(kv_append_kernel<false>, grid, dim3(256), 0, st, a.part, a.M, a.T, a.nh, a.nkv, a.d, a.cos_t,
+                  a.sin_t, a.kv_stride, a.nblk, a.kc, a.vc, a.ks_out, a.vs_out, a.dump);
     return hipGetLastError();
 }
 

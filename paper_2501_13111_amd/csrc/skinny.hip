@@ -282,6 +282,209 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Batches (M > 1 tokens, one per sequence): the activation is a real M x K operand,
+// so it is not staged whole -- that would cap the k-range per workgroup at the LDS
+// size and force a split-K factor (and partial-sum traffic) that grows with M.
+// Instead the workgroup walks its k-range in chunks of 128 (one int4 group, two
+// int8 or four bf16 K-steps): the M x 128 activation chunk is staged in LDS (double
+// buffered, loaded into registers one chunk ahead) and shared by the 64 * NS weight
+// rows of the workgroup, whose fragments (and int4 scale / zero pairs) are streamed
+// into registers one chunk ahead.  The split-K factor only has to fill the GPU.
+constexpr int SB_KC = 128;              // k per staged activation chunk
+constexpr int SB_LDA = SB_KC + 8;       // LDS row stride (u16)
+
+template <int WF, int MT, int NS>
+__global__ void __launch_bounds__(256) skinny_batch_kernel(SkinnyArgs a) {
+    constexpr int KS = SkinnyTraits<WF>::KS;
+    constexpr int NJ = SkinnyTraits<WF>::NJ;
+    constexpr int SPC = SB_KC / KS;                  // K-steps per chunk
+    constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][16 * MT * SB_LDA];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int kb = blockIdx.y * a.krange;
+    const int ke = min(a.K, kb + a.krange);
+    const int nch = (ke - kb + SB_KC - 1) / SB_KC;
+
+    int row[NS];
+    bool rv[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (a.dual_F > 0) {
+            const int fw = blockIdx.x * (32 * NS) + w * (8 * NS);
+            const int f = fw + 16 * (s % (NS / 2)) + r;
+            rv[s] = f < a.dual_F;
+            row[s] = (s < NS / 2 ? 0 : a.dual_F) + f;
+        } else {
+            row[s] = blockIdx.x * (64 * NS) + w * (16 * NS) + 16 * s + r;
+            rv[s] = row[s] < a.N;
+        }
+    }
+
+    // activation chunk: 16 MT rows x 16 pieces of 8 values = MT pieces per thread
+    auto load_a = [&](int ci, u32x4* ra) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+            const int c = tid + 256 * i;
+            const int m = c >> 4, k = kb + ci * SB_KC + (c & 15) * 8;
+            ra[i] = u32x4{0u, 0u, 0u, 0u};
+            if (m < a.M && k < ke) ra[i] = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+        }
+    };
+    auto store_a = [&](uint16_t* dst, const u32x4* ra) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+            const int c = tid + 256 * i;
+            *(u32x4*)(dst + (c >> 4) * SB_LDA + (c & 15) * 8) = ra[i];
+        }
+    };
+    // weight fragments of one chunk (and the int4 scale / zero of its group)
+    auto load_w = [&](int ci, u32x4 (*wv)[NS], float* sc, float* zz) {
+        const int st0 = (kb + ci * SB_KC) / KS;
+#pragma unroll
+        for (int u = 0; u < SPC; ++u)
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                wv[u][s] = u32x4{0u, 0u, 0u, 0u};
+                if (rv[s] && ci < nch && st0 + u < a.kst)
+                    wv[u][s] = __builtin_nontemporal_load((const u32x4*)a.W + ((int64_t)(row[s] >> 4) * a.kst + st0 + u) * 64 + lane);
+            }
+        if constexpr (WF == W_INT4) {
+            const int grp = st0;
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                sc[s] = 0.f;
+                zz[s] = 0.f;
+                if (rv[s] && ci < nch) {
+                    sc[s] = h2f(a.scales[(int64_t)row[s] * (a.K / 128) + grp]);
+                    zz[s] = h2f(a.zeros[(int64_t)row[s] * (a.K / 128) + grp]);
+                }
+            }
+        }
+    };
+
+    f32x4 acc[MT][NS];
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int s = 0; s < NS; ++s) acc[t][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    u32x4 ra[MT];
+    u32x4 wc[SPC][NS], wn[SPC][NS];
+    float scc[NS], zzc[NS], scn[NS], zzn[NS];
+    load_w(0, wc, scc, zzc);
+    load_a(0, ra);
+    store_a(As[0], ra);
+    __syncthreads();
+    for (int ci = 0; ci < nch; ++ci) {
+        load_w(ci + 1, wn, scn, zzn);
+        if (ci + 1 < nch) load_a(ci + 1, ra);
+        const uint16_t* Ab = As[ci & 1];
+#pragma unroll
+        for (int u = 0; u < SPC; ++u) {
+            u32x4 bop[NJ][NS];
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                if constexpr (WF == W_BF16) {
+                    bop[0][s] = wc[u][s];
+                } else if constexpr (WF == W_INT8) {
+                    const u32x2 c0 = i8x4_to_f16x4(wc[u][s].x), c1 = i8x4_to_f16x4(wc[u][s].y);
+                    const u32x2 c2 = i8x4_to_f16x4(wc[u][s].z), c3 = i8x4_to_f16x4(wc[u][s].w);
+                    bop[0][s] = u32x4{c0.x, c0.y, c1.x, c1.y};
+                    bop[1][s] = u32x4{c2.x, c2.y, c3.x, c3.y};
+                } else {
+                    const _Float16 bz = (_Float16)(1024.0f + zzc[s]);
+                    const f16x2 bias = {bz, bz};
+                    const _Float16 sh = (_Float16)scc[s];
+                    const f16x2 s2 = {sh, sh};
+                    const uint32_t wd[4] = {wc[u][s].x, wc[u][s].y, wc[u][s].z, wc[u][s].w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const u32x4 q = i4x8_to_f16x8(wd[j], bias);
+                        bop[j][s] = u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
+                    }
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                int koff;
+                if constexpr (WF == W_BF16) koff = u * KS + 8 * g;
+                else if constexpr (WF == W_INT8) koff = u * KS + 16 * g + 8 * j;
+                else koff = 32 * g + 8 * j;
+#pragma unroll
+                for (int t = 0; t < MT; ++t) {
+                    const u32x4 av = *(const u32x4*)(Ab + (16 * t + r) * SB_LDA + koff);
+#pragma unroll
+                    for (int s = 0; s < NS; ++s) acc[t][s] = mfma16<AF>(av, bop[j][s], acc[t][s]);
+                }
+            }
+        }
+        if (ci + 1 < nch) store_a(As[(ci + 1) & 1], ra);
+#pragma unroll
+        for (int u = 0; u < SPC; ++u)
+#pragma unroll
+            for (int s = 0; s < NS; ++s) wc[u][s] = wn[u][s];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) { scc[s] = scn[s]; zzc[s] = zzn[s]; }
+        __syncthreads();
+    }
+
+    const int ncols = a.dual_F > 0 ? 2 * a.dual_F : a.N;
+    float* out = a.part + (int64_t)blockIdx.y * a.M * ncols;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (!rv[s]) continue;
+        float rs = 1.f;
+        if constexpr (WF == W_INT8) rs = h2f(a.scales[row[s]]);
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = 16 * t + 4 * g + i;
+                if (m < a.M) out[(int64_t)m * ncols + row[s]] = acc[t][s][i] * rs;
+            }
+    }
+}
+
+template <int WF, int MT>
+static hipError_t launch_batch(const SkinnyArgs& a, int ks, hipStream_t st) {
+    constexpr int NS = skinny_batch_ns(WF);
+    dim3 grid(skinny_batch_tiles(a.N, a.dual_F, WF), ks);
+    FP_LAUNCH((skinny_batch_kernel<WF, MT, NS>), grid, dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int WF>
+static hipError_t launch_batch_w(const SkinnyArgs& a, int ks, hipStream_t st) {
+    switch ((a.M + 15) / 16) {
+        case 1: return launch_batch<WF, 1>(a, ks, st);
+        case 2: return launch_batch<WF, 2>(a, ks, st);
+        case 3: return launch_batch<WF, 3>(a, ks, st);
+        case 4: return launch_batch<WF, 4>(a, ks, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+int skinny_batch_tiles(int N, int dual_F, int wf) {
+    const int ns = skinny_batch_ns(wf);
+    return dual_F > 0 ? (dual_F + 32 * ns - 1) / (32 * ns) : (N + 64 * ns - 1) / (64 * ns);
+}
+
+int skinny_batch_chunk() { return SB_KC; }
+
+hipError_t launch_skinny_batch(const SkinnyArgs& a, int wf, int ks, hipStream_t st) {
+    if (a.M < 1 || a.M > 64 || a.xf != XF_COPY || a.krange <= 0 || a.krange % SB_KC != 0) return hipErrorInvalidValue;
+    if ((int64_t)ks * a.krange < a.K || (int64_t)(ks - 1) * a.krange >= a.K) return hipErrorInvalidValue;
+    switch (wf) {
+        case W_BF16: return launch_batch_w<W_BF16>(a, ks, st);
+        case W_INT8: return launch_batch_w<W_INT8>(a, ks, st);
+        case W_INT4: return launch_batch_w<W_INT4>(a, ks, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 template <int WF, int MT, int NS, int XF>
 static hipError_t launch4(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
     constexpr int UNR = (WF == W_INT4) ? 2 : 4;
