@@ -76,6 +76,7 @@ struct Mat {
     void* codes = nullptr;        // fragment-major tiles of bf16 / int8 / int4 (device nibble order)
     uint16_t* scales = nullptr;
     uint16_t* zeros = nullptr;
+    uint32_t* sz = nullptr;       // int4: scale | zero << 16 per (row, group)
     int N = 0, K = 0;
     int kst = 0;                  // K-steps (1 KiB blocks) per 16-row block row
 };
@@ -236,6 +237,7 @@ fp_status alloc_mat(fp_layer* h, Mat* m, int N, int K) {
     if (h->wq == FP_WQ_INT8_CHANNEL) return alloc_t(h, &m->scales, (size_t)N, &h->bytes_w);
     if (h->wq == FP_WQ_INT4_G128) {
         if ((st = alloc_t(h, &m->scales, nk / 128, &h->bytes_w))) return st;
+        if ((st = alloc_t(h, &m->sz, nk / 128, &h->bytes_w))) return st;
         return alloc_t(h, &m->zeros, nk / 128, &h->bytes_w);
     }
     return FP_OK;
@@ -337,6 +339,7 @@ fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, 
     a.W = m.codes;
     a.scales = m.scales;
     a.zeros = m.zeros;
+    a.sz = m.sz;
     a.M = M;
     a.N = m.N;
     a.K = m.K;
@@ -753,6 +756,10 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
         if ((st = synth_rows(h, &W.gu, 0, F, l, FP_T_GATE, tmp, tmpq))) return bail(st);
         if ((st = synth_rows(h, &W.gu, F, F, l, FP_T_UP, tmp, tmpq))) return bail(st);
         if ((st = synth_rows(h, &W.down, 0, H, l, FP_T_DOWN, tmp, tmpq))) return bail(st);
+        if (h->wq == FP_WQ_INT4_G128) {
+            for (Mat* m : {&W.qkv, &W.o, &W.gu, &W.down})
+                if ((st = chk(launch_pack_sz(m->scales, m->zeros, (int64_t)m->N * (m->K / 128), m->sz, 0)))) return bail(st);
+        }
     }
     if (hipDeviceSynchronize() != hipSuccess) return bail(fail(FP_ERR_HIP, "weight synthesis failed"));
     for (void* p : {(void*)tmp, tmpq}) {

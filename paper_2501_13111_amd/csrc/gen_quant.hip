@@ -7,6 +7,8 @@
 // both with fp16 scales.  Quantiser arithmetic uses correctly rounded fp32
 // division, round-half-to-even and no contraction, so codes are a pure function
 // of the bf16 weights.
+#include <algorithm>
+
 #include "fp_device.h"
 #include "fp_internal.h"
 
@@ -146,6 +148,22 @@ hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint64_t key, float mean, 
 hipError_t launch_quant_int8(const uint16_t* w, int N, int K, int8_t* codes, uint16_t* scales,
                              hipStream_t st) {
     FP_LAUNCH(quant_int8_rows_kernel, dim3(N), dim3(256), 0, st, w, K, codes, scales);
+    return hipGetLastError();
+}
+
+// int4 groups: scale and zero point of each (row, group) packed into one word
+// (scale bits low, zero bits high), so a kernel fetches both with one load.
+__global__ void __launch_bounds__(256) pack_sz_kernel(const uint16_t* __restrict__ scales,
+                                                      const uint16_t* __restrict__ zeros, int64_t n,
+                                                      uint32_t* __restrict__ sz) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+        sz[i] = (uint32_t)scales[i] | ((uint32_t)zeros[i] << 16);
+}
+
+hipError_t launch_pack_sz(const uint16_t* scales, const uint16_t* zeros, int64_t n, uint32_t* sz,
+                          hipStream_t st) {
+    const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
+    FP_LAUNCH(pack_sz_kernel, dim3((unsigned)blocks), dim3(256), 0, st, scales, zeros, n, sz);
     return hipGetLastError();
 }
 

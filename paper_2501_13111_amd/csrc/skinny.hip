@@ -287,20 +287,24 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 // so it is not staged whole -- that would cap the k-range per workgroup at the LDS
 // size and force a split-K factor (and partial-sum traffic) that grows with M.
 // Instead the workgroup walks its k-range in chunks of 128 (one int4 group, two
-// int8 or four bf16 K-steps): the M x 128 activation chunk is staged in LDS (double
-// buffered, loaded into registers one chunk ahead) and shared by the 64 * NS weight
-// rows of the workgroup, whose fragments (and int4 scale / zero pairs) are streamed
-// into registers one chunk ahead.  The split-K factor only has to fill the GPU.
-constexpr int SB_KC = 128;              // k per staged activation chunk
-constexpr int SB_LDA = SB_KC + 8;       // LDS row stride (u16)
+// int8 or four bf16 K-steps).  Activation chunks are loaded into registers two
+// chunks ahead and written to one of two LDS buffers one chunk ahead (rows of 256 B,
+// 16-byte pieces XOR-swizzled by the row so MFMA fragment reads are free of bank
+// conflicts); weight fragments (and int4 scale / zero words) run two chunks ahead
+// in registers.  The workgroup synchronises with a bare s_barrier after the LDS
+// writes, so the global loads in flight are not drained at every chunk.  The
+// split-K factor only has to fill the GPU.
+constexpr int SB_KC = 128;              // k per activation chunk
+constexpr int SB_PD = 2;                // chunks of loads in flight
 
 template <int WF, int MT, int NS>
-__global__ void __launch_bounds__(256) skinny_batch_kernel(SkinnyArgs a) {
+__global__ void __launch_bounds__(256, 2) skinny_batch_kernel(SkinnyArgs a) {
     constexpr int KS = SkinnyTraits<WF>::KS;
     constexpr int NJ = SkinnyTraits<WF>::NJ;
     constexpr int SPC = SB_KC / KS;                  // K-steps per chunk
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][16 * MT * SB_LDA];
+    constexpr int ABUF = 16 * MT * 256;              // bytes of one activation chunk
+    __shared__ __attribute__((aligned(1024))) char As[2 * ABUF];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -308,6 +312,8 @@ __global__ void __launch_bounds__(256) skinny_batch_kernel(SkinnyArgs a) {
     const int ke = min(a.K, kb + a.krange);
     const int nch = (ke - kb + SB_KC - 1) / SB_KC;
 
+    // weight rows of this wave's subtiles (rows past the matrix are clamped for the
+    // loads and never stored)
     int row[NS];
     bool rv[NS];
 #pragma unroll
@@ -316,52 +322,43 @@ __global__ void __launch_bounds__(256) skinny_batch_kernel(SkinnyArgs a) {
             const int fw = blockIdx.x * (32 * NS) + w * (8 * NS);
             const int f = fw + 16 * (s % (NS / 2)) + r;
             rv[s] = f < a.dual_F;
-            row[s] = (s < NS / 2 ? 0 : a.dual_F) + f;
+            row[s] = (s < NS / 2 ? 0 : a.dual_F) + min(f, a.dual_F - 1);
         } else {
-            row[s] = blockIdx.x * (64 * NS) + w * (16 * NS) + 16 * s + r;
-            rv[s] = row[s] < a.N;
+            const int n = blockIdx.x * (64 * NS) + w * (16 * NS) + 16 * s + r;
+            rv[s] = n < a.N;
+            row[s] = min(n, a.N - 1);
         }
     }
 
-    // activation chunk: 16 MT rows x 16 pieces of 8 values = MT pieces per thread
+    // activation chunk ci: thread piece c = tid + 256 i is row c / 16, LDS slot c % 16,
+    // which holds the row's 16-byte piece slot ^ (row % 16)
     auto load_a = [&](int ci, u32x4* ra) {
 #pragma unroll
         for (int i = 0; i < MT; ++i) {
             const int c = tid + 256 * i;
-            const int m = c >> 4, k = kb + ci * SB_KC + (c & 15) * 8;
+            const int rr = c >> 4, slot = c & 15;
+            const int k = kb + ci * SB_KC + ((slot ^ (rr & 15)) * 8);
             ra[i] = u32x4{0u, 0u, 0u, 0u};
-            if (m < a.M && k < ke) ra[i] = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+            if (rr < a.M && k < ke && ci < nch) ra[i] = *(const u32x4*)(a.X + (int64_t)rr * a.K + k);
         }
     };
-    auto store_a = [&](uint16_t* dst, const u32x4* ra) {
+    auto store_a = [&](char* buf, const u32x4* ra) {
 #pragma unroll
-        for (int i = 0; i < MT; ++i) {
-            const int c = tid + 256 * i;
-            *(u32x4*)(dst + (c >> 4) * SB_LDA + (c & 15) * 8) = ra[i];
-        }
+        for (int i = 0; i < MT; ++i) *(u32x4*)(buf + (tid + 256 * i) * 16) = ra[i];
     };
-    // weight fragments of one chunk (and the int4 scale / zero of its group)
-    auto load_w = [&](int ci, u32x4 (*wv)[NS], float* sc, float* zz) {
-        const int st0 = (kb + ci * SB_KC) / KS;
+    // weight fragments of chunk ci (clamped to the last chunk past the end)
+    auto load_w = [&](int ci, u32x4 (*wv)[NS], uint32_t* sz) {
+        const int cc = min(ci, nch - 1);
+        const int st0 = (kb + cc * SB_KC) / KS;
 #pragma unroll
         for (int u = 0; u < SPC; ++u)
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                wv[u][s] = u32x4{0u, 0u, 0u, 0u};
-                if (rv[s] && ci < nch && st0 + u < a.kst)
-                    wv[u][s] = __builtin_nontemporal_load((const u32x4*)a.W + ((int64_t)(row[s] >> 4) * a.kst + st0 + u) * 64 + lane);
-            }
+            for (int s = 0; s < NS; ++s)
+                wv[u][s] = __builtin_nontemporal_load((const u32x4*)a.W +
+                                                      ((int64_t)(row[s] >> 4) * a.kst + min(st0 + u, a.kst - 1)) * 64 + lane);
         if constexpr (WF == W_INT4) {
-            const int grp = st0;
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                sc[s] = 0.f;
-                zz[s] = 0.f;
-                if (rv[s] && ci < nch) {
-                    sc[s] = h2f(a.scales[(int64_t)row[s] * (a.K / 128) + grp]);
-                    zz[s] = h2f(a.zeros[(int64_t)row[s] * (a.K / 128) + grp]);
-                }
-            }
+            for (int s = 0; s < NS; ++s) sz[s] = a.sz[(int64_t)row[s] * (a.K / 128) + st0];
         }
     };
 
@@ -371,35 +368,25 @@ __global__ void __launch_bounds__(256) skinny_batch_kernel(SkinnyArgs a) {
 #pragma unroll
         for (int s = 0; s < NS; ++s) acc[t][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    u32x4 ra[MT];
-    u32x4 wc[SPC][NS], wn[SPC][NS];
-    float scc[NS], zzc[NS], scn[NS], zzn[NS];
-    load_w(0, wc, scc, zzc);
-    load_a(0, ra);
-    store_a(As[0], ra);
-    __syncthreads();
-    for (int ci = 0; ci < nch; ++ci) {
-        load_w(ci + 1, wn, scn, zzn);
-        if (ci + 1 < nch) load_a(ci + 1, ra);
-        const uint16_t* Ab = As[ci & 1];
+    auto compute = [&](const char* Ab, const u32x4 (*wv)[NS], const uint32_t* sz) {
 #pragma unroll
         for (int u = 0; u < SPC; ++u) {
             u32x4 bop[NJ][NS];
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 if constexpr (WF == W_BF16) {
-                    bop[0][s] = wc[u][s];
+                    bop[0][s] = wv[u][s];
                 } else if constexpr (WF == W_INT8) {
-                    const u32x2 c0 = i8x4_to_f16x4(wc[u][s].x), c1 = i8x4_to_f16x4(wc[u][s].y);
-                    const u32x2 c2 = i8x4_to_f16x4(wc[u][s].z), c3 = i8x4_to_f16x4(wc[u][s].w);
+                    const u32x2 c0 = i8x4_to_f16x4(wv[u][s].x), c1 = i8x4_to_f16x4(wv[u][s].y);
+                    const u32x2 c2 = i8x4_to_f16x4(wv[u][s].z), c3 = i8x4_to_f16x4(wv[u][s].w);
                     bop[0][s] = u32x4{c0.x, c0.y, c1.x, c1.y};
                     bop[1][s] = u32x4{c2.x, c2.y, c3.x, c3.y};
                 } else {
-                    const _Float16 bz = (_Float16)(1024.0f + zzc[s]);
+                    const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(sz[s] >> 16)));
                     const f16x2 bias = {bz, bz};
-                    const _Float16 sh = (_Float16)scc[s];
+                    const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(sz[s] & 0xFFFFu));
                     const f16x2 s2 = {sh, sh};
-                    const uint32_t wd[4] = {wc[u][s].x, wc[u][s].y, wc[u][s].z, wc[u][s].w};
+                    const uint32_t wd[4] = {wv[u][s].x, wv[u][s].y, wv[u][s].z, wv[u][s].w};
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const u32x4 q = i4x8_to_f16x8(wd[j], bias);
@@ -413,22 +400,44 @@ __global__ void __launch_bounds__(256) skinny_batch_kernel(SkinnyArgs a) {
                 if constexpr (WF == W_BF16) koff = u * KS + 8 * g;
                 else if constexpr (WF == W_INT8) koff = u * KS + 16 * g + 8 * j;
                 else koff = 32 * g + 8 * j;
+                const int piece = koff >> 3;
 #pragma unroll
                 for (int t = 0; t < MT; ++t) {
-                    const u32x4 av = *(const u32x4*)(Ab + (16 * t + r) * SB_LDA + koff);
+                    const int rr = 16 * t + r;
+                    const u32x4 av = *(const u32x4*)(Ab + rr * 256 + ((piece ^ (rr & 15)) << 4));
 #pragma unroll
                     for (int s = 0; s < NS; ++s) acc[t][s] = mfma16<AF>(av, bop[j][s], acc[t][s]);
                 }
             }
         }
-        if (ci + 1 < nch) store_a(As[(ci + 1) & 1], ra);
+    };
+    // LDS writes done, then a bare barrier (no drain of the global loads in flight)
+    auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+
+    u32x4 wr[SB_PD][SPC][NS];
+    uint32_t szr[SB_PD][NS];
+    u32x4 ra[SB_PD][MT];
+    load_a(0, ra[0]);
+    load_a(1, ra[1]);
+    load_w(0, wr[0], szr[0]);
+    load_w(1, wr[1], szr[1]);
+    store_a(As, ra[0]);
+    load_a(2, ra[0]);
+    barrier();
+    for (int ci0 = 0; ci0 < nch; ci0 += SB_PD) {
 #pragma unroll
-        for (int u = 0; u < SPC; ++u)
-#pragma unroll
-            for (int s = 0; s < NS; ++s) wc[u][s] = wn[u][s];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) { scc[s] = scn[s]; zzc[s] = zzn[s]; }
-        __syncthreads();
+        for (int p = 0; p < SB_PD; ++p) {
+            const int ci = ci0 + p;
+            if (ci < nch) {
+                compute(As + p * ABUF, wr[p], szr[p]);
+                load_w(ci + SB_PD, wr[p], szr[p]);
+                // chunk ci + 1 (registers since two chunks) into the other buffer, whose
+                // last reader was chunk ci - 1 (every wave passed the barrier since)
+                store_a(As + (1 - p) * ABUF, ra[1 - p]);
+                load_a(ci + 3, ra[1 - p]);
+                barrier();
+            }
+        }
     }
 
     const int ncols = a.dual_F > 0 ? 2 * a.dual_F : a.N;
@@ -477,6 +486,7 @@ int skinny_batch_chunk() { return SB_KC; }
 hipError_t launch_skinny_batch(const SkinnyArgs& a, int wf, int ks, hipStream_t st) {
     if (a.M < 1 || a.M > 64 || a.xf != XF_COPY || a.krange <= 0 || a.krange % SB_KC != 0) return hipErrorInvalidValue;
     if ((int64_t)ks * a.krange < a.K || (int64_t)(ks - 1) * a.krange >= a.K) return hipErrorInvalidValue;
+    if (wf == W_INT4 && a.sz == nullptr) return hipErrorInvalidValue;
     switch (wf) {
         case W_BF16: return launch_batch_w<W_BF16>(a, ks, st);
         case W_INT8: return launch_batch_w<W_INT8>(a, ks, st);
@@ -487,7 +497,11 @@ hipError_t launch_skinny_batch(const SkinnyArgs& a, int wf, int ks, hipStream_t 
 
 template <int WF, int MT, int NS, int XF>
 static hipError_t launch4(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
+#ifdef SKINNY_UNR
+    constexpr int UNR = SKINNY_UNR;
+#else
     constexpr int UNR = (WF == W_INT4) ? 2 : 4;
+#endif
     const size_t lds = (size_t)a.M * (a.krange + SK_PAD) * 2;
     FP_LAUNCH((skinny_kernel<WF, MT, NS, UNR, XF>), grid, dim3(256), lds, st, a);
     return hipGetLastError();
