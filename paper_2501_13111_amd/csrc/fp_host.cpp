@@ -371,6 +371,7 @@ fp_status run_gemm(fp_layer* h, const uint16_t* X, const Mat& m, int M, int epi,
     a.W = m.codes;
     a.scales = m.scales;
     a.zeros = m.zeros;
+    a.sz = m.sz;
     a.M = M;
     a.N = m.N;
     a.K = m.K;

@@ -79,6 +79,7 @@ struct GemmArgs {
     const void* W;            // fragment-major tiles
     const uint16_t* scales;
     const uint16_t* zeros;
+    const uint32_t* sz;       // int4: scale | zero << 16 per (row, group)
     int M, N, K, F;           // F: SwiGLU width (N = 2F rows of [gate; up])
     int kst;                  // K-steps per 16-row block row of W
     float* out32;             // EPI_F32: [M, N]

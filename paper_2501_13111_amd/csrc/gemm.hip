@@ -31,13 +31,23 @@
 
 namespace fpk {
 
-constexpr int GBM = 128, GBN = 128, GBK = 64, GPAD = 8;
+constexpr int GBN = 128, GBK = 64, GPAD = 8;
+#ifndef GEMM_BIG_MIN_TILES
+#define GEMM_BIG_MIN_TILES 128   // 256 x 256 tiles from this many
+#endif
+#ifndef GEMM_SMALL_TILES
+#define GEMM_SMALL_TILES 256
+#endif
 constexpr int GLD = GBK + GPAD;   // LDS row (u16)
 
-template <int WF, int EPI>
+// BM = 128 (waves 2 x 2 of 64 x 64) or 64 (waves 2 x 2 of 32 x 64, for problems with
+// too few 128-row tiles to fill the GPU)
+template <int WF, int EPI, int BM>
 __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
-    __shared__ __attribute__((aligned(16))) uint16_t Asb[2][GBM * GLD];
+    constexpr int MI = BM / 32;                 // 16-row MFMA tiles per wave
+    constexpr int NA = BM / 32;                 // 16-byte A loads per thread per K tile
+    __shared__ __attribute__((aligned(16))) uint16_t Asb[2][BM * GLD];
     __shared__ __attribute__((aligned(16))) uint16_t Bsb[2][GBN * GLD];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -59,7 +69,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
         mt = gm0 + tt % gsz;
         nb = tt / gsz;
     }
-    const int m0 = mt * GBM;
+    const int m0 = mt * BM;
 
     // global row of B-tile row lr (plain: n0 + lr; dual: gate / up rows of 64 f's)
     auto brow = [&](int lr, bool& valid) -> int {
@@ -77,11 +87,17 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
 
     // ---- register staging of one K tile
     constexpr int BCH = (WF == W_BF16) ? 4 : (WF == W_INT8 ? 2 : 1);   // 16-byte B loads per thread
-    u32x4 ra[4], rb[BCH];
-    float bs_scale = 0.f, bs_zero = 0.f;
-    auto load_tile = [&](int k0) {
+    struct Stage {
+        u32x4 ra[NA], rb[BCH];
+        float bs_scale, bs_zero;
+    };
+    auto load_tile = [&](int k0, Stage& sg) {
+        u32x4* ra = sg.ra;
+        u32x4* rb = sg.rb;
+        float& bs_scale = sg.bs_scale;
+        float& bs_zero = sg.bs_zero;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < NA; ++i) {
             const int c = tid + 256 * i;
             const int row = c >> 3, kc = (c & 7) * 8;
             const int m = m0 + row, k = k0 + kc;
@@ -133,9 +149,12 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
             }
         }
     };
-    auto store_tile = [&](uint16_t* As, uint16_t* Bs) {
+    auto store_tile = [&](uint16_t* As, uint16_t* Bs, const Stage& sg) {
+        const u32x4* ra = sg.ra;
+        const u32x4* rb = sg.rb;
+        const float bs_scale = sg.bs_scale, bs_zero = sg.bs_zero;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < NA; ++i) {
             const int c = tid + 256 * i;
             *(u32x4*)(As + (c >> 3) * GLD + (c & 7) * 8) = ra[i];
         }
@@ -173,36 +192,51 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
         }
     };
 
-    f32x4 acc[4][4];
+    f32x4 acc[MI][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int nk = (a.K + GBK - 1) / GBK;
-    load_tile(0);
-    store_tile(Asb[0], Bsb[0]);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const uint16_t* As = Asb[kt & 1];
-        const uint16_t* Bs = Bsb[kt & 1];
-        if (kt + 1 < nk) load_tile((kt + 1) * GBK);
+    auto compute = [&](const uint16_t* As, const uint16_t* Bs) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            u32x4 af[4], bf[4];
+            u32x4 af[MI], bf[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                af[i] = *(const u32x4*)(As + (wm * 64 + 16 * i + r) * GLD + 32 * ks + 8 * g);
+            for (int i = 0; i < MI; ++i)
+                af[i] = *(const u32x4*)(As + (wm * (BM / 2) + 16 * i + r) * GLD + 32 * ks + 8 * g);
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 bf[j] = *(const u32x4*)(Bs + (wn * 64 + 16 * j + r) * GLD + 32 * ks + 8 * g);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = mfma16<AF>(af[i], bf[j], acc[i][j]);
         }
-        if (kt + 1 < nk) store_tile(Asb[(kt + 1) & 1], Bsb[(kt + 1) & 1]);
-        __syncthreads();
+    };
+    // LDS writes done, then a bare barrier: the global loads in flight are not drained
+    auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+
+    // K tiles are loaded into registers two tiles ahead and written to the other LDS
+    // buffer while the current one is multiplied
+    Stage st[2];
+    load_tile(0, st[0]);
+    if (nk > 1) load_tile(GBK, st[1]);
+    store_tile(Asb[0], Bsb[0], st[0]);
+    if (nk > 2) load_tile(2 * GBK, st[0]);
+    barrier();
+    for (int kt0 = 0; kt0 < nk; kt0 += 2) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int kt = kt0 + p;
+            if (kt < nk) {
+                compute(Asb[p], Bsb[p]);
+                if (kt + 1 < nk) store_tile(Asb[1 - p], Bsb[1 - p], st[1 - p]);
+                if (kt + 3 < nk) load_tile((kt + 3) * GBK, st[1 - p]);
+                barrier();
+            }
+        }
     }
 
     // ---- epilogue
@@ -217,10 +251,10 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
                 su = h2f(a.scales[a.F + f]);
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int m = m0 + wm * 64 + 16 * i + 4 * g + e;
+                    const int m = m0 + wm * (BM / 2) + 16 * i + 4 * g + e;
                     if (m >= a.M) continue;
                     const float gv = acc[i][j][e] * sg, uv = acc[i][j + 2][e] * su;
                     a.out16[(int64_t)m * a.F + f] = act_store(bfround(silu_f(gv) * uv), a.out_fmt);
@@ -234,10 +268,10 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
             float sn = 1.f;
             if constexpr (WF == W_INT8) sn = h2f(a.scales[n]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int m = m0 + wm * 64 + 16 * i + 4 * g + e;
+                    const int m = m0 + wm * (BM / 2) + 16 * i + 4 * g + e;
                     if (m >= a.M) continue;
                     const float v = acc[i][j][e] * sn;
                     if constexpr (EPI == EPI_F32) a.out32[(int64_t)m * a.N + n] = v;
@@ -247,19 +281,28 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     }
 }
 
-template <int WF>
-static hipError_t launch_w(const GemmArgs& a, int epi, hipStream_t st) {
+template <int WF, int BM>
+static hipError_t launch_wm(const GemmArgs& a, int epi, hipStream_t st) {
     GemmArgs b = a;
     b.tiles_n = (epi == EPI_SWIGLU) ? (a.F + 63) / 64 : (a.N + GBN - 1) / GBN;
-    b.tiles_m = (a.M + GBM - 1) / GBM;
+    b.tiles_m = (a.M + BM - 1) / BM;
     dim3 grid(b.tiles_n * b.tiles_m);
     switch (epi) {
-        case EPI_F32: FP_LAUNCH((gemm_kernel<WF, EPI_F32>), grid, dim3(256), 0, st, b); break;
-        case EPI_RESID: FP_LAUNCH((gemm_kernel<WF, EPI_RESID>), grid, dim3(256), 0, st, b); break;
-        case EPI_SWIGLU: FP_LAUNCH((gemm_kernel<WF, EPI_SWIGLU>), grid, dim3(256), 0, st, b); break;
+        case EPI_F32: FP_LAUNCH((gemm_kernel<WF, EPI_F32, BM>), grid, dim3(256), 0, st, b); break;
+        case EPI_RESID: FP_LAUNCH((gemm_kernel<WF, EPI_RESID, BM>), grid, dim3(256), 0, st, b); break;
+        case EPI_SWIGLU: FP_LAUNCH((gemm_kernel<WF, EPI_SWIGLU, BM>), grid, dim3(256), 0, st, b); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+// 64-row tiles when 128-row tiles would leave most of the 256 CUs idle
+template <int WF>
+static hipError_t launch_w(const GemmArgs& a, int epi, hipStream_t st) {
+    const int tn = (epi == EPI_SWIGLU) ? (a.F + 63) / 64 : (a.N + GBN - 1) / GBN;
+    const int t128 = tn * ((a.M + 127) / 128);
+    if (t128 < GEMM_SMALL_TILES) return launch_wm<WF, 64>(a, epi, st);
+    return launch_wm<WF, 128>(a, epi, st);
 }
 
 hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st) {
@@ -343,7 +386,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
         else return wn * 4 + j;
     };
 
-    float nsc[4], nzz[4], csc[4], czz[4];
+    uint32_t nsz[4], csz[4];       // int4: scale | zero << 16 of the next / current stage
     auto issue = [&](int stage, int k0) {
         char* sA = smem + stage * T::STAGE;
         char* sB = sA + T::A_BYTES;
@@ -371,18 +414,15 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(sB + blk * 1024), 16, 0, 0);
         }
         if constexpr (WF == W_INT4) {
+            // raw words, not converted here: a conversion would wait for them (and for
+            // the stage's LDS copies issued before them)
             const int grp = k0 / 128, ng = a.K / 128;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 bool v;
                 const int gb = grow_block(col_rb(j), v);
-                nsc[j] = 0.f;
-                nzz[j] = 0.f;
-                if (v) {
-                    const int64_t n = (int64_t)gb * 16 + r;
-                    nsc[j] = h2f(a.scales[n * ng + grp]);
-                    nzz[j] = h2f(a.zeros[n * ng + grp]);
-                }
+                nsz[j] = 0u;
+                if (v) nsz[j] = a.sz[((int64_t)gb * 16 + r) * ng + grp];
             }
         }
     };
@@ -423,9 +463,9 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                     bop[j] = u32x4{c0.x, c0.y, c1.x, c1.y};
                 } else {
                     const uint32_t wd = s == 0 ? raw[j].x : (s == 1 ? raw[j].y : (s == 2 ? raw[j].z : raw[j].w));
-                    const _Float16 bz = (_Float16)(1024.0f + czz[j]);
+                    const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(csz[j] >> 16)));
                     const f16x2 bias = {bz, bz};
-                    const _Float16 sh = (_Float16)csc[j];
+                    const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(csz[j] & 0xFFFFu));
                     const f16x2 s2 = {sh, sh};
                     const u32x4 q = i4x8_to_f16x8(wd, bias);
                     bop[j] = u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
@@ -445,7 +485,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     for (int kt = 0; kt < nk; ++kt) {
         if constexpr (WF == W_INT4) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) { csc[j] = nsc[j]; czz[j] = nzz[j]; }
+            for (int j = 0; j < 4; ++j) csz[j] = nsz[j];
         }
         if (kt + 1 < nk) issue((kt + 1) & 1, (kt + 1) * T::TK);
         compute(kt & 1);
@@ -521,7 +561,7 @@ hipError_t launch_gemm_big(const GemmArgs& a, int wf, int epi, hipStream_t st) {
 
 hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st) {
     const int tiles = ((a.M + BT - 1) / BT) * ((epi == EPI_SWIGLU) ? (a.F + 127) / 128 : (a.N + BT - 1) / BT);
-    if (tiles >= 128) return launch_gemm_big(a, wf, epi, st);
+    if (tiles >= GEMM_BIG_MIN_TILES) return launch_gemm_big(a, wf, epi, st);
     return launch_gemm_small(a, wf, epi, st);
 }
 

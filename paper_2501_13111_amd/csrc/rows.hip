@@ -17,23 +17,42 @@
 namespace fpk {
 
 // ---------------------------------------------------------------- RMSNorm
-// One workgroup per row.  out = act(bf16(x * r * g)), r = 1 / sqrt(mean(x^2) + eps).
+// One workgroup per row, 16-byte accesses (H is a multiple of 16).
+// out = act(bf16(x * r * g)), r = 1 / sqrt(mean(x^2) + eps).  The second pass reads the
+// row again (it is in L2).
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const uint16_t* __restrict__ x, int H,
                                                        const uint16_t* __restrict__ g, float eps,
                                                        uint16_t* __restrict__ out, int out_fmt) {
     __shared__ float red[16];
     const int64_t row = blockIdx.x;
-    const uint16_t* xr = x + row * (int64_t)H;
+    const u32x4* xr = (const u32x4*)(x + row * (int64_t)H);
+    const int nv = H / 8;
     float ss = 0.f;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) {
-        const float v = bf2f(xr[k]);
-        ss += v * v;
+    for (int c = threadIdx.x; c < nv; c += 256) {
+        const u32x4 v = xr[c];
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float e0 = __uint_as_float(w4[j] << 16), e1 = __uint_as_float(w4[j] & 0xFFFF0000u);
+            ss += e0 * e0 + e1 * e1;
+        }
     }
     ss = block_sum(ss, red);
     const float r = 1.0f / __fsqrt_rn(ss / (float)H + eps);
-    uint16_t* orow = out + row * (int64_t)H;
-    for (int k = threadIdx.x; k < H; k += blockDim.x)
-        orow[k] = act_store(bfround(bf2f(xr[k]) * r * bf2f(g[k])), out_fmt);
+    u32x4* orow = (u32x4*)(out + row * (int64_t)H);
+    const u32x4* gv = (const u32x4*)g;
+    for (int c = threadIdx.x; c < nv; c += 256) {
+        const u32x4 v = xr[c], gg = gv[c];
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w}, g4[4] = {gg.x, gg.y, gg.z, gg.w};
+        uint32_t o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float e0 = bfround(__uint_as_float(w4[j] << 16) * r * __uint_as_float(g4[j] << 16));
+            const float e1 = bfround(__uint_as_float(w4[j] & 0xFFFF0000u) * r * __uint_as_float(g4[j] & 0xFFFF0000u));
+            o[j] = (uint32_t)act_store(e0, out_fmt) | ((uint32_t)act_store(e1, out_fmt) << 16);
+        }
+        orow[c] = u32x4{o[0], o[1], o[2], o[3]};
+    }
 }
 
 // ---------------------------------------------------------------- residual epilogue
