@@ -3,7 +3,7 @@
 // per-(position, kv head) scales -- the INT8 KV cache of paper Sec. 3.2), so
 // that prefill sees exactly what later decode steps see.
 //
-// Flash-style on bf16 MFMA 16x16x32, written in the transposed form
+// Flash-style on MFMA 16x16x32, written in the transposed form
 //     S^T = K Q^T          (A = key rows from LDS, B = the wave's 16 queries)
 //     O^T += V^T P^T       (A = value columns, B = the probabilities already in
 //                           the lanes)
@@ -14,34 +14,52 @@
 // order (vt_slot), so the value tile is copied into LDS as it is and each A
 // fragment is one contiguous 16-byte LDS read.
 // Online softmax per query column (max / sum across the 4 lane groups by
-// shuffles).  int8 caches: codes are exact in bf16; s_k scales the scores and
-// s_v the probabilities.  Workgroup = 4 waves x 16 queries of one head; key
-// tiles of 64; heaviest (latest) query tiles are launched first.
+// shuffles).  int8 caches: codes are exact in fp16; s_k scales the scores and
+// s_v the probabilities.  Heaviest (latest) query tiles are launched first.
 #include "fp_device.h"
 #include "fp_internal.h"
 
 namespace fpk {
 
-template <int D>
-__global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
-    constexpr int KT = 64;
-    constexpr int KP = D + 8;     // padded row of the key tile (u16)
-    constexpr int VP = KT + 8;    // padded row of the transposed value tile (u16)
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KP];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VP];
-    __shared__ float ksc[KT], vsc[KT];
+// Workgroup = 8 waves x 16 queries of one head; key tiles of 64 are staged in LDS
+// (double buffered: the next tile is loaded into registers while the current one is
+// multiplied, then written to the other buffer; a bare barrier keeps those loads in
+// flight).  A bf16 cache runs on bf16 MFMA; an int8 cache is converted to exact fp16
+// codes while staging and runs on fp16 MFMA (queries and probabilities in fp16).
+// Scores are kept in the base-2 domain (scaled by log2 e) so each probability is
+// one exp2; the causal mask is applied only on tiles that reach past the wave's
+// first query.
+constexpr int PQ = 128;          // queries per workgroup
+constexpr int PKT = 64;          // keys per tile
 
-    const int nqt = (a.P + 63) / 64;
-    const int qt = nqt - 1 - (int)blockIdx.x;
+template <int D, bool KV8>
+__global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
+    constexpr int AF = KV8 ? ACT_F16 : ACT_BF16;
+    constexpr int KP = D + 8;     // padded row of the key tile (u16)
+    constexpr int VP = PKT + 8;   // padded row of the value tile (u16), slots in vt_slot order
+    constexpr int KSZ = PKT * KP, VSZ = D * VP;
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KSZ];
+    __shared__ __attribute__((aligned(16))) uint16_t Vt[2][VSZ];
+    __shared__ float ksc[2][PKT], vsc[2][PKT];
+    // register staging: 16-byte pieces of the K tile and of the two value blocks
+    constexpr int KPC = PKT * D * (KV8 ? 1 : 2) / 16;
+    constexpr int NKP = (KPC + 511) / 512;
+    constexpr int EPP = KV8 ? 16 : 8;            // elements per piece
+
+    const int nqt = (a.P + PQ - 1) / PQ;
+    const int qt = nqt - 1 - (int)blockIdx.x;     // heaviest (latest) query tiles first
     const int h = blockIdx.y, b = blockIdx.z;
     const int kvh = (h * a.nkv) / a.nh;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
-    const int p0 = qt * 64;
-    const int qpos = p0 + 16 * w + r;           // this lane's query column
+    const int p0 = qt * PQ;
+    const int qpos = p0 + 16 * w + r;             // this lane's query column
     const bool qvalid = qpos < a.P;
+    const int wfirst = p0 + 16 * w;               // first and last query of this wave
+    const int wlast = min(a.P - 1, wfirst + 15);
+    const float sl2 = a.scale * 1.4426950408889634f;   // scores in the base-2 domain
 
-    // Q^T fragments (bf16) for the D/32 MFMA k-steps
+    // Q^T fragments for the D/32 MFMA k-steps
     u32x4 qf[D / 32];
     {
         const float* qrow = a.q + ((int64_t)b * a.P + (qvalid ? qpos : 0)) * a.nh * D + h * D;
@@ -51,10 +69,13 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
             if (qvalid) {
                 const float4 x0 = *(const float4*)(qrow + 32 * j + 8 * g);
                 const float4 x1 = *(const float4*)(qrow + 32 * j + 8 * g + 4);
-                v[0] = (uint32_t)f2bf(x0.x) | ((uint32_t)f2bf(x0.y) << 16);
-                v[1] = (uint32_t)f2bf(x0.z) | ((uint32_t)f2bf(x0.w) << 16);
-                v[2] = (uint32_t)f2bf(x1.x) | ((uint32_t)f2bf(x1.y) << 16);
-                v[3] = (uint32_t)f2bf(x1.z) | ((uint32_t)f2bf(x1.w) << 16);
+                if constexpr (KV8) {
+                    v[0] = pack_f16_hw(x0.x, x0.y); v[1] = pack_f16_hw(x0.z, x0.w);
+                    v[2] = pack_f16_hw(x1.x, x1.y); v[3] = pack_f16_hw(x1.z, x1.w);
+                } else {
+                    v[0] = pack_bf16_hw(x0.x, x0.y); v[1] = pack_bf16_hw(x0.z, x0.w);
+                    v[2] = pack_bf16_hw(x1.x, x1.y); v[3] = pack_bf16_hw(x1.z, x1.w);
+                }
             }
             qf[j] = u32x4{v[0], v[1], v[2], v[3]};
         }
@@ -67,87 +88,95 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
 
     const int64_t crow0 = ((int64_t)b * a.nkv + kvh) * a.kv_stride; // key row of position 0
     const int64_t vblk0 = ((int64_t)b * a.nkv + kvh) * a.nblk;      // value block of position 0
-    const int kend = min(a.P, p0 + 64);
-    const int ntiles = (kend + KT - 1) / KT;
-    for (int kt = 0; kt < ntiles; ++kt) {
-        __syncthreads();
-        // ---- stage the K tile (row-major) and the two value blocks of the tile, bf16
-        if (a.kv_int8) {
-            constexpr int CPR = D / 16;            // 16-code chunks per key row
-            for (int c = tid; c < KT * CPR; c += 256) {
-                const int key = c / CPR, dc = (c % CPR) * 16;
-                const int kpos = kt * KT + key;
-                u32x4 kr = u32x4{0u, 0u, 0u, 0u};
-                if (kpos < a.P) kr = *(const u32x4*)((const int8_t*)a.kc + (crow0 + kpos) * D + dc);
-                const uint32_t kw[4] = {kr.x, kr.y, kr.z, kr.w};
-                uint32_t o[8];
+    const int kend = min(a.P, p0 + PQ);
+    const int ntiles = (kend + PKT - 1) / PKT;
+
+    // ---- staging of key tile kt: global -> registers.  K piece c: key c / (D / EPP);
+    // V piece c: dim (c / (VPD)) % D of block c / (VPD * D), VPD pieces per dim and block
+    constexpr int VPD = 32 / EPP;
+    struct Stage {
+        u32x4 k[NKP], v[NKP];
+        uint16_t sc;
+    };
+    auto load = [&](int kt, Stage& sg) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {     // codes are exact in bf16
-                    const float f0 = (float)(int8_t)((kw[e >> 1] >> (16 * (e & 1))) & 0xFF);
-                    const float f1 = (float)(int8_t)((kw[e >> 1] >> (16 * (e & 1) + 8)) & 0xFF);
-                    o[e] = (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xFFFF0000u);
-                }
-                *(u32x4*)(Ks + key * KP + dc) = u32x4{o[0], o[1], o[2], o[3]};
-                *(u32x4*)(Ks + key * KP + dc + 8) = u32x4{o[4], o[5], o[6], o[7]};
-            }
-            for (int c = tid; c < 2 * D * 2; c += 256) {   // 2 blocks x D dims x 2 chunks of 16 codes
-                const int half = c & 1, dd = (c >> 1) % D, blk = c / (2 * D);
+        for (int i = 0; i < NKP; ++i) {
+            const int c = tid + 512 * i;
+            sg.k[i] = u32x4{0u, 0u, 0u, 0u};
+            sg.v[i] = u32x4{0u, 0u, 0u, 0u};
+            if (c < KPC) {
+                const int key = c / (D / EPP), dc = (c % (D / EPP)) * EPP;
+                const int kpos = kt * PKT + key;
+                if (kpos < a.P) sg.k[i] = *(const u32x4*)((const char*)a.kc + ((crow0 + kpos) * D + dc) * (KV8 ? 1 : 2));
+                const int q = c % VPD, dd = (c / VPD) % D, blk = c / (VPD * D);
                 const int gb = 2 * kt + blk;
-                u32x4 vr = u32x4{0u, 0u, 0u, 0u};
-                if (gb < a.nblk) vr = *(const u32x4*)((const int8_t*)a.vc + ((vblk0 + gb) * D + dd) * VT_BLK + 16 * half);
-                const uint32_t vw[4] = {vr.x, vr.y, vr.z, vr.w};
-                uint32_t o[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float f0 = (float)(int8_t)((vw[e >> 1] >> (16 * (e & 1))) & 0xFF);
-                    const float f1 = (float)(int8_t)((vw[e >> 1] >> (16 * (e & 1) + 8)) & 0xFF);
-                    o[e] = (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xFFFF0000u);
-                }
-                uint16_t* dst = Vt + dd * VP + 32 * blk + 16 * half;
-                *(u32x4*)(dst) = u32x4{o[0], o[1], o[2], o[3]};
-                *(u32x4*)(dst + 8) = u32x4{o[4], o[5], o[6], o[7]};
-            }
-            if (tid < KT) {
-                const int kpos = kt * KT + tid;
-                ksc[tid] = kpos < a.P ? h2f(a.k_scales[crow0 + kpos]) : 0.f;
-                vsc[tid] = kpos < a.P ? h2f(a.v_scales[crow0 + kpos]) : 0.f;
-            }
-        } else {
-            constexpr int CPR = D / 8;             // 8-value chunks per key row
-            for (int c = tid; c < KT * CPR; c += 256) {
-                const int key = c / CPR, dc = (c % CPR) * 8;
-                const int kpos = kt * KT + key;
-                u32x4 kr = u32x4{0u, 0u, 0u, 0u};
-                if (kpos < a.P) kr = *(const u32x4*)((const uint16_t*)a.kc + (crow0 + kpos) * D + dc);
-                *(u32x4*)(Ks + key * KP + dc) = kr;
-            }
-            for (int c = tid; c < 2 * D * 4; c += 256) {   // 2 blocks x D dims x 4 chunks of 8 values
-                const int q4 = c & 3, dd = (c >> 2) % D, blk = c / (4 * D);
-                const int gb = 2 * kt + blk;
-                u32x4 vr = u32x4{0u, 0u, 0u, 0u};
-                if (gb < a.nblk) vr = *(const u32x4*)((const uint16_t*)a.vc + ((vblk0 + gb) * D + dd) * VT_BLK + 8 * q4);
-                *(u32x4*)(Vt + dd * VP + 32 * blk + 8 * q4) = vr;
+                if (gb < a.nblk)
+                    sg.v[i] = *(const u32x4*)((const char*)a.vc + (((vblk0 + gb) * D + dd) * VT_BLK + EPP * q) * (KV8 ? 1 : 2));
             }
         }
-        __syncthreads();
+        if constexpr (KV8) {
+            sg.sc = 0;
+            if (tid < 2 * PKT) {
+                const int kpos = kt * PKT + (tid & (PKT - 1));
+                if (kpos < a.P) sg.sc = tid < PKT ? a.k_scales[crow0 + kpos] : a.v_scales[crow0 + kpos];
+            }
+        }
+    };
+    // ---- registers -> LDS buffer st (int8 codes become exact fp16 values)
+    auto store = [&](int st, const Stage& sg) {
+#pragma unroll
+        for (int i = 0; i < NKP; ++i) {
+            const int c = tid + 512 * i;
+            if (c < KPC) {
+                const int key = c / (D / EPP), dc = (c % (D / EPP)) * EPP;
+                const int q = c % VPD, dd = (c / VPD) % D, blk = c / (VPD * D);
+                uint16_t* kd = &Ks[st][key * KP + dc];
+                uint16_t* vd = &Vt[st][dd * VP + 32 * blk + EPP * q];
+                if constexpr (KV8) {
+                    const u32x2 k0 = i8x4_to_f16x4(sg.k[i].x), k1 = i8x4_to_f16x4(sg.k[i].y);
+                    const u32x2 k2 = i8x4_to_f16x4(sg.k[i].z), k3 = i8x4_to_f16x4(sg.k[i].w);
+                    *(u32x4*)(kd) = u32x4{k0.x, k0.y, k1.x, k1.y};
+                    *(u32x4*)(kd + 8) = u32x4{k2.x, k2.y, k3.x, k3.y};
+                    const u32x2 v0 = i8x4_to_f16x4(sg.v[i].x), v1 = i8x4_to_f16x4(sg.v[i].y);
+                    const u32x2 v2 = i8x4_to_f16x4(sg.v[i].z), v3 = i8x4_to_f16x4(sg.v[i].w);
+                    *(u32x4*)(vd) = u32x4{v0.x, v0.y, v1.x, v1.y};
+                    *(u32x4*)(vd + 8) = u32x4{v2.x, v2.y, v3.x, v3.y};
+                } else {
+                    *(u32x4*)(kd) = sg.k[i];
+                    *(u32x4*)(vd) = sg.v[i];
+                }
+            }
+        }
+        if constexpr (KV8) {
+            if (tid < 2 * PKT) {
+                if (tid < PKT) ksc[st][tid] = h2f(sg.sc) * sl2;
+                else vsc[st][tid - PKT] = h2f(sg.sc);
+            }
+        }
+    };
 
-        // ---- S^T = K Q^T for the 4 key subtiles
+    auto compute = [&](int kt, int st, bool masked) {
+        // ---- S^T = K Q^T for the 4 key subtiles (base-2 domain)
         float s[4][4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
             f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int j = 0; j < D / 32; ++j) {
-                const u32x4 ka = *(const u32x4*)(Ks + (16 * kk + r) * KP + 32 * j + 8 * g);
-                acc = mfma_bf16(ka, qf[j], acc);
+                const u32x4 ka = *(const u32x4*)(&Ks[st][(16 * kk + r) * KP + 32 * j + 8 * g]);
+                acc = mfma16<AF>(ka, qf[j], acc);
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int key = 16 * kk + 4 * g + i;
-                const int kpos = kt * KT + key;
-                float v = acc[i] * a.scale;
-                if (a.kv_int8) v *= ksc[key];
-                s[kk][i] = (kpos <= qpos && kpos < a.P) ? v : -INFINITY;
+                float v;
+                if constexpr (KV8) v = acc[i] * ksc[st][key];
+                else v = acc[i] * sl2;
+                if (masked) {
+                    const int kpos = kt * PKT + key;
+                    v = (kpos <= qpos && kpos < a.P) ? v : -INFINITY;
+                }
+                s[kk][i] = v;
             }
         }
         // ---- online softmax for this lane's query column
@@ -159,13 +188,13 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
         tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
         const float m_new = fmaxf(m_run, tmax);
-        const float alpha = __expf(m_run - m_new);
+        const float alpha = exp2f(m_run - m_new);
         float psum = 0.f;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = __expf(s[kk][i] - m_new);
+                const float p = exp2f(s[kk][i] - m_new);
                 s[kk][i] = p;
                 psum += p;
             }
@@ -187,18 +216,39 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     pv[i] = s[kk][i];
-                    if (a.kv_int8) pv[i] *= vsc[16 * kk + 4 * g + i];
+                    if constexpr (KV8) pv[i] *= vsc[st][16 * kk + 4 * g + i];
                 }
-                pb[2 * half] = (uint32_t)f2bf(pv[0]) | ((uint32_t)f2bf(pv[1]) << 16);
-                pb[2 * half + 1] = (uint32_t)f2bf(pv[2]) | ((uint32_t)f2bf(pv[3]) << 16);
+                if constexpr (KV8) {
+                    pb[2 * half] = pack_f16_hw(pv[0], pv[1]);
+                    pb[2 * half + 1] = pack_f16_hw(pv[2], pv[3]);
+                } else {
+                    pb[2 * half] = pack_bf16_hw(pv[0], pv[1]);
+                    pb[2 * half + 1] = pack_bf16_hw(pv[2], pv[3]);
+                }
             }
             const u32x4 pfrag = u32x4{pb[0], pb[1], pb[2], pb[3]};
 #pragma unroll
             for (int dd = 0; dd < D / 16; ++dd) {
-                const u32x4 vf = *(const u32x4*)(Vt + (16 * dd + r) * VP + 32 * k2 + 8 * g);
-                oacc[dd] = mfma_bf16(vf, pfrag, oacc[dd]);
+                const u32x4 vf = *(const u32x4*)(&Vt[st][(16 * dd + r) * VP + 32 * k2 + 8 * g]);
+                oacc[dd] = mfma16<AF>(vf, pfrag, oacc[dd]);
             }
         }
+    };
+    auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+
+    Stage sg;
+    load(0, sg);
+    store(0, sg);
+    if (ntiles > 1) load(1, sg);
+    barrier();
+    for (int kt = 0; kt < ntiles; ++kt) {
+        if (kt * PKT <= wlast) {                  // tiles past the wave's queries: nothing
+            if ((kt + 1) * PKT - 1 > wfirst || (kt + 1) * PKT > a.P) compute(kt, kt & 1, true);
+            else compute(kt, kt & 1, false);
+        }
+        if (kt + 1 < ntiles) store((kt + 1) & 1, sg);
+        if (kt + 2 < ntiles) load(kt + 2, sg);
+        barrier();
     }
 
     if (!qvalid) return;
@@ -215,11 +265,17 @@ __global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPreArgs a) {
 }
 
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st) {
-    const int nqt = (a.P + 63) / 64;
+    const int nqt = (a.P + PQ - 1) / PQ;
     dim3 grid(nqt, a.nh, B);
-    if (a.d == 128) FP_LAUNCH(attn_prefill_kernel<128>, grid, dim3(256), 0, st, a);
-    else if (a.d == 64) FP_LAUNCH(attn_prefill_kernel<64>, grid, dim3(256), 0, st, a);
-    else return hipErrorInvalidValue;
+    if (a.d == 128) {
+        if (a.kv_int8) FP_LAUNCH((attn_prefill_kernel<128, true>), grid, dim3(512), 0, st, a);
+        else FP_LAUNCH((attn_prefill_kernel<128, false>), grid, dim3(512), 0, st, a);
+    } else if (a.d == 64) {
+        if (a.kv_int8) FP_LAUNCH((attn_prefill_kernel<64, true>), grid, dim3(512), 0, st, a);
+        else FP_LAUNCH((attn_prefill_kernel<64, false>), grid, dim3(512), 0, st, a);
+    } else {
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

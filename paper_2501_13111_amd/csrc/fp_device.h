@@ -24,6 +24,18 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 __device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
 __device__ __forceinline__ float bfround(float f) { return bf2f(f2bf(f)); }
 
+// Two floats -> a packed pair by the hardware conversions (round to nearest even),
+// for MFMA operands that only need to be within tolerance (probabilities, queries).
+__device__ __forceinline__ uint32_t pack_bf16_hw(float lo, float hi) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ uint32_t pack_f16_hw(float lo, float hi) {
+    const f16x2 v = {(_Float16)lo, (_Float16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
 __device__ __forceinline__ uint16_t f2h(float f) {
     _Float16 h = (_Float16)f;                      // v_cvt_f16_f32, round to nearest even
     return __builtin_bit_cast(uint16_t, h);
