@@ -128,12 +128,20 @@ __device__ __forceinline__ u32x2 i8x4_to_f16x4(uint32_t w) {
 // int4 word in the device nibble order (nibble p holds column offset 2p for p < 4 and
 // 2(p-4)+1 for p >= 4) -> 8 exact fp16 values (q - z) in column order.
 // fp16 bits 0x6400 | q encode 1024 + q; subtracting 1024 + z is exact.
+// (a & m) | o in one VOP3 instruction (m in an SGPR, o in a VGPR: one scalar operand per
+// VOP3 instruction; the compiler splits the pattern into two instructions otherwise).
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t m, uint32_t o) {
+    uint32_t d;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "s"(m), "v"(o));
+    return d;
+}
+
 __device__ __forceinline__ u32x4 i4x8_to_f16x8(uint32_t w, f16x2 bias) {
     u32x4 r;
-    const uint32_t p0 = (w & 0x000F000Fu) | 0x64006400u;
-    const uint32_t p1 = ((w >> 4) & 0x000F000Fu) | 0x64006400u;
-    const uint32_t p2 = ((w >> 8) & 0x000F000Fu) | 0x64006400u;
-    const uint32_t p3 = ((w >> 12) & 0x000F000Fu) | 0x64006400u;
+    const uint32_t p0 = and_or(w, 0x000F000Fu, 0x64006400u);
+    const uint32_t p1 = and_or(w >> 4, 0x000F000Fu, 0x64006400u);
+    const uint32_t p2 = and_or(w >> 8, 0x000F000Fu, 0x64006400u);
+    const uint32_t p3 = and_or(w >> 12, 0x000F000Fu, 0x64006400u);
     r.x = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, p0) - bias);
     r.y = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, p1) - bias);
     r.z = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, p2) - bias);

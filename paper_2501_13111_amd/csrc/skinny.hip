@@ -332,14 +332,26 @@ __global__ void __launch_bounds__(256, 2) skinny_batch_kernel(SkinnyArgs a) {
 
     // activation chunk ci: thread piece c = tid + 256 i is row c / 16, LDS slot c % 16,
     // which holds the row's 16-byte piece slot ^ (row % 16)
+    // Loads are unconditional (clamped addresses): rows past M only feed output rows
+    // that are never stored; pieces past the k-range are zeroed (the weights there
+    // are padding or clamped copies), which only happens in a ragged last chunk.
     auto load_a = [&](int ci, u32x4* ra) {
+        const int kbase = kb + min(ci, nch - 1) * SB_KC;
+        const bool ragged = kbase + SB_KC > ke;
 #pragma unroll
         for (int i = 0; i < MT; ++i) {
             const int c = tid + 256 * i;
             const int rr = c >> 4, slot = c & 15;
-            const int k = kb + ci * SB_KC + ((slot ^ (rr & 15)) * 8);
-            ra[i] = u32x4{0u, 0u, 0u, 0u};
-            if (rr < a.M && k < ke && ci < nch) ra[i] = *(const u32x4*)(a.X + (int64_t)rr * a.K + k);
+            const int k = kbase + ((slot ^ (rr & 15)) * 8);
+            ra[i] = *(const u32x4*)(a.X + (int64_t)min(rr, a.M - 1) * a.K + min(k, a.K - 8));
+        }
+        if (ragged) {
+#pragma unroll
+            for (int i = 0; i < MT; ++i) {
+                const int c = tid + 256 * i;
+                const int rr = c >> 4, slot = c & 15;
+                if (kbase + ((slot ^ (rr & 15)) * 8) >= ke) ra[i] = u32x4{0u, 0u, 0u, 0u};
+            }
         }
     };
     auto store_a = [&](char* buf, const u32x4* ra) {
