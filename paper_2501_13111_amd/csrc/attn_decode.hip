@@ -324,16 +324,22 @@ __global__ void __launch_bounds__(D) attn_merge_kernel(AttnDecArgs a, int nsw) {
     a.out[((int64_t)b * a.nh + h) * D + i] = act_store(bfround(o / l), a.out_fmt);
 }
 
-// Splits of the context: about 4096 waves over all (sequence, kv head) pairs for a
-// batch, fewer for one sequence (fewer partials for the consumer to merge), at least
-// one 32-key block each.  The grid depends only on the capacity, so a captured graph
-// replays at every position.
+// Splits of the context: about 2048 waves over all (sequence, kv head) pairs for a
+// batch (long waves keep their chunk loads pipelined), fewer for one sequence (fewer
+// partials for the consumer to merge), at least one 32-key block each and four
+// splits per pair when the context has four blocks.  The grid depends only on the
+// capacity, so a captured graph replays at every position.
 void attn_decode_split(int max_seq, int B, int nkv, int group, int* nsplit, int* keys_per_split) {
     (void)group;
-    const int target = B == 1 ? 512 : 4096;
+#ifndef FP_ATTN_WAVES
+#define FP_ATTN_WAVES 2048
+#endif
+    const int target = B == 1 ? 512 : FP_ATTN_WAVES;
     const int want = (target + B * nkv - 1) / (B * nkv);
     const int blocks = (max_seq + VT_BLK - 1) / VT_BLK;
     int ns = want < blocks ? want : blocks;
+    // at least the four splits a workgroup holds (its waves would idle otherwise)
+    if (ns < 4) ns = blocks < 4 ? blocks : 4;
     if (ns < 1) ns = 1;
     const int bps = (blocks + ns - 1) / ns;
     *keys_per_split = bps * VT_BLK;

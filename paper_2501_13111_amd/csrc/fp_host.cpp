@@ -330,7 +330,7 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
 // split-K factor only has to fill the GPU (about TARGET_WG_B workgroups) and stays small,
 // which keeps the partial sums (ks * M * N floats) well below the weight bytes.
 #ifndef FP_TARGET_WG_B
-#define FP_TARGET_WG_B 320
+#define FP_TARGET_WG_B 192
 #endif
 fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, float* part,
                            int* ks_out, hipStream_t st) {

@@ -297,8 +297,10 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 constexpr int SB_KC = 128;              // k per activation chunk
 constexpr int SB_PD = 2;                // chunks of loads in flight
 
-template <int WF, int MT, int NS>
-__global__ void __launch_bounds__(256, 2) skinny_batch_kernel(SkinnyArgs a) {
+template <int WF, int MT, int NS, int NWV>
+__global__ void __launch_bounds__(64 * NWV, NWV == 4 ? 2 : 1) skinny_batch_kernel(SkinnyArgs a) {
+    constexpr int NT = 64 * NWV;                     // threads
+    constexpr int NPA = (256 * MT + NT - 1) / NT;    // activation pieces per thread
     constexpr int KS = SkinnyTraits<WF>::KS;
     constexpr int NJ = SkinnyTraits<WF>::NJ;
     constexpr int SPC = SB_KC / KS;                  // K-steps per chunk
@@ -319,12 +321,12 @@ __global__ void __launch_bounds__(256, 2) skinny_batch_kernel(SkinnyArgs a) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         if (a.dual_F > 0) {
-            const int fw = blockIdx.x * (32 * NS) + w * (8 * NS);
+            const int fw = blockIdx.x * (NWV * 8 * NS) + w * (8 * NS);
             const int f = fw + 16 * (s % (NS / 2)) + r;
             rv[s] = f < a.dual_F;
             row[s] = (s < NS / 2 ? 0 : a.dual_F) + min(f, a.dual_F - 1);
         } else {
-            const int n = blockIdx.x * (64 * NS) + w * (16 * NS) + 16 * s + r;
+            const int n = blockIdx.x * (NWV * 16 * NS) + w * (16 * NS) + 16 * s + r;
             rv[s] = n < a.N;
             row[s] = min(n, a.N - 1);
         }
@@ -339,24 +341,25 @@ __global__ void __launch_bounds__(256, 2) skinny_batch_kernel(SkinnyArgs a) {
         const int kbase = kb + min(ci, nch - 1) * SB_KC;
         const bool ragged = kbase + SB_KC > ke;
 #pragma unroll
-        for (int i = 0; i < MT; ++i) {
-            const int c = tid + 256 * i;
-            const int rr = c >> 4, slot = c & 15;
+        for (int i = 0; i < NPA; ++i) {
+            const int c = tid + NT * i;
+            const int rr = min(c >> 4, 16 * MT - 1), slot = c & 15;
             const int k = kbase + ((slot ^ (rr & 15)) * 8);
             ra[i] = *(const u32x4*)(a.X + (int64_t)min(rr, a.M - 1) * a.K + min(k, a.K - 8));
         }
         if (ragged) {
 #pragma unroll
-            for (int i = 0; i < MT; ++i) {
-                const int c = tid + 256 * i;
-                const int rr = c >> 4, slot = c & 15;
+            for (int i = 0; i < NPA; ++i) {
+                const int c = tid + NT * i;
+                const int rr = min(c >> 4, 16 * MT - 1), slot = c & 15;
                 if (kbase + ((slot ^ (rr & 15)) * 8) >= ke) ra[i] = u32x4{0u, 0u, 0u, 0u};
             }
         }
     };
     auto store_a = [&](char* buf, const u32x4* ra) {
 #pragma unroll
-        for (int i = 0; i < MT; ++i) *(u32x4*)(buf + (tid + 256 * i) * 16) = ra[i];
+        for (int i = 0; i < NPA; ++i)
+            if ((256 * MT) % NT == 0 || tid + NT * i < 256 * MT) *(u32x4*)(buf + (tid + NT * i) * 16) = ra[i];
     };
     // weight fragments of chunk ci (clamped to the last chunk past the end)
     auto load_w = [&](int ci, u32x4 (*wv)[NS], uint32_t* sz) {
@@ -428,7 +431,7 @@ __global__ void __launch_bounds__(256, 2) skinny_batch_kernel(SkinnyArgs a) {
 
     u32x4 wr[SB_PD][SPC][NS];
     uint32_t szr[SB_PD][NS];
-    u32x4 ra[SB_PD][MT];
+    u32x4 ra[SB_PD][NPA];
     load_a(0, ra[0]);
     load_a(1, ra[1]);
     load_w(0, wr[0], szr[0]);
@@ -469,11 +472,18 @@ __global__ void __launch_bounds__(256, 2) skinny_batch_kernel(SkinnyArgs a) {
     }
 }
 
+// Tiling: 16-row subtiles per wave (NS) and waves per workgroup (NWV).  With two or
+// more 16-token tiles the quantised formats run eight waves of two subtiles (more
+// waves per SIMD to overlap the unpacking with the MFMAs); every variant covers
+// skinny_batch_rows() weight rows per workgroup.
 template <int WF, int MT>
 static hipError_t launch_batch(const SkinnyArgs& a, int ks, hipStream_t st) {
-    constexpr int NS = skinny_batch_ns(WF);
+    constexpr bool WIDE = WF != W_BF16 && MT >= 2;
+    constexpr int NS = WF == W_BF16 ? 2 : (WIDE ? 2 : 4);
+    constexpr int NWV = WIDE ? 8 : 4;
+    static_assert(NWV * 16 * NS == (WF == W_BF16 ? 128 : 256), "rows per workgroup");
     dim3 grid(skinny_batch_tiles(a.N, a.dual_F, WF), ks);
-    FP_LAUNCH((skinny_batch_kernel<WF, MT, NS>), grid, dim3(256), 0, st, a);
+    FP_LAUNCH((skinny_batch_kernel<WF, MT, NS, NWV>), grid, dim3(64 * NWV), 0, st, a);
     return hipGetLastError();
 }
 
@@ -489,8 +499,8 @@ static hipError_t launch_batch_w(const SkinnyArgs& a, int ks, hipStream_t st) {
 }
 
 int skinny_batch_tiles(int N, int dual_F, int wf) {
-    const int ns = skinny_batch_ns(wf);
-    return dual_F > 0 ? (dual_F + 32 * ns - 1) / (32 * ns) : (N + 64 * ns - 1) / (64 * ns);
+    const int rows = wf == W_BF16 ? 128 : 256;       // weight rows per workgroup
+    return dual_F > 0 ? (dual_F + rows / 2 - 1) / (rows / 2) : (N + rows - 1) / rows;
 }
 
 int skinny_batch_chunk() { return SB_KC; }
