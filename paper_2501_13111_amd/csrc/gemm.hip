@@ -42,8 +42,9 @@ constexpr int GLD = GBK + GPAD;   // LDS row (u16)
 
 // BM = 128 (waves 2 x 2 of 64 x 64) or 64 (waves 2 x 2 of 32 x 64, for problems with
 // too few 128-row tiles to fill the GPU)
-template <int WF, int EPI, int BM>
+template <int WF, int EPI, int BM, int RD>
 __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
+    static_assert(RD % 2 == 0, "the LDS buffer parity of a tile is fixed within the unrolled ring");
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
     constexpr int MI = BM / 32;                 // 16-row MFMA tiles per wave
     constexpr int NA = BM / 32;                 // 16-byte A loads per thread per K tile
@@ -89,20 +90,26 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     constexpr int BCH = (WF == W_BF16) ? 4 : (WF == W_INT8 ? 2 : 1);   // 16-byte B loads per thread
     struct Stage {
         u32x4 ra[NA], rb[BCH];
-        float bs_scale, bs_zero;
+        uint32_t sz;              // int4: scale | zero << 16 of the lane's row and group
     };
+    // Loads are unconditional (clamped addresses) so the compiler can count them across
+    // the loop and keep several tiles in flight: rows past M or N only feed outputs that
+    // are never stored; activation pieces past K are zeroed (the weights there are
+    // padding or a clamped copy), which only happens in a ragged last tile.
     auto load_tile = [&](int k0, Stage& sg) {
         u32x4* ra = sg.ra;
         u32x4* rb = sg.rb;
-        float& bs_scale = sg.bs_scale;
-        float& bs_zero = sg.bs_zero;
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             const int c = tid + 256 * i;
             const int row = c >> 3, kc = (c & 7) * 8;
-            const int m = m0 + row, k = k0 + kc;
-            ra[i] = u32x4{0u, 0u, 0u, 0u};
-            if (m < a.M && k < a.K) ra[i] = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+            const int m = min(m0 + row, a.M - 1), k = min(k0 + kc, a.K - 8);
+            ra[i] = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+        }
+        if (k0 + GBK > a.K) {
+#pragma unroll
+            for (int i = 0; i < NA; ++i)
+                if (k0 + ((tid + 256 * i) & 7) * 8 >= a.K) ra[i] = u32x4{0u, 0u, 0u, 0u};
         }
         // B: fragment-major tiles -- each 64-thread group reads one contiguous 1 KiB block
         // (16 rows x one K-step); chunk L = r + 16 g holds row r, k-slice g of the block.
@@ -114,11 +121,9 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
                 const int blk = c >> 6, L = c & 63, ntl = blk >> 1, kst = blk & 1;
                 const int lr = 16 * ntl + (L & 15);
                 bool v;
-                const int n = brow(lr, v);
-                const int kabs = k0 + 32 * kst;
-                rb[i] = u32x4{0u, 0u, 0u, 0u};
-                if (v && kabs + 8 * (L >> 4) < a.K)
-                    rb[i] = Wt[((int64_t)(n >> 4) * a.kst + kabs / 32) * 64 + L];
+                int n = brow(lr, v);
+                n = v ? n : 0;
+                rb[i] = Wt[((int64_t)(n >> 4) * a.kst + min((k0 + 32 * kst) / 32, a.kst - 1)) * 64 + L];
             }
         } else if constexpr (WF == W_INT8) {
 #pragma unroll
@@ -127,32 +132,24 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
                 const int ntl = c >> 6, L = c & 63;
                 const int lr = 16 * ntl + (L & 15);
                 bool v;
-                const int n = brow(lr, v);
-                rb[i] = u32x4{0u, 0u, 0u, 0u};
-                if (v && k0 + 16 * (L >> 4) < a.K)
-                    rb[i] = Wt[((int64_t)(n >> 4) * a.kst + k0 / 64) * 64 + L];
+                int n = brow(lr, v);
+                n = v ? n : 0;
+                rb[i] = Wt[((int64_t)(n >> 4) * a.kst + min(k0 / 64, a.kst - 1)) * 64 + L];
             }
         } else {                                           // 8 subtiles x half a K-step of 128
             const int ntl = tid >> 5, j = tid & 31;
             const int lr = 16 * ntl + (j & 15);
             const int gg = j >> 4, g = gg + 2 * ((k0 >> 6) & 1);
             bool v;
-            const int n = brow(lr, v);
-            rb[0] = u32x4{0u, 0u, 0u, 0u};
-            bs_scale = 0.f;
-            bs_zero = 0.f;
-            if (v && k0 < a.K) {
-                rb[0] = Wt[((int64_t)(n >> 4) * a.kst + k0 / 128) * 64 + (j & 15) + 16 * g];
-                const int grp = k0 / 128;
-                bs_scale = h2f(a.scales[(int64_t)n * (a.K / 128) + grp]);
-                bs_zero = h2f(a.zeros[(int64_t)n * (a.K / 128) + grp]);
-            }
+            int n = brow(lr, v);
+            n = v ? n : 0;
+            rb[0] = Wt[((int64_t)(n >> 4) * a.kst + k0 / 128) * 64 + (j & 15) + 16 * g];
+            sg.sz = a.sz[(int64_t)n * (a.K / 128) + k0 / 128];
         }
     };
     auto store_tile = [&](uint16_t* As, uint16_t* Bs, const Stage& sg) {
         const u32x4* ra = sg.ra;
         const u32x4* rb = sg.rb;
-        const float bs_scale = sg.bs_scale, bs_zero = sg.bs_zero;
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             const int c = tid + 256 * i;
@@ -178,9 +175,9 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
             }
         } else {
             uint16_t* dst = Bs + (16 * (tid >> 5) + (tid & 15)) * GLD + 32 * ((tid >> 4) & 1);
-            const _Float16 bz = (_Float16)(1024.0f + bs_zero);
+            const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(sg.sz >> 16)));
             const f16x2 bias = {bz, bz};
-            const _Float16 sh = (_Float16)bs_scale;
+            const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(sg.sz & 0xFFFFu));
             const f16x2 sc = {sh, sh};
             const uint32_t wd[4] = {rb[0].x, rb[0].y, rb[0].z, rb[0].w};
 #pragma unroll
@@ -218,24 +215,27 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     // LDS writes done, then a bare barrier: the global loads in flight are not drained
     auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
-    // K tiles are loaded into registers two tiles ahead and written to the other LDS
-    // buffer while the current one is multiplied
-    Stage st[2];
-    load_tile(0, st[0]);
-    if (nk > 1) load_tile(GBK, st[1]);
-    store_tile(Asb[0], Bsb[0], st[0]);
-    if (nk > 2) load_tile(2 * GBK, st[0]);
-    barrier();
-    for (int kt0 = 0; kt0 < nk; kt0 += 2) {
+    // K tiles are loaded into a ring of RD register stages, RD tiles ahead, and written
+    // to the other LDS buffer while the current one is multiplied (tile t lives in
+    // stage t % RD)
+    // Every trip issues the same memory operations (tile indexes past the end are
+    // clamped, their copies never read), so the compiler's wait counts stay exact and
+    // the ring stays in flight; only the MFMA work is skipped past the last tile.
+    Stage st[RD];
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const int kt = kt0 + p;
-            if (kt < nk) {
-                compute(Asb[p], Bsb[p]);
-                if (kt + 1 < nk) store_tile(Asb[1 - p], Bsb[1 - p], st[1 - p]);
-                if (kt + 3 < nk) load_tile((kt + 3) * GBK, st[1 - p]);
-                barrier();
-            }
+    for (int q = 0; q < RD; ++q) load_tile(min(q, nk - 1) * GBK, st[q]);
+    store_tile(Asb[0], Bsb[0], st[0]);
+    load_tile(min(RD, nk - 1) * GBK, st[0]);
+    barrier();
+    for (int kt0 = 0; kt0 < nk; kt0 += RD) {
+#pragma unroll
+        for (int q = 0; q < RD; ++q) {
+            const int kt = kt0 + q;
+            const int nq = (q + 1) % RD;
+            if (kt < nk) compute(Asb[q & 1], Bsb[q & 1]);
+            store_tile(Asb[(q + 1) & 1], Bsb[(q + 1) & 1], st[nq]);
+            load_tile(min(kt + 1 + RD, nk - 1) * GBK, st[nq]);
+            barrier();
         }
     }
 
@@ -281,16 +281,18 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     }
 }
 
-template <int WF, int BM>
+// register ring depth: deeper for 64-row tiles (one workgroup per CU, nothing else to
+// hide the load latency)
+template <int WF, int BM, int RD = (BM == 64 ? 4 : 2)>
 static hipError_t launch_wm(const GemmArgs& a, int epi, hipStream_t st) {
     GemmArgs b = a;
     b.tiles_n = (epi == EPI_SWIGLU) ? (a.F + 63) / 64 : (a.N + GBN - 1) / GBN;
     b.tiles_m = (a.M + BM - 1) / BM;
     dim3 grid(b.tiles_n * b.tiles_m);
     switch (epi) {
-        case EPI_F32: FP_LAUNCH((gemm_kernel<WF, EPI_F32, BM>), grid, dim3(256), 0, st, b); break;
-        case EPI_RESID: FP_LAUNCH((gemm_kernel<WF, EPI_RESID, BM>), grid, dim3(256), 0, st, b); break;
-        case EPI_SWIGLU: FP_LAUNCH((gemm_kernel<WF, EPI_SWIGLU, BM>), grid, dim3(256), 0, st, b); break;
+        case EPI_F32: FP_LAUNCH((gemm_kernel<WF, EPI_F32, BM, RD>), grid, dim3(256), 0, st, b); break;
+        case EPI_RESID: FP_LAUNCH((gemm_kernel<WF, EPI_RESID, BM, RD>), grid, dim3(256), 0, st, b); break;
+        case EPI_SWIGLU: FP_LAUNCH((gemm_kernel<WF, EPI_SWIGLU, BM, RD>), grid, dim3(256), 0, st, b); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
