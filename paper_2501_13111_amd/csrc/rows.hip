@@ -98,6 +98,73 @@ __global__ void __launch_bounds__(256) norm_apply_kernel(const uint16_t* __restr
         nout[m * (int64_t)N + n] = act_store(bfround(bf2f(y[m * (int64_t)N + n]) * r * bf2f(g[n])), nfmt);
 }
 
+// Batches: one workgroup of 1024 threads per row does both steps, keeping the row in
+// registers (8 consecutive values per thread and pass, N <= 16384): out = bf16(resid +
+// sum_s part[s]) (skipped for ks == 0), the row's sum of squares by a block reduction,
+// then nout = act(bf16(out * r * g)).  One launch instead of two.
+constexpr int RN_T = 1024;
+__global__ void __launch_bounds__(RN_T) resid_norm_row_kernel(const float* __restrict__ part, int ks, int M, int N,
+                                                               const uint16_t* __restrict__ resid,
+                                                               uint16_t* __restrict__ out,
+                                                               const uint16_t* __restrict__ g, float eps,
+                                                               uint16_t* __restrict__ nout, int nfmt,
+                                                               int* __restrict__ d_pos) {
+    __shared__ float red[16];
+    const int64_t m = blockIdx.x;
+    const int64_t pstride = (int64_t)M * N;
+    float v[2][8];
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int n0 = (threadIdx.x + RN_T * j) * 8;
+        if (n0 >= N) continue;
+        const u32x4 rv = *(const u32x4*)(resid + m * N + n0);
+        const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[j][2 * e] = __uint_as_float(rw[e] << 16);
+            v[j][2 * e + 1] = __uint_as_float(rw[e] & 0xFFFF0000u);
+        }
+        if (ks > 0) {
+            float acc[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+            for (int s = 0; s < ks; ++s) {
+                const float* p = part + s * pstride + m * N + n0;
+                const float4 a0 = *(const float4*)p, a1 = *(const float4*)(p + 4);
+                acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
+                acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
+            }
+            uint32_t o[4];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[j][e] = bfround(v[j][e] + acc[e]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = (uint32_t)f2bf(v[j][2 * e]) | ((uint32_t)f2bf(v[j][2 * e + 1]) << 16);
+            *(u32x4*)(out + m * N + n0) = u32x4{o[0], o[1], o[2], o[3]};
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += v[j][e] * v[j][e];
+    }
+    ss = block_sum(ss, red);
+    const float r = 1.0f / __fsqrt_rn(ss / (float)N + eps);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int n0 = (threadIdx.x + RN_T * j) * 8;
+        if (n0 >= N) continue;
+        const u32x4 gv = *(const u32x4*)(g + n0);
+        const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w};
+        uint32_t o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float e0 = bfround(v[j][2 * e] * r * __uint_as_float(gw[e] << 16));
+            const float e1 = bfround(v[j][2 * e + 1] * r * __uint_as_float(gw[e] & 0xFFFF0000u));
+            o[e] = (uint32_t)act_store(e0, nfmt) | ((uint32_t)act_store(e1, nfmt) << 16);
+        }
+        *(u32x4*)(nout + m * N + n0) = u32x4{o[0], o[1], o[2], o[3]};
+    }
+    if (d_pos && blockIdx.x == 0 && threadIdx.x == 0) *d_pos += 1;
+}
+
 // ---------------------------------------------------------------- SwiGLU epilogue
 // a[m, f] = act(bf16(silu(G) * U)), G = sum_s part[s, m, f], U = sum_s part[s, m, F + f].
 __global__ void __launch_bounds__(256) swiglu_kernel(const float* __restrict__ part, int ks, int M,
@@ -231,6 +298,11 @@ hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, fl
 hipError_t launch_resid_norm(const float* part, int ks, int M, int N, const uint16_t* resid,
                              uint16_t* out, const uint16_t* g, float eps, uint16_t* nout, int nfmt,
                              float* ssq, int* inc_pos, hipStream_t st) {
+    if (g != nullptr && M > 1 && N % 8 == 0 && N <= 2 * RN_T * 8) {
+        FP_LAUNCH(resid_norm_row_kernel, dim3(M), dim3(RN_T), 0, st, part, ks, M, N, resid, out, g, eps, nout, nfmt,
+                  inc_pos);
+        return hipGetLastError();
+    }
     const int nblk = (N + RB - 1) / RB;
     FP_LAUNCH(resid_ssq_kernel, dim3(nblk, M), dim3(256), 0, st, part, ks, M, N, resid, out, ssq,
                        inc_pos);
