@@ -170,6 +170,18 @@ __device__ __forceinline__ float sum_parts(const float* __restrict__ p, int ks, 
     return acc;
 }
 
+// Raw buffer resource over [base, base + bytes), bytes < 2^32.  A load at or past the
+// end returns zeros without a memory access, so a pipelined loop can issue the same
+// loads on every trip (exact wait counts) and pay nothing for the trips past its range.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte non-temporal load at byte offset off (zeros if off >= the resource's size)
+__device__ __forceinline__ u32x4 buf_load_nt(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
+}
+constexpr uint32_t BUF_OOB = 0xFFFFFFF0u;   // an offset past the end of every resource
+
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
 
 }  // namespace fpk

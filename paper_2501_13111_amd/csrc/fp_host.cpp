@@ -327,11 +327,13 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
 }
 
 // Batched decode projection: the workgroup walks its k-range in staged chunks, so the
-// split-K factor only has to fill the GPU (about TARGET_WG_B workgroups) and stays small,
-// which keeps the partial sums (ks * M * N floats) well below the weight bytes.
-#ifndef FP_TARGET_WG_B
-#define FP_TARGET_WG_B 192
-#endif
+// split-K factor only has to fill the GPU and stays small.  The kernels hold one
+// workgroup per compute unit, so the factor is chosen by a cost model in units of one
+// workgroup's chunk time: rounds of resident workgroups times (chunks per workgroup +
+// a start-up cost of about two chunks), plus the partial sums each extra split writes
+// and the consumer reads back (ks * M * N floats each way, at about 5 TB/s, against a
+// chunk time of the workgroup's weight bytes at about 25 GB/s per compute unit).
+constexpr int NCU = 256;
 fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, float* part,
                            int* ks_out, hipStream_t st) {
     SkinnyArgs a{};
@@ -350,14 +352,21 @@ fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, 
     const int KC = skinny_batch_chunk();
     const int nch = (m.K + KC - 1) / KC;
     const int tiles = skinny_batch_tiles(m.N, dual_F, h->wq);
-    int ks = (FP_TARGET_WG_B + tiles - 1) / tiles;
-    int kmax = nch / 4;                  // at least four chunks per workgroup
-    if (kmax < 1) kmax = 1;
-    if (ks > kmax) ks = kmax;
-    if (ks < 1) ks = 1;
-    const int per = (nch + ks - 1) / ks;
+    const int rows = h->wq == FP_WQ_BF16 ? 128 : 256;
+    const double bpw = h->wq == FP_WQ_BF16 ? 2.0 : (h->wq == FP_WQ_INT8_CHANNEL ? 1.0 : 0.5);
+    const double chunk_s = rows * KC * bpw / 25e9;
+    const double split_s = (double)M * (dual_F > 0 ? 2.0 * dual_F : m.N) * 8.0 / 5e12;
+    int per = nch;
+    double best = 1e30;
+    for (int k = 1; k <= std::min(nch, KSMAX); ++k) {
+        const int p = (nch + k - 1) / k;
+        const int ksk = (nch + p - 1) / p;
+        const int rounds = (tiles * ksk + NCU - 1) / NCU;
+        const double cost = rounds * (p + 2.0) * chunk_s + ksk * split_s;
+        if (cost < best - 1e-12) { best = cost; per = p; }
+    }
     a.krange = per * KC;
-    ks = (nch + per - 1) / per;
+    int ks = (nch + per - 1) / per;
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     HIPCHK(launch_skinny_batch(a, h->wq, ks, st));
     *ks_out = ks;

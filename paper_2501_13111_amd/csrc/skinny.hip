@@ -85,13 +85,17 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
         }
     }
 
-    // ---- weight loads of one K-step
+    // ---- weight loads of one K-step: one 1 KiB block per wave (16 rows x one K-step).
+    // Rows past the matrix and steps past the k-range read past the end of the buffer
+    // resource (zeros, no memory access), so every load is issued unconditionally and
+    // the compiler's wait counts stay exact.
+    const int nrows = a.dual_F > 0 ? 2 * a.dual_F : a.N;
+    const __amdgpu_buffer_rsrc_t wres = buf_rsrc(a.W, (uint32_t)((nrows / 16) * a.kst * 1024));
     auto load_w = [&](int kk, u32x4* dst) {
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            dst[s] = u32x4{0u, 0u, 0u, 0u};
-            if (rv[s] && kk < ke)   // one 1 KiB block per wave: 16 rows x one K-step
-                dst[s] = __builtin_nontemporal_load((const u32x4*)a.W + ((int64_t)(row[s] >> 4) * a.kst + kk / KS) * 64 + lane);
+            const uint32_t blk = (uint32_t)((row[s] >> 4) * a.kst + kk / KS);
+            dst[s] = buf_load_nt(wres, (rv[s] && kk < ke) ? (blk * 64 + lane) * 16 : BUF_OOB);
         }
     };
 
@@ -256,10 +260,8 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
         for (int u = 0; u < UNR; ++u) load_w(base + (UNR + u) * KS, wb[u]);
 #pragma unroll
         for (int u = 0; u < UNR; ++u) compute(base + u * KS, wa[u]);
-        if (base + 2 * UNR * KS < ke) {
 #pragma unroll
-            for (int u = 0; u < UNR; ++u) load_w(base + (2 * UNR + u) * KS, wa[u]);
-        }
+        for (int u = 0; u < UNR; ++u) load_w(base + (2 * UNR + u) * KS, wa[u]);
 #pragma unroll
         for (int u = 0; u < UNR; ++u) compute(base + (UNR + u) * KS, wb[u]);
     }
@@ -287,18 +289,23 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 // so it is not staged whole -- that would cap the k-range per workgroup at the LDS
 // size and force a split-K factor (and partial-sum traffic) that grows with M.
 // Instead the workgroup walks its k-range in chunks of 128 (one int4 group, two
-// int8 or four bf16 K-steps).  Activation chunks are loaded into registers two
+// int8 or four bf16 K-steps).  Activation chunks are loaded into registers PD
 // chunks ahead and written to one of two LDS buffers one chunk ahead (rows of 256 B,
 // 16-byte pieces XOR-swizzled by the row so MFMA fragment reads are free of bank
-// conflicts); weight fragments (and int4 scale / zero words) run two chunks ahead
-// in registers.  The workgroup synchronises with a bare s_barrier after the LDS
+// conflicts); weight fragments (and int4 scale / zero words) run PD chunks ahead in
+// registers (PD = SB_PD for quantised weights, 2 for bf16, whose chunks hold four
+// K-steps of weights).  The workgroup synchronises with a bare s_barrier after the LDS
 // writes, so the global loads in flight are not drained at every chunk.  The
 // split-K factor only has to fill the GPU.
 constexpr int SB_KC = 128;              // k per activation chunk
-constexpr int SB_PD = 2;                // chunks of loads in flight
+#ifndef SKINNY_BATCH_PD
+#define SKINNY_BATCH_PD 4
+#endif
+constexpr int SB_PD = SKINNY_BATCH_PD;  // chunks of loads in flight (even: the LDS buffer is the chunk's parity)
+static_assert(SB_PD >= 2 && SB_PD % 2 == 0, "load depth");
 
 template <int WF, int MT, int NS, int NWV>
-__global__ void __launch_bounds__(64 * NWV, NWV == 4 ? 2 : 1) skinny_batch_kernel(SkinnyArgs a) {
+__global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a) {
     constexpr int NT = 64 * NWV;                     // threads
     constexpr int NPA = (256 * MT + NT - 1) / NT;    // activation pieces per thread
     constexpr int KS = SkinnyTraits<WF>::KS;
@@ -306,6 +313,7 @@ __global__ void __launch_bounds__(64 * NWV, NWV == 4 ? 2 : 1) skinny_batch_kerne
     constexpr int SPC = SB_KC / KS;                  // K-steps per chunk
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
     constexpr int ABUF = 16 * MT * 256;              // bytes of one activation chunk
+    constexpr int PD = WF == W_BF16 ? 2 : SB_PD;     // bf16 chunks hold four K-steps of weights
     __shared__ __attribute__((aligned(1024))) char As[2 * ABUF];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -332,14 +340,14 @@ __global__ void __launch_bounds__(64 * NWV, NWV == 4 ? 2 : 1) skinny_batch_kerne
         }
     }
 
-    // activation chunk ci: thread piece c = tid + 256 i is row c / 16, LDS slot c % 16,
+    // activation chunk ci: thread piece c = tid + NT i is row c / 16, LDS slot c % 16,
     // which holds the row's 16-byte piece slot ^ (row % 16)
     // Loads are unconditional (clamped addresses): rows past M only feed output rows
-    // that are never stored; pieces past the k-range are zeroed (the weights there
-    // are padding or clamped copies), which only happens in a ragged last chunk.
+    // that are never stored.  Pieces past the k-range (only in a ragged last chunk; the
+    // weights there are padding or clamped copies) are zeroed when the chunk is written
+    // to LDS, after its loads have landed, so no load has to be waited for early.
     auto load_a = [&](int ci, u32x4* ra) {
         const int kbase = kb + min(ci, nch - 1) * SB_KC;
-        const bool ragged = kbase + SB_KC > ke;
 #pragma unroll
         for (int i = 0; i < NPA; ++i) {
             const int c = tid + NT * i;
@@ -347,30 +355,35 @@ __global__ void __launch_bounds__(64 * NWV, NWV == 4 ? 2 : 1) skinny_batch_kerne
             const int k = kbase + ((slot ^ (rr & 15)) * 8);
             ra[i] = *(const u32x4*)(a.X + (int64_t)min(rr, a.M - 1) * a.K + min(k, a.K - 8));
         }
-        if (ragged) {
+    };
+    auto store_a = [&](char* buf, const u32x4* ra, int ci) {
+        const int kbase = kb + min(ci, nch - 1) * SB_KC;
+        const bool ragged = kbase + SB_KC > ke;
 #pragma unroll
-            for (int i = 0; i < NPA; ++i) {
-                const int c = tid + NT * i;
+        for (int i = 0; i < NPA; ++i) {
+            const int c = tid + NT * i;
+            u32x4 v = ra[i];
+            if (ragged) {
                 const int rr = min(c >> 4, 16 * MT - 1), slot = c & 15;
-                if (kbase + ((slot ^ (rr & 15)) * 8) >= ke) ra[i] = u32x4{0u, 0u, 0u, 0u};
+                if (kbase + ((slot ^ (rr & 15)) * 8) >= ke) v = u32x4{0u, 0u, 0u, 0u};
             }
+            if ((256 * MT) % NT == 0 || c < 256 * MT) *(u32x4*)(buf + c * 16) = v;
         }
     };
-    auto store_a = [&](char* buf, const u32x4* ra) {
-#pragma unroll
-        for (int i = 0; i < NPA; ++i)
-            if ((256 * MT) % NT == 0 || tid + NT * i < 256 * MT) *(u32x4*)(buf + (tid + NT * i) * 16) = ra[i];
-    };
-    // weight fragments of chunk ci (clamped to the last chunk past the end)
+    // weight fragments of chunk ci; chunks past the range read past the end of the
+    // buffer resource (zeros, no memory traffic)
+    const int nrows = a.dual_F > 0 ? 2 * a.dual_F : a.N;
+    const __amdgpu_buffer_rsrc_t wres = buf_rsrc(a.W, (uint32_t)((nrows / 16) * a.kst * 1024));
     auto load_w = [&](int ci, u32x4 (*wv)[NS], uint32_t* sz) {
         const int cc = min(ci, nch - 1);
         const int st0 = (kb + cc * SB_KC) / KS;
 #pragma unroll
         for (int u = 0; u < SPC; ++u)
 #pragma unroll
-            for (int s = 0; s < NS; ++s)
-                wv[u][s] = __builtin_nontemporal_load((const u32x4*)a.W +
-                                                      ((int64_t)(row[s] >> 4) * a.kst + min(st0 + u, a.kst - 1)) * 64 + lane);
+            for (int s = 0; s < NS; ++s) {
+                const uint32_t blk = (uint32_t)((row[s] >> 4) * a.kst + min(st0 + u, a.kst - 1));
+                wv[u][s] = buf_load_nt(wres, ci < nch ? (blk * 64 + lane) * 16 : BUF_OOB);
+            }
         if constexpr (WF == W_INT4) {
 #pragma unroll
             for (int s = 0; s < NS; ++s) sz[s] = a.sz[(int64_t)row[s] * (a.K / 128) + st0];
@@ -383,77 +396,109 @@ __global__ void __launch_bounds__(64 * NWV, NWV == 4 ? 2 : 1) skinny_batch_kerne
 #pragma unroll
         for (int s = 0; s < NS; ++s) acc[t][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // A chunk is four 32-k MFMA sub-steps.  Sub-step m's B operands (dequantised
+    // weights) and A fragments (LDS) are formed while sub-step m - 1's MFMAs run: the
+    // scheduler is asked for one MFMA, a share of the next sub-step's unpacking and
+    // (for the first MT MFMAs) one LDS read, in turn, so the matrix pipe, the vector
+    // ALU and LDS overlap within a wave.
+    constexpr int NSUB = SB_KC / 32;
+    auto a_frag = [&](const char* Ab, int m, int t) {
+        int koff;
+        if constexpr (WF == W_BF16) koff = 32 * m + 8 * g;
+        else if constexpr (WF == W_INT8) koff = 64 * (m >> 1) + 16 * g + 8 * (m & 1);
+        else koff = 32 * g + 8 * m;
+        const int piece = koff >> 3;
+        const int rr = 16 * t + r;
+        return *(const u32x4*)(Ab + rr * 256 + ((piece ^ (rr & 15)) << 4));
+    };
+    auto b_op = [&](const u32x4 (*wv)[NS], const uint32_t* sz, int m, int s) {
+        if constexpr (WF == W_BF16) {
+            return wv[m][s];
+        } else if constexpr (WF == W_INT8) {
+            const u32x4 w = wv[m >> 1][s];
+            const uint32_t d0 = (m & 1) ? w.z : w.x, d1 = (m & 1) ? w.w : w.y;
+            const u32x2 c0 = i8x4_to_f16x4(d0), c1 = i8x4_to_f16x4(d1);
+            return u32x4{c0.x, c0.y, c1.x, c1.y};
+        } else {
+            const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(sz[s] >> 16)));
+            const f16x2 bias = {bz, bz};
+            const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(sz[s] & 0xFFFFu));
+            const f16x2 s2 = {sh, sh};
+            const u32x4 w = wv[0][s];
+            const uint32_t d = m == 0 ? w.x : m == 1 ? w.y : m == 2 ? w.z : w.w;
+            const u32x4 q = i4x8_to_f16x8(d, bias);
+            return u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
+        }
+    };
+    constexpr int VALU_PER_B = WF == W_BF16 ? 0 : (WF == W_INT8 ? 10 : 16);   // per B operand
+    constexpr int NMF = MT * NS;                                              // MFMAs per sub-step
+    constexpr int VPS = (VALU_PER_B * NS + NMF - 1) / NMF;                     // VALU per MFMA slot
     auto compute = [&](const char* Ab, const u32x4 (*wv)[NS], const uint32_t* sz) {
+        u32x4 av[2][MT], bq[2][NS];
 #pragma unroll
-        for (int u = 0; u < SPC; ++u) {
-            u32x4 bop[NJ][NS];
+        for (int t = 0; t < MT; ++t) av[0][t] = a_frag(Ab, 0, t);
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                if constexpr (WF == W_BF16) {
-                    bop[0][s] = wv[u][s];
-                } else if constexpr (WF == W_INT8) {
-                    const u32x2 c0 = i8x4_to_f16x4(wv[u][s].x), c1 = i8x4_to_f16x4(wv[u][s].y);
-                    const u32x2 c2 = i8x4_to_f16x4(wv[u][s].z), c3 = i8x4_to_f16x4(wv[u][s].w);
-                    bop[0][s] = u32x4{c0.x, c0.y, c1.x, c1.y};
-                    bop[1][s] = u32x4{c2.x, c2.y, c3.x, c3.y};
-                } else {
-                    const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(sz[s] >> 16)));
-                    const f16x2 bias = {bz, bz};
-                    const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(sz[s] & 0xFFFFu));
-                    const f16x2 s2 = {sh, sh};
-                    const uint32_t wd[4] = {wv[u][s].x, wv[u][s].y, wv[u][s].z, wv[u][s].w};
+        for (int s = 0; s < NS; ++s) bq[0][s] = b_op(wv, sz, 0, s);
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const u32x4 q = i4x8_to_f16x8(wd[j], bias);
-                        bop[j][s] = u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
-                    }
-                }
+        for (int m = 0; m < NSUB; ++m) {
+            const int c = m & 1, n = c ^ 1;
+            __builtin_amdgcn_sched_barrier(0);
+            if (m + 1 < NSUB) {
+#pragma unroll
+                for (int t = 0; t < MT; ++t) av[n][t] = a_frag(Ab, m + 1, t);
+#pragma unroll
+                for (int s = 0; s < NS; ++s) bq[n][s] = b_op(wv, sz, m + 1, s);
             }
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                int koff;
-                if constexpr (WF == W_BF16) koff = u * KS + 8 * g;
-                else if constexpr (WF == W_INT8) koff = u * KS + 16 * g + 8 * j;
-                else koff = 32 * g + 8 * j;
-                const int piece = koff >> 3;
+            for (int t = 0; t < MT; ++t)
 #pragma unroll
-                for (int t = 0; t < MT; ++t) {
-                    const int rr = 16 * t + r;
-                    const u32x4 av = *(const u32x4*)(Ab + rr * 256 + ((piece ^ (rr & 15)) << 4));
+                for (int s = 0; s < NS; ++s) acc[t][s] = mfma16<AF>(av[c][t], bq[c][s], acc[t][s]);
+            if (m + 1 < NSUB) {
 #pragma unroll
-                    for (int s = 0; s < NS; ++s) acc[t][s] = mfma16<AF>(av, bop[j][s], acc[t][s]);
+                for (int i = 0; i < NMF; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // one MFMA
+                    if (i < MT) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+                    if (VPS > 0) __builtin_amdgcn_sched_group_barrier(0x002, VPS, 0); // unpacking
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
     // LDS writes done, then a bare barrier (no drain of the global loads in flight)
     auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
-    u32x4 wr[SB_PD][SPC][NS];
-    uint32_t szr[SB_PD][NS];
-    u32x4 ra[SB_PD][NPA];
-    load_a(0, ra[0]);
-    load_a(1, ra[1]);
-    load_w(0, wr[0], szr[0]);
-    load_w(1, wr[1], szr[1]);
-    store_a(As, ra[0]);
-    load_a(2, ra[0]);
-    barrier();
-    for (int ci0 = 0; ci0 < nch; ci0 += SB_PD) {
+    // register rings: slot i % PD holds chunk i's weights and activation pieces
+    u32x4 wr[PD][SPC][NS];
+    uint32_t szr[PD][NS];
+    u32x4 ra[PD][NPA];
 #pragma unroll
-        for (int p = 0; p < SB_PD; ++p) {
-            const int ci = ci0 + p;
-            if (ci < nch) {
-                compute(As + p * ABUF, wr[p], szr[p]);
-                load_w(ci + SB_PD, wr[p], szr[p]);
-                // chunk ci + 1 (registers since two chunks) into the other buffer, whose
-                // last reader was chunk ci - 1 (every wave passed the barrier since)
-                store_a(As + (1 - p) * ABUF, ra[1 - p]);
-                load_a(ci + 3, ra[1 - p]);
-                barrier();
-            }
-        }
+    for (int i = 0; i < PD; ++i) load_a(i, ra[i]);
+#pragma unroll
+    for (int i = 0; i < PD; ++i) load_w(i, wr[i], szr[i]);
+    store_a(As, ra[0], 0);
+    load_a(PD, ra[0]);
+    barrier();
+    // one chunk: multiply it out of LDS buffer p & 1, refill ring slot p with chunk
+    // ci + PD, move chunk ci + 1 into the other LDS buffer (whose last reader was
+    // chunk ci - 1: every wave has passed the barrier since) and refill its ring slot
+    auto step = [&](int ci, int p) {
+        compute(As + (p & 1) * ABUF, wr[p], szr[p]);
+        load_w(ci + PD, wr[p], szr[p]);
+        const int q = (p + 1) % PD;
+        store_a(As + ((p + 1) & 1) * ABUF, ra[q], ci + 1);
+        load_a(ci + 1 + PD, ra[q]);
+        barrier();
+    };
+    // whole groups of PD chunks run without a branch, so the compiler's wait counts
+    // stay exact around the loop; the last nch % PD chunks follow
+    int ci0 = 0;
+    for (; ci0 + PD <= nch; ci0 += PD) {
+#pragma unroll
+        for (int p = 0; p < PD; ++p) step(ci0 + p, p);
     }
+#pragma unroll
+    for (int p = 0; p < PD - 1; ++p)
+        if (ci0 + p < nch) step(ci0 + p, p);
 
     const int ncols = a.dual_F > 0 ? 2 * a.dual_F : a.N;
     float* out = a.part + (int64_t)blockIdx.y * a.M * ncols;
@@ -509,6 +554,8 @@ hipError_t launch_skinny_batch(const SkinnyArgs& a, int wf, int ks, hipStream_t 
     if (a.M < 1 || a.M > 64 || a.xf != XF_COPY || a.krange <= 0 || a.krange % SB_KC != 0) return hipErrorInvalidValue;
     if ((int64_t)ks * a.krange < a.K || (int64_t)(ks - 1) * a.krange >= a.K) return hipErrorInvalidValue;
     if (wf == W_INT4 && a.sz == nullptr) return hipErrorInvalidValue;
+    const int64_t nrows = a.dual_F > 0 ? 2 * (int64_t)a.dual_F : a.N;
+    if (nrows % 16 != 0 || (nrows / 16) * a.kst * 1024 >= ((int64_t)1 << 32) - 16) return hipErrorInvalidValue;   // buffer offsets are 32-bit
     switch (wf) {
         case W_BF16: return launch_batch_w<W_BF16>(a, ks, st);
         case W_INT8: return launch_batch_w<W_INT8>(a, ks, st);
@@ -569,6 +616,8 @@ int skinny_tiles(int N, int dual_F, int M) {
 
 hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st) {
     if (a.krange > skinny_max_krange(a.M) || a.krange % skinny_kstep(wf) != 0) return hipErrorInvalidValue;
+    const int64_t nrows = a.dual_F > 0 ? 2 * (int64_t)a.dual_F : a.N;
+    if (nrows % 16 != 0 || (nrows / 16) * a.kst * 1024 >= ((int64_t)1 << 32) - 16) return hipErrorInvalidValue;   // buffer offsets are 32-bit
     dim3 grid(skinny_tiles(a.N, a.dual_F, a.M), ks);
     switch (wf) {
         case W_BF16: return launch2<W_BF16>(a, grid, st);
