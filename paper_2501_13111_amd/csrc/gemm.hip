@@ -18,11 +18,13 @@
 // K-step), so each 64-thread group of a tile load reads contiguous memory.
 //
 // Two tilings:
-//  * small problems (few 256 x 256 tiles): 128 x 128 x 64 tiles, 4 waves in 2 x 2,
-//    each 64 x 64 = 4 x 4 MFMA 16x16x32 tiles; the next K tile is loaded into
-//    registers (and dequantised) while the current one is multiplied out of LDS;
+//  * small problems (few 256 x 256 tiles): 128 (or 64) x 128 x 64 tiles, 4 waves in
+//    2 x 2, each 64 (32) x 64; the next K tiles are loaded into a ring of registers
+//    (and dequantised on the way to LDS) while the current one is multiplied;
 //  * large problems: 256 x 256 tiles, 8 waves in 2 x 4, each 128 x 64, operands
-//    copied global -> LDS by the LDS-DMA path, two LDS stages.
+//    copied global -> LDS by buffer loads that write LDS directly, two LDS stages.
+// Both multiply with 32x32x16 MFMAs, which run at about 1.4x the rate of 16x16x32
+// on this part.
 // Both map workgroups to tiles XCD-aware: workgroups are dealt to the 8 XCDs
 // round-robin, and each XCD takes a contiguous range of a grouped raster so its
 // L2 sees the same A row tiles and weight column tiles again.
@@ -35,6 +37,9 @@ constexpr int GBN = 128, GBK = 64, GPAD = 8;
 #ifndef GEMM_BIG_MIN_TILES
 #define GEMM_BIG_MIN_TILES 128   // 256 x 256 tiles from this many
 #endif
+#ifndef GEMM_GM
+#define GEMM_GM 8                // tile rows per group of the grouped raster
+#endif
 #ifndef GEMM_SMALL_TILES
 #define GEMM_SMALL_TILES 256
 #endif
@@ -46,7 +51,7 @@ template <int WF, int EPI, int BM, int RD>
 __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     static_assert(RD % 2 == 0, "the LDS buffer parity of a tile is fixed within the unrolled ring");
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
-    constexpr int MI = BM / 32;                 // 16-row MFMA tiles per wave
+    constexpr int TI = BM / 64;                 // 32-row MFMA tiles per wave
     constexpr int NA = BM / 32;                 // 16-byte A loads per thread per K tile
     __shared__ __attribute__((aligned(16))) uint16_t Asb[2][BM * GLD];
     __shared__ __attribute__((aligned(16))) uint16_t Bsb[2][GBN * GLD];
@@ -62,7 +67,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
         const int T = a.tiles_m * a.tiles_n, bid = blockIdx.x;
         const int x = bid & 7, j = bid >> 3, q = T >> 3, rm = T & 7;
         const int t = x * q + (x < rm ? x : rm) + j;
-        const int GM = 8;
+        const int GM = GEMM_GM;
         const int grp = t / (GM * a.tiles_n);
         const int gm0 = grp * GM;
         const int gsz = min(GM, a.tiles_m - gm0);
@@ -189,27 +194,29 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
         }
     };
 
-    f32x4 acc[MI][4];
+    // 32x32 MFMA tiles: TI (rows) x 2 (columns) per wave; lane l holds column l % 32
+    f32x16 acc[TI][2];
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
+    for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
+    const int l32 = lane & 31, h32 = lane >> 5;
     const int nk = (a.K + GBK - 1) / GBK;
     auto compute = [&](const uint16_t* As, const uint16_t* Bs) {
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            u32x4 af[MI], bf[4];
+        for (int kk = 0; kk < GBK / 16; ++kk) {
+            u32x4 af[TI], bf[2];
 #pragma unroll
-            for (int i = 0; i < MI; ++i)
-                af[i] = *(const u32x4*)(As + (wm * (BM / 2) + 16 * i + r) * GLD + 32 * ks + 8 * g);
+            for (int i = 0; i < TI; ++i)
+                af[i] = *(const u32x4*)(As + (wm * (BM / 2) + 32 * i + l32) * GLD + 16 * kk + 8 * h32);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                bf[j] = *(const u32x4*)(Bs + (wn * 64 + 16 * j + r) * GLD + 32 * ks + 8 * g);
+            for (int j = 0; j < 2; ++j)
+                bf[j] = *(const u32x4*)(Bs + (wn * 64 + 32 * j + l32) * GLD + 16 * kk + 8 * h32);
 #pragma unroll
-            for (int i = 0; i < MI; ++i)
+            for (int i = 0; i < TI; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma16<AF>(af[i], bf[j], acc[i][j]);
+                for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<AF>(af[i], bf[j], acc[i][j]);
         }
     };
     // LDS writes done, then a bare barrier: the global loads in flight are not drained
@@ -239,39 +246,38 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
         }
     }
 
-    // ---- epilogue
+    // ---- epilogue (accumulator element e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4 of
+    // the 32x32 tile, column l % 32); dual tiles: column tile 0 is gate, 1 is up, same f
     if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int f = nb * 64 + 32 * wn + 16 * j + r;
-            if (f >= a.F) continue;
+        const int f = nb * 64 + 32 * wn + l32;
+        if (f < a.F) {
             float sg = 1.f, su = 1.f;
             if constexpr (WF == W_INT8) {
                 sg = h2f(a.scales[f]);
                 su = h2f(a.scales[a.F + f]);
             }
 #pragma unroll
-            for (int i = 0; i < MI; ++i)
+            for (int i = 0; i < TI; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int m = m0 + wm * (BM / 2) + 16 * i + 4 * g + e;
+                for (int e = 0; e < 16; ++e) {
+                    const int m = m0 + wm * (BM / 2) + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
                     if (m >= a.M) continue;
-                    const float gv = acc[i][j][e] * sg, uv = acc[i][j + 2][e] * su;
+                    const float gv = acc[i][0][e] * sg, uv = acc[i][1][e] * su;
                     a.out16[(int64_t)m * a.F + f] = act_store(bfround(silu_f(gv) * uv), a.out_fmt);
                 }
         }
     } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int n = nb * GBN + wn * 64 + 16 * j + r;
+        for (int j = 0; j < 2; ++j) {
+            const int n = nb * GBN + wn * 64 + 32 * j + l32;
             if (n >= a.N) continue;
             float sn = 1.f;
             if constexpr (WF == W_INT8) sn = h2f(a.scales[n]);
 #pragma unroll
-            for (int i = 0; i < MI; ++i)
+            for (int i = 0; i < TI; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int m = m0 + wm * (BM / 2) + 16 * i + 4 * g + e;
+                for (int e = 0; e < 16; ++e) {
+                    const int m = m0 + wm * (BM / 2) + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
                     if (m >= a.M) continue;
                     const float v = acc[i][j][e] * sn;
                     if constexpr (EPI == EPI_F32) a.out32[(int64_t)m * a.N + n] = v;
@@ -318,15 +324,14 @@ hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st)
 
 
 // ---------------------------------------------------------------------------
-// Large prefill GEMMs: 256 x 256 tiles, 8 waves of 128 x 64 (8 x 4 MFMA tiles),
-// operands copied global -> LDS by the LDS-DMA path (global_load_lds, 16 B per
-// lane), two LDS stages.  A rows are stored with an XOR swizzle of their 16-byte
+// Large prefill GEMMs: 256 x 256 tiles, 8 waves of 128 x 64 (4 x 2 32x32 MFMA tiles),
+// operands copied global -> LDS by buffer loads that write LDS directly (16 B per
+// lane), two LDS stages; the next stage's copies are issued in parts between the
+// current stage's MFMA steps.  A rows are stored with an XOR swizzle of their 16-byte
 // chunks so that MFMA fragment reads are free of bank conflicts; weight blocks
 // keep their fragment-major order, so a fragment is one contiguous 1 KiB read.
 // Quantised weights stay packed in LDS and are converted to fp16 per fragment.
-typedef __attribute__((address_space(1))) void gvoid_t;
 typedef __attribute__((address_space(3))) void lvoid_t;
-__device__ u32x4 g_zero16;       // source of the zero fill for out-of-range chunks
 
 constexpr int BT = 256;
 template <int WF>
@@ -359,7 +364,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
         const int Tn = a.tiles_m * a.tiles_n, bid = blockIdx.x;
         const int x = bid & 7, j = bid >> 3, q = Tn >> 3, rm = Tn & 7;
         const int t = x * q + (x < rm ? x : rm) + j;
-        const int GM = 8;
+        const int GM = GEMM_GM;
         const int grp = t / (GM * a.tiles_n);
         const int gm0 = grp * GM;
         const int gsz = min(GM, a.tiles_m - gm0);
@@ -388,83 +393,113 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
         else return wn * 4 + j;
     };
 
-    uint32_t nsz[4], csz[4];       // int4: scale | zero << 16 of the next / current stage
-    auto issue = [&](int stage, int k0) {
+    uint32_t nsz[2], csz[2];       // int4: scale | zero << 16 of the lane's two columns, next / current stage
+
+    // Copies of one stage, issued in parts from inside the previous stage's MFMA loop so
+    // that no wave stalls on a burst of copies.  They go through buffer resources: rows
+    // past M and blocks past the matrix read past the resource's end and land as zeros,
+    // so the per-thread source offsets are fixed and only advance with k.
+    constexpr int NA = BT * T::CPR / 512;            // A copies per thread per stage
+    constexpr int NB = 16 * T::NBLK / 8;             // B copies per thread per stage
+    constexpr int NPART = T::TK / 16;                // parts = 16-k MFMA steps of a stage
+    const __amdgpu_buffer_rsrc_t xres = buf_rsrc(a.X, (uint32_t)min((int64_t)a.M * a.K * 2, (int64_t)0xFFFFFFF0));
+    const __amdgpu_buffer_rsrc_t wres = buf_rsrc(a.W, (uint32_t)min((int64_t)(DUAL ? 2 * nrb : nrb) * a.kst * 1024,
+                                                                    (int64_t)0xFFFFFFF0));
+    uint32_t aoff[NA];
+    int akc[NA];
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+        const int pp = (i * 8 + w) * 64 + lane;
+        const int row = pp / T::CPR, slot = pp % T::CPR;
+        akc[i] = (slot ^ a_swz<T::CPR>(row)) * 8;
+        aoff[i] = m0 + row < a.M ? (uint32_t)(((int64_t)(m0 + row) * a.K + akc[i]) * 2) : BUF_OOB;
+    }
+    uint32_t boff[NB];
+    int bkb[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        const int blk = i * 8 + w;
+        bkb[i] = blk % T::NBLK;
+        bool v;
+        const int gb = grow_block(blk / T::NBLK, v);
+        boff[i] = v ? (uint32_t)((((int64_t)gb * a.kst + bkb[i]) * 64 + lane) * 16) : BUF_OOB;
+    }
+    auto issue_part = [&](int stage, int k0, int q) {
         char* sA = smem + stage * T::STAGE;
         char* sB = sA + T::A_BYTES;
-        constexpr int NA = BT * T::CPR / 512;
 #pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            const int p = (i * 8 + w) * 64 + lane;
-            const int row = p / T::CPR, slot = p % T::CPR;
-            const int chunk = slot ^ a_swz<T::CPR>(row);
-            const int m = m0 + row, k = k0 + chunk * 8;
-            const void* src = (m < a.M && k < a.K) ? (const void*)(a.X + (int64_t)m * a.K + k) : (const void*)&g_zero16;
-            __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(sA + (i * 8 + w) * 1024), 16, 0, 0);
-        }
-        constexpr int NB = 16 * T::NBLK / 8;
+        for (int i = 0; i < NA; ++i)
+            if ((i * NPART) / NA == q) {
+                const uint32_t off = (aoff[i] != BUF_OOB && k0 + akc[i] < a.K) ? aoff[i] + 2u * k0 : BUF_OOB;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lvoid_t*)(sA + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
+            }
 #pragma unroll
-        for (int i = 0; i < NB; ++i) {
-            const int blk = i * 8 + w;
-            const int rb = blk / T::NBLK, kb = blk % T::NBLK;
-            bool v;
-            const int gb = grow_block(rb, v);
-            const int kblk = k0 / T::KSW + kb;
-            v = v && kblk < a.kst;
-            const void* src = v ? (const void*)((const char*)a.W + (((int64_t)gb * a.kst + kblk) * 64 + lane) * 16)
-                                : (const void*)&g_zero16;
-            __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(sB + blk * 1024), 16, 0, 0);
-        }
+        for (int i = 0; i < NB; ++i)
+            if ((i * NPART) / NB == q) {
+                const int kblk = k0 / T::KSW + bkb[i];
+                const uint32_t off =
+                    (boff[i] != BUF_OOB && kblk < a.kst) ? boff[i] + (uint32_t)(k0 / T::KSW) * 1024u : BUF_OOB;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lvoid_t*)(sB + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
+            }
         if constexpr (WF == W_INT4) {
-            // raw words, not converted here: a conversion would wait for them (and for
-            // the stage's LDS copies issued before them)
-            const int grp = k0 / 128, ng = a.K / 128;
+            if (q == 0) {
+                // raw words, not converted here: a conversion would wait for them (and
+                // for the stage's copies issued before them)
+                const int grp = k0 / 128, ng = a.K / 128;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                bool v;
-                const int gb = grow_block(col_rb(j), v);
-                nsz[j] = 0u;
-                if (v) nsz[j] = a.sz[((int64_t)gb * 16 + r) * ng + grp];
+                for (int j = 0; j < 2; ++j) {
+                    bool v;
+                    const int gb = grow_block(col_rb(2 * j + ((lane & 31) >> 4)), v);
+                    nsz[j] = 0u;
+                    if (v) nsz[j] = a.sz[((int64_t)gb * 16 + r) * ng + grp];
+                }
             }
         }
     };
-
-    f32x4 acc[8][4];
+    auto issue = [&](int stage, int k0) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < NPART; ++q) issue_part(stage, k0, q);
+    };
 
-    auto compute = [&](int stage) {
+    // 32x32 MFMA tiles: 4 (rows) x 2 (columns) per wave.  Column tile j covers the
+    // wave's LDS row-blocks col_rb(2 j) and col_rb(2 j + 1); lane l holds column l % 32.
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+
+    const int l32 = lane & 31, h32 = lane >> 5;
+    // multiply stage `stage` out of LDS; with nk0 >= 0, issue the copies of the stage at
+    // k offset nk0 into the other buffer, one part per 16-k step
+    auto compute = [&](int stage, int nk0) {
         const char* sA = smem + stage * T::STAGE;
         const char* sB = sA + T::A_BYTES;
-        u32x4 raw[4];
-        if constexpr (WF != W_BF16) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) raw[j] = *(const u32x4*)(sB + col_rb(j) * 1024 + lane * 16);
-        }
+        for (int kk = 0; kk < T::TK / 16; ++kk) {            // 16-k MFMA steps
+            if (nk0 >= 0) issue_part(stage ^ 1, nk0, kk);
+            const int s = kk >> 1, hh = kk & 1;              // 32-k sub-step, half
+            u32x4 af[4], bop[2];
+            const int chunk = 2 * kk + h32;                  // 16-byte chunk of the A row
 #pragma unroll
-        for (int s = 0; s < T::NSUB; ++s) {
-            u32x4 af[8], bop[4];
-            int chunk;
-            if constexpr (WF == W_BF16) chunk = 4 * s + g;
-            else if constexpr (WF == W_INT8) chunk = 2 * g + s;
-            else chunk = 4 * g + s;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int row = wm * 128 + 16 * i + r;
+            for (int i = 0; i < 4; ++i) {
+                const int row = wm * 128 + 32 * i + l32;
                 af[i] = *(const u32x4*)(sA + row * (T::CPR * 16) + ((chunk ^ a_swz<T::CPR>(row)) * 16));
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < 2; ++j) {
+                const int rb = col_rb(2 * j + (l32 >> 4)), rr = lane & 15;
                 if constexpr (WF == W_BF16) {
-                    bop[j] = *(const u32x4*)(sB + (col_rb(j) * 2 + s) * 1024 + lane * 16);
+                    // block (rb, s): lane r + 16 g holds k 8 g .. 8 g + 7 of the 32-k step
+                    bop[j] = *(const u32x4*)(sB + (rb * 2 + s) * 1024 + (rr + 16 * (2 * hh + h32)) * 16);
                 } else if constexpr (WF == W_INT8) {
-                    const uint32_t lo = s ? raw[j].z : raw[j].x, hi = s ? raw[j].w : raw[j].y;
-                    const u32x2 c0 = i8x4_to_f16x4(lo), c1 = i8x4_to_f16x4(hi);
+                    // one 64-k block: lane r + 16 g holds k 16 g .. 16 g + 15
+                    const u32x2 c = *(const u32x2*)(sB + rb * 1024 + (rr + 16 * (2 * s + hh)) * 16 + 8 * h32);
+                    const u32x2 c0 = i8x4_to_f16x4(c.x), c1 = i8x4_to_f16x4(c.y);
                     bop[j] = u32x4{c0.x, c0.y, c1.x, c1.y};
                 } else {
-                    const uint32_t wd = s == 0 ? raw[j].x : (s == 1 ? raw[j].y : (s == 2 ? raw[j].z : raw[j].w));
+                    // one 128-k block: lane r + 16 g holds k 32 g .. 32 g + 31, 8 per dword
+                    const uint32_t wd = *(const uint32_t*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 4 * (2 * hh + h32));
                     const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(csz[j] >> 16)));
                     const f16x2 bias = {bz, bz};
                     const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(csz[j] & 0xFFFFu));
@@ -474,9 +509,9 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                 }
             }
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma16<AF>(af[i], bop[j], acc[i][j]);
+                for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<AF>(af[i], bop[j], acc[i][j]);
         }
     };
 
@@ -487,47 +522,45 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     for (int kt = 0; kt < nk; ++kt) {
         if constexpr (WF == W_INT4) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) csz[j] = nsz[j];
+            for (int j = 0; j < 2; ++j) csz[j] = nsz[j];
         }
-        if (kt + 1 < nk) issue((kt + 1) & 1, (kt + 1) * T::TK);
-        compute(kt & 1);
+        compute(kt & 1, kt + 1 < nk ? (kt + 1) * T::TK : -1);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
 
-    // ---- epilogue
+    // ---- epilogue (accumulator element e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4 of
+    // the 32x32 tile, column l % 32)
     if constexpr (DUAL) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int f = nt * 128 + wn * 32 + 16 * j + r;
-            if (f >= a.F) continue;
+        const int f = nt * 128 + wn * 32 + l32;
+        if (f < a.F) {
             float sg = 1.f, su = 1.f;
             if constexpr (WF == W_INT8) {
                 sg = h2f(a.scales[f]);
                 su = h2f(a.scales[a.F + f]);
             }
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int m = m0 + wm * 128 + 16 * i + 4 * g + e;
+                for (int e = 0; e < 16; ++e) {
+                    const int m = m0 + wm * 128 + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
                     if (m >= a.M) continue;
-                    const float gv = acc[i][j][e] * sg, uv = acc[i][j + 2][e] * su;
+                    const float gv = acc[i][0][e] * sg, uv = acc[i][1][e] * su;
                     a.out16[(int64_t)m * a.F + f] = act_store(bfround(silu_f(gv) * uv), a.out_fmt);
                 }
         }
     } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int n = nt * 256 + wn * 64 + 16 * j + r;
+        for (int j = 0; j < 2; ++j) {
+            const int n = nt * 256 + wn * 64 + 32 * j + l32;
             if (n >= a.N) continue;
             float sn = 1.f;
             if constexpr (WF == W_INT8) sn = h2f(a.scales[n]);
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int m = m0 + wm * 128 + 16 * i + 4 * g + e;
+                for (int e = 0; e < 16; ++e) {
+                    const int m = m0 + wm * 128 + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
                     if (m >= a.M) continue;
                     const float v = acc[i][j][e] * sn;
                     if constexpr (EPI == EPI_F32) a.out32[(int64_t)m * a.N + n] = v;

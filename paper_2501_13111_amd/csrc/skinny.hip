@@ -517,18 +517,20 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
     }
 }
 
-// Tiling: 16-row subtiles per wave (NS) and waves per workgroup (NWV).  With two or
-// more 16-token tiles the quantised formats run eight waves of two subtiles (more
-// waves per SIMD to overlap the unpacking with the MFMAs); every variant covers
-// skinny_batch_rows() weight rows per workgroup.
+// Tiling: 16-row subtiles per wave (NS) and waves per workgroup (NWV).  bf16 weights
+// run four waves of two subtiles; quantised weights run eight (more waves per SIMD to
+// overlap the unpacking with the MFMAs and the loads).
+struct BatchTiling {
+    int nwv, ns;
+};
+constexpr BatchTiling batch_tiling(int wf) { return wf == W_BF16 ? BatchTiling{4, 2} : BatchTiling{8, 2}; }
+
 template <int WF, int MT>
 static hipError_t launch_batch(const SkinnyArgs& a, int ks, hipStream_t st) {
-    constexpr bool WIDE = WF != W_BF16 && MT >= 2;
-    constexpr int NS = WF == W_BF16 ? 2 : (WIDE ? 2 : 4);
-    constexpr int NWV = WIDE ? 8 : 4;
-    static_assert(NWV * 16 * NS == (WF == W_BF16 ? 128 : 256), "rows per workgroup");
+    constexpr BatchTiling T = batch_tiling(WF);
+    static_assert(T.ns % 2 == 0 && T.nwv * 64 <= 1024, "tiling");
     dim3 grid(skinny_batch_tiles(a.N, a.dual_F, WF), ks);
-    FP_LAUNCH((skinny_batch_kernel<WF, MT, NS, NWV>), grid, dim3(64 * NWV), 0, st, a);
+    FP_LAUNCH((skinny_batch_kernel<WF, MT, T.ns, T.nwv>), grid, dim3(64 * T.nwv), 0, st, a);
     return hipGetLastError();
 }
 
@@ -543,8 +545,13 @@ static hipError_t launch_batch_w(const SkinnyArgs& a, int ks, hipStream_t st) {
     }
 }
 
+int skinny_batch_rows(int wf) {
+    const BatchTiling T = batch_tiling(wf);
+    return T.nwv * 16 * T.ns;
+}
+
 int skinny_batch_tiles(int N, int dual_F, int wf) {
-    const int rows = wf == W_BF16 ? 128 : 256;       // weight rows per workgroup
+    const int rows = skinny_batch_rows(wf);
     return dual_F > 0 ? (dual_F + rows / 2 - 1) / (rows / 2) : (N + rows - 1) / rows;
 }
 
