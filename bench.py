@@ -35,18 +35,25 @@ PROJ = {"qkv", "o", "gate_up", "down"}
 # HBM bytes per decode-projection launch of the weight-streaming kernel, from two
 # rocprofv3 --pmc passes (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0, the factors a 1 GiB device
 # copy gives), averaged over the qkv / o / gate_up / down launches.  Valid only for the
-# kernel sources they were taken on (hash of skinny.hip, fp_device.h, fp_internal.h);
-# the summary and the commands are in profiles/skinny_kernel_llama2-7b-bf16.md.
-SKINNY_TRAFFIC = {"llama2-7b-bf16": {"src": "ab291c8799a07db0", "bytes_per_launch": 102243459}}
-SKINNY_SRC = ("skinny.hip", "fp_device.h", "fp_internal.h")
+# kernel sources they were taken on (hash of skinny.hip, fp_device.h and the kernel's
+# argument block and input transforms in fp_internal.h); the summary and the commands
+# are in profiles/skinny_kernel_llama2-7b-bf16.md.
+SKINNY_TRAFFIC = {"llama2-7b-bf16": {"src": "02e8f33d930f9bb9", "bytes_per_launch": 102243459}}
+SKINNY_SRC = ("skinny.hip", "fp_device.h")
 
 
 def skinny_src_hash():
     import hashlib
+    import re
     h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2501_13111_amd", "csrc")
     for f in SKINNY_SRC:
-        with open(os.path.join(ROOT, "paper_2501_13111_amd", "csrc", f), "rb") as fh:
+        with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
+    with open(os.path.join(csrc, "fp_internal.h")) as fh:
+        hdr = fh.read()
+    m = re.search(r"enum XForm \{.*?\n\};\n.*?struct SkinnyArgs \{.*?\n\};", hdr, re.S)
+    h.update(m.group(0).encode() if m else b"")
     return h.hexdigest()[:16]
 
 

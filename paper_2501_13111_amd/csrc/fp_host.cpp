@@ -147,6 +147,7 @@ struct fp_layer {
     float* q32 = nullptr;         // rotated queries                      [Mmax, q_dim]
     float* part = nullptr;        // decode split-K partials              [KSMAX, Bmax, Ncol]
     float* part2 = nullptr;       // gate|up partials (read while down writes part)
+    float* ppart = nullptr;       // prefill split-K partials (GEMMs with too few large tiles)
     float* attn_ws = nullptr;     // decode attention partials
     float* ssq = nullptr;         // decode row-norm block sums         [Bmax, nblk]
     int* d_pos = nullptr;
@@ -420,18 +421,57 @@ RopeKvArgs rope_args(fp_layer* h, int l, const float* part, int ks, int M, int T
     return r;
 }
 
+// Split factor of a prefill GEMM on the large tiling (1: no split).  Splits are used
+// for the residual and SwiGLU GEMMs only, whose reductions (resid_norm_row_kernel,
+// swiglu_kernel) also finish the epilogue; the residual reduction keeps a row in one
+// workgroup, which bounds the hidden size.
+int prefill_split(const fp_layer* h, int M, int N, int K, int dual_F, int* krange) {
+    const int H = h->s.hidden;
+    if (H % 8 != 0 || H > 16384) return 1;
+    return gemm_split_factor(M, N, K, dual_F, h->wq, krange);
+}
+
+fp_status run_gemm_split(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, int ks, int krange,
+                         float* part, hipStream_t st) {
+    GemmArgs a{};
+    a.X = X;
+    a.W = m.codes;
+    a.scales = m.scales;
+    a.zeros = m.zeros;
+    a.sz = m.sz;
+    a.M = M;
+    a.N = m.N;
+    a.K = m.K;
+    a.kst = m.kst;
+    a.F = h->s.ffn;
+    a.out32 = part;
+    a.krange = krange;
+    HIPCHK(launch_gemm_split(a, h->wq, dual_F > 0, ks, st));
+    return FP_OK;
+}
+
 fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t* y, hipStream_t st) {
     const fp_shape& s = h->s;
     const int M = B * P;
     const float scale = (float)(1.0 / std::sqrt((double)s.head_dim));
     fp_status rc;
+    const int H = s.hidden, F = s.ffn;
+    int kr_o, kr_g, kr_d;
+    const int ks_o = prefill_split(h, M, H, h->q_dim, 0, &kr_o);
+    const int ks_g = prefill_split(h, M, 2 * F, H, F, &kr_g);
+    const int ks_d = prefill_split(h, M, H, F, 0, &kr_d);
+    bool normed = false;    // act_in already holds this layer's normalised input
     for (int l = 0; l < s.n_layers; ++l) {
         const LayerW& W = h->L[l];
+        const bool last = l == s.n_layers - 1;
         const uint16_t* in = (l == 0) ? x : h->xbuf;
-        uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
+        uint16_t* out = last ? y : h->xbuf;
         float* dump = h->dump ? h->dump + (size_t)l * 2 * M * h->kv_dim : nullptr;
-        h->prof.mark(FP_K_RMSNORM, l);
-        HIPCHK(launch_rmsnorm(in, M, s.hidden, W.attn_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+        if (!normed) {
+            h->prof.mark(FP_K_RMSNORM, l);
+            HIPCHK(launch_rmsnorm(in, M, s.hidden, W.attn_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+        }
+        normed = false;
         h->prof.mark(FP_K_QKV, l);
         if ((rc = run_gemm(h, h->act_in, W.qkv, M, EPI_F32, h->qkv32, nullptr, nullptr, st))) return rc;
         h->prof.mark(FP_K_ROPE_KV, l);
@@ -456,13 +496,33 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
         h->prof.mark(FP_K_ATTN, l);
         HIPCHK(launch_attn_prefill(aa, B, st));
         h->prof.mark(FP_K_O, l);
-        if ((rc = run_gemm(h, h->act_o, W.o, M, EPI_RESID, nullptr, h->hbuf, in, st))) return rc;
-        h->prof.mark(FP_K_RMSNORM, l);
-        HIPCHK(launch_rmsnorm(h->hbuf, M, s.hidden, W.mlp_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+        if (ks_o > 1) {
+            // split-K partials; the residual add and the MLP RMSNorm in one row kernel
+            if ((rc = run_gemm_split(h, h->act_o, W.o, M, 0, ks_o, kr_o, h->ppart, st))) return rc;
+            HIPCHK(launch_resid_norm(h->ppart, ks_o, M, H, in, h->hbuf, W.mlp_norm, s.rms_eps, h->act_in,
+                                     h->act_fmt, nullptr, nullptr, st));
+        } else {
+            if ((rc = run_gemm(h, h->act_o, W.o, M, EPI_RESID, nullptr, h->hbuf, in, st))) return rc;
+            h->prof.mark(FP_K_RMSNORM, l);
+            HIPCHK(launch_rmsnorm(h->hbuf, M, s.hidden, W.mlp_norm, s.rms_eps, h->act_in, h->act_fmt, st));
+        }
         h->prof.mark(FP_K_GATE_UP, l);
-        if ((rc = run_gemm(h, h->act_in, W.gu, M, EPI_SWIGLU, nullptr, h->act_f, nullptr, st))) return rc;
+        if (ks_g > 1) {
+            if ((rc = run_gemm_split(h, h->act_in, W.gu, M, F, ks_g, kr_g, h->ppart, st))) return rc;
+            HIPCHK(launch_swiglu(h->ppart, ks_g, M, F, h->act_f, h->act_fmt, st));
+        } else {
+            if ((rc = run_gemm(h, h->act_in, W.gu, M, EPI_SWIGLU, nullptr, h->act_f, nullptr, st))) return rc;
+        }
         h->prof.mark(FP_K_DOWN, l);
-        if ((rc = run_gemm(h, h->act_f, W.down, M, EPI_RESID, nullptr, out, h->hbuf, st))) return rc;
+        if (ks_d > 1) {
+            // the residual add, and the next layer's attention RMSNorm
+            if ((rc = run_gemm_split(h, h->act_f, W.down, M, 0, ks_d, kr_d, h->ppart, st))) return rc;
+            HIPCHK(launch_resid_norm(h->ppart, ks_d, M, H, h->hbuf, out, last ? nullptr : h->L[l + 1].attn_norm,
+                                     s.rms_eps, h->act_in, h->act_fmt, nullptr, nullptr, st));
+            normed = !last;
+        } else {
+            if ((rc = run_gemm(h, h->act_f, W.down, M, EPI_RESID, nullptr, out, h->hbuf, st))) return rc;
+        }
         if (h->ldump) HIPCHK(hipMemcpyAsync(h->ldump + (size_t)l * M * s.hidden, out, (size_t)M * s.hidden * 2,
                                             hipMemcpyDeviceToDevice, st));
     }
@@ -723,6 +783,22 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     if ((st = alloc_t(h, &h->q32, Mmax * h->q_dim, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return bail(st);
     if ((st = alloc_t(h, &h->part2, (size_t)KSMAX * s.max_batch * 2 * F, &h->bytes_ws))) return bail(st);
+    {
+        // the largest split-K partial buffer any prefill size up to Mmax asks for (the split
+        // factor depends on the number of 256-row tiles, so the worst case is at a whole tile)
+        size_t pp = 0;
+        const int Mp = (int)act_elems(h);
+        for (int tm = 1; (int64_t)(tm - 1) * 256 < Mp; ++tm) {
+            const int M = std::min(tm * 256, Mp);
+            int kr;
+            const int ko = prefill_split(h, M, H, h->q_dim, 0, &kr);
+            const int kg = prefill_split(h, M, 2 * F, H, F, &kr);
+            const int kd = prefill_split(h, M, H, F, 0, &kr);
+            pp = std::max({pp, (size_t)(ko > 1 ? ko : 0) * M * H, (size_t)(kg > 1 ? kg : 0) * M * 2 * F,
+                           (size_t)(kd > 1 ? kd : 0) * M * H});
+        }
+        if (pp > 0 && (st = alloc_t(h, &h->ppart, pp, &h->bytes_ws))) return bail(st);
+    }
     const size_t nch = attn_decode_max_splits(s.max_seq);
     if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 4), &h->bytes_ws)))
         return bail(st);

@@ -29,7 +29,9 @@ extern thread_local LaunchTimer g_launch_timer;
     } while (0)
 
 enum WFmt { W_BF16 = 0, W_INT8 = 1, W_INT4 = 2 };
-enum Epi { EPI_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+// EPI_PART: fp32 partial sums of one k-split, [ks, M, N] (or [ks, M, 2F] for the
+// [gate; up] matrix), multiplied by the int8 row scales; a reduction kernel finishes.
+enum Epi { EPI_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PART = 3 };
 // Activation format of a GEMM's A operand: bf16 for bf16 weights, fp16 for quantised
 // weights (the fp16 copy of a bf16-rounded value is exact in fp16's normal range).
 enum ActFmt { ACT_BF16 = 0, ACT_F16 = 1 };
@@ -86,6 +88,7 @@ struct GemmArgs {
     uint16_t* out16;          // EPI_RESID: bf16 [M, N]; EPI_SWIGLU: act [M, F]
     const uint16_t* resid;    // EPI_RESID: bf16 [M, N]
     int out_fmt;              // EPI_SWIGLU activation format
+    int krange;               // EPI_PART: k per split (multiple of the large tiling's k per stage)
     int tiles_m, tiles_n;     // set by the launcher
 };
 
@@ -197,6 +200,11 @@ int skinny_batch_tiles(int N, int dual_F, int wf);
 int skinny_batch_chunk();
 hipError_t launch_skinny_batch(const SkinnyArgs& a, int wf, int ks, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st);
+// Split-K on the large tiling for prefill GEMMs with too few 256 x 256 tiles to fill
+// the GPU: the split factor (1: no split) and k per split for an [M, N] x [N, K]
+// product (dual_F > 0: the [gate; up] matrix), and the launch writing EPI_PART partials.
+int gemm_split_factor(int M, int N, int K, int dual_F, int wf, int* krange);
+hipError_t launch_gemm_split(const GemmArgs& a, int wf, bool dual, int ks, hipStream_t st);
 
 int attn_decode_max_splits(int max_seq);
 int attn_decode_partials(int nsplit);

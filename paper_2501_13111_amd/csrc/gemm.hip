@@ -289,7 +289,13 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
 
 // register ring depth: deeper for 64-row tiles (one workgroup per CU, nothing else to
 // hide the load latency)
-template <int WF, int BM, int RD = (BM == 64 ? 4 : 2)>
+#ifndef GEMM_RD64
+#define GEMM_RD64 4
+#endif
+#ifndef GEMM_RD128
+#define GEMM_RD128 2
+#endif
+template <int WF, int BM, int RD = (BM == 64 ? GEMM_RD64 : GEMM_RD128)>
 static hipError_t launch_wm(const GemmArgs& a, int epi, hipStream_t st) {
     GemmArgs b = a;
     b.tiles_n = (epi == EPI_SWIGLU) ? (a.F + 63) / 64 : (a.N + GBN - 1) / GBN;
@@ -349,11 +355,11 @@ struct BigT {
 template <int CPR>
 __device__ __forceinline__ int a_swz(int row) { return CPR == 8 ? ((row >> 1) & 7) : (row & 15); }
 
-template <int WF, int EPI>
+template <int WF, int EPI, bool DUAL>
 __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     using T = BigT<WF>;
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
-    constexpr bool DUAL = EPI == EPI_SWIGLU;
+    static_assert(DUAL == (EPI == EPI_SWIGLU) || EPI == EPI_PART, "dual tiling");
     __shared__ __attribute__((aligned(1024))) char smem[2 * T::STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -515,8 +521,11 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
         }
     };
 
-    const int nk = (a.K + T::TK - 1) / T::TK;
-    issue(0, 0);
+    // k-range of this workgroup (the whole of K unless the GEMM is split)
+    const int kb = EPI == EPI_PART ? blockIdx.y * a.krange : 0;
+    const int ke = EPI == EPI_PART ? min(a.K, kb + a.krange) : a.K;
+    const int nk = (ke - kb + T::TK - 1) / T::TK;
+    issue(0, kb);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
@@ -524,14 +533,33 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
 #pragma unroll
             for (int j = 0; j < 2; ++j) csz[j] = nsz[j];
         }
-        compute(kt & 1, kt + 1 < nk ? (kt + 1) * T::TK : -1);
+        compute(kt & 1, kt + 1 < nk ? kb + (kt + 1) * T::TK : -1);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
 
     // ---- epilogue (accumulator element e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4 of
     // the 32x32 tile, column l % 32)
-    if constexpr (DUAL) {
+    if constexpr (EPI == EPI_PART) {
+        const int ncols = DUAL ? 2 * a.F : a.N;
+        float* out = a.out32 + (int64_t)blockIdx.y * a.M * ncols;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            int n;
+            if constexpr (DUAL) n = (j == 0 ? 0 : a.F) + nt * 128 + wn * 32 + l32;
+            else n = nt * 256 + wn * 64 + 32 * j + l32;
+            if (DUAL ? nt * 128 + wn * 32 + l32 >= a.F : n >= a.N) continue;
+            float sn = 1.f;
+            if constexpr (WF == W_INT8) sn = h2f(a.scales[n]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int m = m0 + wm * 128 + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
+                    if (m < a.M) out[(int64_t)m * ncols + n] = acc[i][j][e] * sn;
+                }
+        }
+    } else if constexpr (DUAL) {
         const int f = nt * 128 + wn * 32 + l32;
         if (f < a.F) {
             float sg = 1.f, su = 1.f;
@@ -577,12 +605,56 @@ static hipError_t launch_big(const GemmArgs& a, int epi, hipStream_t st) {
     b.tiles_m = (a.M + BT - 1) / BT;
     dim3 grid(b.tiles_n * b.tiles_m);
     switch (epi) {
-        case EPI_F32: FP_LAUNCH((gemm_big_kernel<WF, EPI_F32>), grid, dim3(512), 0, st, b); break;
-        case EPI_RESID: FP_LAUNCH((gemm_big_kernel<WF, EPI_RESID>), grid, dim3(512), 0, st, b); break;
-        case EPI_SWIGLU: FP_LAUNCH((gemm_big_kernel<WF, EPI_SWIGLU>), grid, dim3(512), 0, st, b); break;
+        case EPI_F32: FP_LAUNCH((gemm_big_kernel<WF, EPI_F32, false>), grid, dim3(512), 0, st, b); break;
+        case EPI_RESID: FP_LAUNCH((gemm_big_kernel<WF, EPI_RESID, false>), grid, dim3(512), 0, st, b); break;
+        case EPI_SWIGLU: FP_LAUNCH((gemm_big_kernel<WF, EPI_SWIGLU, true>), grid, dim3(512), 0, st, b); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+template <int WF>
+static hipError_t launch_big_split(const GemmArgs& a, bool dual, int ks, hipStream_t st) {
+    GemmArgs b = a;
+    b.tiles_n = dual ? (a.F + 127) / 128 : (a.N + BT - 1) / BT;
+    b.tiles_m = (a.M + BT - 1) / BT;
+    dim3 grid(b.tiles_n * b.tiles_m, ks);
+    if (dual) FP_LAUNCH((gemm_big_kernel<WF, EPI_PART, true>), grid, dim3(512), 0, st, b);
+    else FP_LAUNCH((gemm_big_kernel<WF, EPI_PART, false>), grid, dim3(512), 0, st, b);
+    return hipGetLastError();
+}
+
+static int big_tk(int wf) { return wf == W_INT4 ? BigT<W_INT4>::TK : BigT<W_BF16>::TK; }
+
+#ifndef GEMM_SPLIT_MAX
+#define GEMM_SPLIT_MAX 16
+#endif
+int gemm_split_factor(int M, int N, int K, int dual_F, int wf, int* krange) {
+    const int tiles = ((M + BT - 1) / BT) * (dual_F > 0 ? (dual_F + 127) / 128 : (N + BT - 1) / BT);
+    const int tk = big_tk(wf);
+    const int stages = (K + tk - 1) / tk;
+    *krange = stages * tk;
+    if (M < BT || tiles >= 256) return 1;
+    // one round of workgroups (one per compute unit), at least four stages per split
+    int ks = 256 / tiles;
+    if (ks > GEMM_SPLIT_MAX) ks = GEMM_SPLIT_MAX;
+    if (ks > stages / 4) ks = stages / 4;
+    if (ks < 2) return 1;
+    const int per = (stages + ks - 1) / ks;
+    *krange = per * tk;
+    return (stages + per - 1) / per;
+}
+
+hipError_t launch_gemm_split(const GemmArgs& a, int wf, bool dual, int ks, hipStream_t st) {
+    if (ks < 1 || a.krange <= 0 || a.krange % big_tk(wf) != 0 || (int64_t)ks * a.krange < a.K ||
+        (int64_t)(ks - 1) * a.krange >= a.K)
+        return hipErrorInvalidValue;
+    switch (wf) {
+        case W_BF16: return launch_big_split<W_BF16>(a, dual, ks, st);
+        case W_INT8: return launch_big_split<W_INT8>(a, dual, ks, st);
+        case W_INT4: return launch_big_split<W_INT4>(a, dual, ks, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_gemm_big(const GemmArgs& a, int wf, int epi, hipStream_t st) {

@@ -101,7 +101,7 @@ __global__ void __launch_bounds__(256) norm_apply_kernel(const uint16_t* __restr
 // Batches: one workgroup of 1024 threads per row does both steps, keeping the row in
 // registers (8 consecutive values per thread and pass, N <= 16384): out = bf16(resid +
 // sum_s part[s]) (skipped for ks == 0), the row's sum of squares by a block reduction,
-// then nout = act(bf16(out * r * g)).  One launch instead of two.
+// then nout = act(bf16(out * r * g)) (skipped for g == NULL).  One launch instead of two.
 constexpr int RN_T = 1024;
 __global__ void __launch_bounds__(RN_T) resid_norm_row_kernel(const float* __restrict__ part, int ks, int M, int N,
                                                                const uint16_t* __restrict__ resid,
@@ -145,22 +145,24 @@ __global__ void __launch_bounds__(RN_T) resid_norm_row_kernel(const float* __res
 #pragma unroll
         for (int e = 0; e < 8; ++e) ss += v[j][e] * v[j][e];
     }
-    ss = block_sum(ss, red);
-    const float r = 1.0f / __fsqrt_rn(ss / (float)N + eps);
+    if (g != nullptr) {
+        ss = block_sum(ss, red);
+        const float r = 1.0f / __fsqrt_rn(ss / (float)N + eps);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int n0 = (threadIdx.x + RN_T * j) * 8;
-        if (n0 >= N) continue;
-        const u32x4 gv = *(const u32x4*)(g + n0);
-        const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w};
-        uint32_t o[4];
+        for (int j = 0; j < 2; ++j) {
+            const int n0 = (threadIdx.x + RN_T * j) * 8;
+            if (n0 >= N) continue;
+            const u32x4 gv = *(const u32x4*)(g + n0);
+            const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w};
+            uint32_t o[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float e0 = bfround(v[j][2 * e] * r * __uint_as_float(gw[e] << 16));
-            const float e1 = bfround(v[j][2 * e + 1] * r * __uint_as_float(gw[e] & 0xFFFF0000u));
-            o[e] = (uint32_t)act_store(e0, nfmt) | ((uint32_t)act_store(e1, nfmt) << 16);
+            for (int e = 0; e < 4; ++e) {
+                const float e0 = bfround(v[j][2 * e] * r * __uint_as_float(gw[e] << 16));
+                const float e1 = bfround(v[j][2 * e + 1] * r * __uint_as_float(gw[e] & 0xFFFF0000u));
+                o[e] = (uint32_t)act_store(e0, nfmt) | ((uint32_t)act_store(e1, nfmt) << 16);
+            }
+            *(u32x4*)(nout + m * N + n0) = u32x4{o[0], o[1], o[2], o[3]};
         }
-        *(u32x4*)(nout + m * N + n0) = u32x4{o[0], o[1], o[2], o[3]};
     }
     if (d_pos && blockIdx.x == 0 && threadIdx.x == 0) *d_pos += 1;
 }
@@ -298,7 +300,7 @@ hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, fl
 hipError_t launch_resid_norm(const float* part, int ks, int M, int N, const uint16_t* resid,
                              uint16_t* out, const uint16_t* g, float eps, uint16_t* nout, int nfmt,
                              float* ssq, int* inc_pos, hipStream_t st) {
-    if (g != nullptr && M > 1 && N % 8 == 0 && N <= 2 * RN_T * 8) {
+    if ((g != nullptr || ks > 0) && M > 1 && N % 8 == 0 && N <= 2 * RN_T * 8) {
         FP_LAUNCH(resid_norm_row_kernel, dim3(M), dim3(RN_T), 0, st, part, ks, M, N, resid, out, g, eps, nout, nfmt,
                   inc_pos);
         return hipGetLastError();

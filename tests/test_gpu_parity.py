@@ -93,6 +93,11 @@ CASES = [
     ("batch40-int8", Shape(1, 256, 2, 2, 128, 384, 40, 20, 23), "int8", "int8", 40, 20, 3),
     ("batch64-int4", Shape(1, 256, 2, 2, 128, 384, 64, 9, 12), "int4", "bf16", 64, 9, 3),
     ("long-ctx-bf16", Shape(1, 256, 2, 2, 128, 384, 2, 520, 530), "bf16", "bf16", 2, 520, 3),
+    # prefill GEMMs with too few 256 x 256 tiles run split-K with reduction kernels
+    # (M >= 256; M = 300 leaves a ragged row tile)
+    ("splitk-bf16", Shape(2, 512, 4, 4, 128, 1024, 2, 160, 164), "bf16", "bf16", 2, 160, 2),
+    ("splitk-int4-int8kv", Shape(2, 1024, 8, 8, 128, 2048, 2, 160, 164), "int4", "int8", 2, 160, 2),
+    ("splitk-int8-gqa", Shape(2, 1024, 8, 4, 128, 2048, 1, 300, 302), "int8", "int8", 1, 300, 2),
 ]
 
 
