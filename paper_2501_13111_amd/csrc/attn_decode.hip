@@ -6,12 +6,11 @@
 // reading it is the second HBM stream of a decode step after the weights, and
 // with an INT8 KV cache (Sec. 3.2) it is half as many bytes.
 //
-// Two kernels:
-//  * qkv_rope_kernel reduces the qkv projection's split-K partial sums once, applies
-//    the rotary embedding to q and k, appends k and v to the cache -- bf16, or int8
-//    with s = fp16(absmax/127), code = rint(v/s) per (sequence, position, kv head) --
-//    and writes q in the MFMA operand format;
-//  * attn_decode_kernel attends.  Both contractions run on MFMA 16x16x32 (bf16 for a
+// One kernel, attn_decode_kernel.  Each workgroup reduces the qkv projection's split-K
+// partial sums for the queries of its group and rotates them; the workgroup whose
+// keys include the new position also rotates k and appends k and v to the cache --
+// bf16, or int8 with s = fp16(absmax/127), code = rint(v/s) per (sequence, position,
+// kv head) -- before its waves load that block.  Both contractions run on MFMA 16x16x32 (bf16 for a
 //    bf16 cache, fp16 for int8 codes, which are exact in fp16), in the transposed form
 //        S^T = K Q^T     A = 16 cached keys (rows), B = the G queries (columns)
 //        O^T += V^T P^T  A = 16 dims of a value block, B = the probabilities
@@ -40,31 +39,19 @@
 namespace fpk {
 
 // ---------------------------------------------------------------------------------
-// One 64-lane workgroup per (sequence, head slot): slots 0..nh-1 are query heads,
-// nh..nh+nkv-1 kv heads (K and V).  Lane j handles the rotation pair (j, j + D/2).
+// The new token's k and v for kv head kvh of sequence b, done by one wave (lane j
+// handles the rotation pair (j, j + D/2)): reduce the qkv projection's split-K
+// partial sums, rotate k, and append k and v to the cache (bf16, or int8 with
+// s = fp16(absmax/127), code = rint(x/s)).
 template <int D, bool KV8>
-__global__ void __launch_bounds__(64) qkv_rope_kernel(AttnDecArgs a) {
-    constexpr int AF = KV8 ? ACT_F16 : ACT_BF16;
-    const int slot = blockIdx.x, b = blockIdx.y, j = threadIdx.x;
-    const int pos = *a.d_pos;
+__device__ __forceinline__ void append_kv(const AttnDecArgs& a, int b, int kvh, int pos, int j) {
     const int Nqkv = (a.nh + 2 * a.nkv) * D;
     const int64_t pstride = (int64_t)a.batch * Nqkv;
     const float* prow = a.qkv_part + (int64_t)b * Nqkv;
-    const float c = j < D / 2 ? a.cos_t[(int64_t)pos * (D / 2) + j] : 0.f;
-    const float sn = j < D / 2 ? a.sin_t[(int64_t)pos * (D / 2) + j] : 0.f;
-    if (slot < a.nh) {
-        if (j >= D / 2) return;
-        const int col = slot * D + j;
-        const float u = sum_parts(prow + col, a.ks, pstride), v = sum_parts(prow + col + D / 2, a.ks, pstride);
-        uint16_t* q = a.q16 + ((int64_t)b * a.nh + slot) * D;
-        q[j] = act_store(__fsub_rn(__fmul_rn(u, c), __fmul_rn(v, sn)), AF);
-        q[j + D / 2] = act_store(__fadd_rn(__fmul_rn(v, c), __fmul_rn(u, sn)), AF);
-        return;
-    }
-    const int kvh = slot - a.nh;
     const int kcol = a.nh * D + kvh * D, vcol = a.nh * D + a.nkv * D + kvh * D;
     float k0 = 0.f, k1 = 0.f, v0 = 0.f, v1 = 0.f;
     if (j < D / 2) {
+        const float c = a.cos_t[(int64_t)pos * (D / 2) + j], sn = a.sin_t[(int64_t)pos * (D / 2) + j];
         const float u = sum_parts(prow + kcol + j, a.ks, pstride);
         const float x = sum_parts(prow + kcol + j + D / 2, a.ks, pstride);
         k0 = __fsub_rn(__fmul_rn(u, c), __fmul_rn(x, sn));
@@ -138,6 +125,7 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
     constexpr int NK = DecChunk<D, KV8>::NK;
     __shared__ float mw[4][16], lw[4][16];
     __shared__ __attribute__((aligned(16))) float ow[4][16 * D];
+    __shared__ __attribute__((aligned(16))) uint16_t qs[16 * D];    // rotated queries of the group
 
     const int G = a.nh / a.nkv;
     const int kvh = blockIdx.y, b = blockIdx.z;
@@ -178,13 +166,33 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
         }
     };
 
+    // The workgroup whose range holds the new position appends its k and v first (one
+    // wave; the barrier below publishes the row to the other waves, and no other
+    // workgroup reads that position).  Every workgroup reduces and rotates the queries
+    // of its group into LDS, in the MFMA operand format.
+    const int pos = len - 1;
+    if (pos / (4 * kps) == (int)blockIdx.x && w == 0) append_kv<D, KV8>(a, b, kvh, pos, lane);
+    {
+        const int Nqkv = (a.nh + 2 * a.nkv) * D;
+        const int64_t pstride = (int64_t)a.batch * Nqkv;
+        const float* prow = a.qkv_part + (int64_t)b * Nqkv + (int64_t)kvh * G * D;
+        for (int i = tid; i < G * (D / 2); i += 256) {
+            const int c = i / (D / 2), j = i % (D / 2);
+            const float cs = a.cos_t[(int64_t)pos * (D / 2) + j], sn = a.sin_t[(int64_t)pos * (D / 2) + j];
+            const float u = sum_parts(prow + c * D + j, a.ks, pstride);
+            const float v = sum_parts(prow + c * D + j + D / 2, a.ks, pstride);
+            qs[c * D + j] = act_store(__fsub_rn(__fmul_rn(u, cs), __fmul_rn(v, sn)), AF);
+            qs[c * D + j + D / 2] = act_store(__fadd_rn(__fmul_rn(v, cs), __fmul_rn(u, sn)), AF);
+        }
+    }
+    __syncthreads();
+
     // query fragments: column c = head c of the group
     u32x4 qf[NJ];
-    const uint16_t* qrow = a.q16 + ((int64_t)b * a.nh + kvh * G + (r < G ? r : 0)) * D;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         qf[j] = u32x4{0u, 0u, 0u, 0u};
-        if (r < G) qf[j] = *(const u32x4*)(qrow + qdim<D, KV8>(j, g));
+        if (r < G) qf[j] = *(const u32x4*)(qs + r * D + qdim<D, KV8>(j, g));
     }
 
     f32x4 oacc[ND];
@@ -355,11 +363,8 @@ bool attn_decode_supported(int d, int group) { return (d == 64 || d == 128) && g
 
 template <int D, bool KV8>
 static hipError_t launch_dk(const AttnDecArgs& a, int B, int nsplit, hipStream_t st) {
-    FP_LAUNCH((qkv_rope_kernel<D, KV8>), dim3(a.nh + a.nkv, B), dim3(64), 0, st, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
     FP_LAUNCH((attn_decode_kernel<D, KV8>), dim3((nsplit + 3) / 4, a.nkv, B), dim3(256), 0, st, a, nsplit);
-    e = hipGetLastError();
+    hipError_t e = hipGetLastError();
     const int nsw = attn_decode_partials(nsplit);
     if (e != hipSuccess || nsw == 1 || a.skip_merge) return e;
     FP_LAUNCH(attn_merge_kernel<D>, dim3(a.nh, B), dim3(D), 0, st, a, nsw);
@@ -369,7 +374,7 @@ static hipError_t launch_dk(const AttnDecArgs& a, int B, int nsplit, hipStream_t
 hipError_t launch_attn_decode(const AttnDecArgs& a, int B, hipStream_t st) {
     const int G = a.nh / a.nkv;
     if (!attn_decode_supported(a.d, G) || a.nh % a.nkv != 0 || a.batch != B) return hipErrorInvalidValue;
-    if (a.keys_per_split <= 0 || a.keys_per_split % VT_BLK != 0 || a.q16 == nullptr) return hipErrorInvalidValue;
+    if (a.keys_per_split <= 0 || a.keys_per_split % VT_BLK != 0) return hipErrorInvalidValue;
     const int nsplit = (a.max_seq + a.keys_per_split - 1) / a.keys_per_split;
     if (a.d == 128) return a.kv_int8 ? launch_dk<128, true>(a, B, nsplit, st) : launch_dk<128, false>(a, B, nsplit, st);
     return a.kv_int8 ? launch_dk<64, true>(a, B, nsplit, st) : launch_dk<64, false>(a, B, nsplit, st);

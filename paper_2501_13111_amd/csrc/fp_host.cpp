@@ -556,7 +556,6 @@ AttnDecArgs attn_args(fp_layer* h, int l, int ks, int B, float* dump) {
     int nsplit;
     attn_decode_split(s.max_seq, B, s.n_kv_heads, s.n_heads / s.n_kv_heads, &nsplit, &ad.keys_per_split);
     ad.batch = B;
-    ad.q16 = (uint16_t*)h->q32;
     ad.ws = h->attn_ws;
     ad.out = h->act_o;
     ad.out_fmt = h->act_fmt;

@@ -141,7 +141,6 @@ struct AttnDecArgs {
     int keys_per_split;       // context keys per split (multiple of VT_BLK)
     int batch;                // B
     int skip_merge;           // leave split partials in ws (the consumer merges them)
-    uint16_t* q16;            // [B, nh, d] rotated queries in the MFMA operand format (workspace)
     float* ws;                // [B, nh, nsw, d + 4] workgroup partials when nsw > 1 (m at d, l at d + 1)
     uint16_t* out;            // [B, nh*d] activation format out_fmt
     int out_fmt;
