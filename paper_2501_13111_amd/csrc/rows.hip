@@ -300,7 +300,8 @@ hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, fl
 hipError_t launch_resid_norm(const float* part, int ks, int M, int N, const uint16_t* resid,
                              uint16_t* out, const uint16_t* g, float eps, uint16_t* nout, int nfmt,
                              float* ssq, int* inc_pos, hipStream_t st) {
-    if ((g != nullptr || ks > 0) && M > 1 && N % 8 == 0 && N <= 2 * RN_T * 8) {
+    // the row kernel: with a norm, or a residual alone over enough rows to fill the GPU
+    if ((g != nullptr || (ks > 0 && M >= 256)) && M > 1 && N % 8 == 0 && N <= 2 * RN_T * 8) {
         FP_LAUNCH(resid_norm_row_kernel, dim3(M), dim3(RN_T), 0, st, part, ks, M, N, resid, out, g, eps, nout, nfmt,
                   inc_pos);
         return hipGetLastError();
