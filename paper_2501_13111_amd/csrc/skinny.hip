@@ -293,8 +293,7 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 // chunks ahead and written to one of two LDS buffers one chunk ahead (rows of 256 B,
 // 16-byte pieces XOR-swizzled by the row so MFMA fragment reads are free of bank
 // conflicts); weight fragments (and int4 scale / zero words) run PD chunks ahead in
-// registers (PD = SB_PD for quantised weights, 2 for bf16, whose chunks hold four
-// K-steps of weights).  The workgroup synchronises with a bare s_barrier after the LDS
+// registers.  The workgroup synchronises with a bare s_barrier after the LDS
 // writes, so the global loads in flight are not drained at every chunk.  The
 // split-K factor only has to fill the GPU.
 constexpr int SB_KC = 128;              // k per activation chunk
@@ -313,7 +312,10 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
     constexpr int SPC = SB_KC / KS;                  // K-steps per chunk
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
     constexpr int ABUF = 16 * MT * 256;              // bytes of one activation chunk
-    constexpr int PD = WF == W_BF16 ? 2 : SB_PD;     // bf16 chunks hold four K-steps of weights
+    // chunks of loads in flight: four for int8; two for int4 (measured faster: its chunks
+    // are half the bytes and its unpacking keeps the waves busy) and bf16 (four K-steps
+    // of weights per chunk)
+    constexpr int PD = WF == W_INT8 ? SB_PD : 2;
     __shared__ __attribute__((aligned(1024))) char As[2 * ABUF];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
