@@ -296,7 +296,10 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 // registers.  The workgroup synchronises with a bare s_barrier after the LDS
 // writes, so the global loads in flight are not drained at every chunk.  The
 // split-K factor only has to fill the GPU.
-constexpr int SB_KC = 128;              // k per activation chunk
+constexpr int SB_KC = 128;              // k per activation chunk (one int4 group)
+#ifndef SKINNY_I4_POST
+#define SKINNY_I4_POST 1                // int4: scale the group sums instead of the weights
+#endif
 #ifndef SKINNY_BATCH_PD
 #define SKINNY_BATCH_PD 4
 #endif
@@ -404,6 +407,7 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
     // (for the first MT MFMAs) one LDS read, in turn, so the matrix pipe, the vector
     // ALU and LDS overlap within a wave.
     constexpr int NSUB = SB_KC / 32;
+    constexpr bool I4_POST = WF == W_INT4 && SKINNY_I4_POST;
     auto a_frag = [&](const char* Ab, int m, int t) {
         int koff;
         if constexpr (WF == W_BF16) koff = 32 * m + 8 * g;
@@ -429,14 +433,18 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
             const u32x4 w = wv[0][s];
             const uint32_t d = m == 0 ? w.x : m == 1 ? w.y : m == 2 ? w.z : w.w;
             const u32x4 q = i4x8_to_f16x8(d, bias);
+            if constexpr (I4_POST) return q;             // exact q - z; the group scale is applied to the sums
             return u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
         }
     };
-    constexpr int VALU_PER_B = WF == W_BF16 ? 0 : (WF == W_INT8 ? 10 : 16);   // per B operand
+    constexpr int VALU_PER_B = WF == W_BF16 ? 0 : (WF == W_INT8 ? 10 : (I4_POST ? 12 : 16));   // per B operand
     constexpr int NMF = MT * NS;                                              // MFMAs per sub-step
     constexpr int VPS = (VALU_PER_B * NS + NMF - 1) / NMF;                     // VALU per MFMA slot
     auto compute = [&](const char* Ab, const u32x4 (*wv)[NS], const uint32_t* sz) {
         u32x4 av[2][MT], bq[2][NS];
+        // int4 with I4_POST: a chunk is one 128-input group, summed over exact q - z into
+        // fresh accumulators and scaled once per group in fp32
+        f32x4 grp[I4_POST ? MT : 1][I4_POST ? NS : 1];
 #pragma unroll
         for (int t = 0; t < MT; ++t) av[0][t] = a_frag(Ab, 0, t);
 #pragma unroll
@@ -454,7 +462,12 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
 #pragma unroll
             for (int t = 0; t < MT; ++t)
 #pragma unroll
-                for (int s = 0; s < NS; ++s) acc[t][s] = mfma16<AF>(av[c][t], bq[c][s], acc[t][s]);
+                for (int s = 0; s < NS; ++s) {
+                    if constexpr (I4_POST)
+                        grp[t][s] = mfma16<AF>(av[c][t], bq[c][s], m == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : grp[t][s]);
+                    else
+                        acc[t][s] = mfma16<AF>(av[c][t], bq[c][s], acc[t][s]);
+                }
             if (m + 1 < NSUB) {
 #pragma unroll
                 for (int i = 0; i < NMF; ++i) {
@@ -464,6 +477,14 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
+        }
+        if constexpr (I4_POST) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const float sc = h2f((uint16_t)(sz[s] & 0xFFFFu));
+#pragma unroll
+                for (int t = 0; t < MT; ++t) acc[t][s] += grp[t][s] * sc;
+            }
         }
     };
     // LDS writes done, then a bare barrier (no drain of the global loads in flight)
