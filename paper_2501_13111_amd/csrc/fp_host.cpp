@@ -71,6 +71,9 @@ constexpr int KSMAX = 64;         // max split-K factor of the decode projection
 #define FP_TARGET_WG 512
 #endif
 constexpr int TARGET_WG = FP_TARGET_WG;   // decode workgroups per projection the split-K aims for
+#ifndef SPLIT_WIDE_N
+#define SPLIT_WIDE_N 8192
+#endif
 
 struct Mat {
     void* codes = nullptr;        // fragment-major tiles of bf16 / int8 / int4 (device nibble order)
@@ -268,10 +271,10 @@ fp_status synth_rows(fp_layer* h, Mat* m, int row0, int n, int layer, int tensor
 
 // Split-K factor and k-range for a decode projection: aim for TARGET_WG workgroups,
 // within the LDS bound on the staged activation slice.
-void choose_split(int tiles, int K, int M, int wf, int* ks, int* krange) {
+void choose_split(int tiles, int K, int M, int wf, int target, int* ks, int* krange) {
     const int KS = skinny_kstep(wf);
     const int nsteps = (K + KS - 1) / KS;
-    int k = (TARGET_WG + tiles - 1) / tiles;
+    int k = (target + tiles - 1) / tiles;
     int kmax = nsteps / 4;             // keep at least four K-steps per workgroup
     if (kmax < 1) kmax = 1;
     if (k > kmax) k = kmax;
@@ -319,7 +322,10 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     a.head_dim = h->s.head_dim;
     a.d_pos = h->d_pos;
     int ks, kr;
-    choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, h->wq, &ks, &kr);
+    // wide matrices (qkv, gate/up) stream faster with twice the workgroups
+    const int ncols = dual_F > 0 ? 2 * dual_F : m.N;
+    choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, h->wq, ncols >= SPLIT_WIDE_N ? 2 * TARGET_WG : TARGET_WG, &ks,
+                 &kr);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     a.krange = kr;
     HIPCHK(launch_skinny(a, h->wq, ks, st));
