@@ -1,5 +1,6 @@
 // Decode projections: weight-streaming skinny GEMM  part[s] = A[M, K] . W[N, K]^T
-// over the split-K range s, for M <= 64 tokens (one per sequence in the batch).
+// over the split-K range s, M tokens (one per sequence): skinny_kernel for a single
+// sequence (M <= 16), skinny_batch_kernel for batches (M <= 64).
 //
 // Decode is where the fingerprint's per-token time goes (TPOT, paper Sec. 5.3):
 // every step streams all weights once, so the kernel is bound by HBM bandwidth.
@@ -619,17 +620,14 @@ static hipError_t launch3(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
 
 // subtiles per wave: batches stream more rows per workgroup so the staged activation
 // slice is shared by more weights
-static int skinny_ns(int M) { return M > 16 ? 4 : SKINNY_NS; }
+// One 16-token tile: the schedule runs this kernel for a single sequence only (batches
+// use skinny_batch_kernel).
+static int skinny_ns(int M) { return (void)M, SKINNY_NS; }
 
 template <int WF>
 static hipError_t launch2(const SkinnyArgs& a, dim3 grid, hipStream_t st) {
-    switch ((a.M + 15) / 16) {
-        case 1: return launch3<WF, 1, SKINNY_NS>(a, grid, st);
-        case 2: return launch3<WF, 2, 4>(a, grid, st);
-        case 3: return launch3<WF, 3, 4>(a, grid, st);
-        case 4: return launch3<WF, 4, 4>(a, grid, st);
-        default: return hipErrorInvalidValue;
-    }
+    if (a.M < 1 || a.M > 16) return hipErrorInvalidValue;
+    return launch3<WF, 1, SKINNY_NS>(a, grid, st);
 }
 
 int skinny_kstep(int wf) { return weight_kstep(wf); }
