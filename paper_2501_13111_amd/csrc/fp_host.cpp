@@ -359,7 +359,7 @@ fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, 
     const int KC = skinny_batch_chunk();
     const int nch = (m.K + KC - 1) / KC;
     const int tiles = skinny_batch_tiles(m.N, dual_F, h->wq);
-    const int rows = skinny_batch_rows(h->wq);
+    const int rows = skinny_batch_rows(m.N, dual_F, h->wq);
     const double bpw = h->wq == FP_WQ_BF16 ? 2.0 : (h->wq == FP_WQ_INT8_CHANNEL ? 1.0 : 0.5);
     const double chunk_s = rows * KC * bpw / 25e9;
     const double split_s = (double)M * (dual_F > 0 ? 2.0 * dual_F : m.N) * 8.0 / 5e12;

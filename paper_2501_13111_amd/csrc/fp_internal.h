@@ -194,7 +194,7 @@ int skinny_tiles(int N, int dual_F, int M);
 hipError_t launch_skinny(const SkinnyArgs& a, int wf, int ks, hipStream_t st);
 // Batched decode projections (XF_COPY, M <= 64): k-range walked in staged chunks of
 // skinny_batch_chunk() values; krange a multiple of it, ks * krange >= K.
-int skinny_batch_rows(int wf);   // weight rows per workgroup
+int skinny_batch_rows(int N, int dual_F, int wf);   // weight rows per workgroup
 int skinny_batch_tiles(int N, int dual_F, int wf);
 int skinny_batch_chunk();
 hipError_t launch_skinny_batch(const SkinnyArgs& a, int wf, int ks, hipStream_t st);

@@ -336,9 +336,10 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
     for (int s = 0; s < NS; ++s) {
         if (a.dual_F > 0) {
             const int fw = blockIdx.x * (NWV * 8 * NS) + w * (8 * NS);
-            const int f = fw + 16 * (s % (NS / 2)) + r;
+            constexpr int HS = NS / 2 > 0 ? NS / 2 : 1;   // dual tiling needs NS even (the launcher ensures it)
+            const int f = fw + 16 * (s % HS) + r;
             rv[s] = f < a.dual_F;
-            row[s] = (s < NS / 2 ? 0 : a.dual_F) + min(f, a.dual_F - 1);
+            row[s] = (s < HS ? 0 : a.dual_F) + min(f, a.dual_F - 1);
         } else {
             const int n = blockIdx.x * (NWV * 16 * NS) + w * (16 * NS) + 16 * s + r;
             rv[s] = n < a.N;
@@ -547,35 +548,55 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
 struct BatchTiling {
     int nwv, ns;
 };
-constexpr BatchTiling batch_tiling(int wf) { return wf == W_BF16 ? BatchTiling{4, 2} : BatchTiling{8, 2}; }
+// Narrow matrices (fewer than SB_NARROW_TILES workgroups of the regular tiling; not
+// the [gate; up] matrix) take one subtile per wave: twice the workgroups, half the
+// split-K factor, half the partial sums for the consumer to read.
+#ifndef SB_NARROW_TILES
+#define SB_NARROW_TILES 40
+#endif
+constexpr BatchTiling batch_tiling(int wf, bool narrow) {
+    return wf == W_BF16 ? BatchTiling{4, 2} : (narrow ? BatchTiling{8, 1} : BatchTiling{8, 2});
+}
+static bool batch_narrow(int N, int dual_F, int wf) {
+    const BatchTiling T = batch_tiling(wf, false);
+    return wf != W_BF16 && dual_F == 0 && (N + T.nwv * 16 * T.ns - 1) / (T.nwv * 16 * T.ns) < SB_NARROW_TILES;
+}
 
-template <int WF, int MT>
+template <int WF, int MT, bool NARROW>
 static hipError_t launch_batch(const SkinnyArgs& a, int ks, hipStream_t st) {
-    constexpr BatchTiling T = batch_tiling(WF);
-    static_assert(T.ns % 2 == 0 && T.nwv * 64 <= 1024, "tiling");
+    constexpr BatchTiling T = batch_tiling(WF, NARROW);
+    static_assert((NARROW || T.ns % 2 == 0) && T.nwv * 64 <= 1024, "tiling");
     dim3 grid(skinny_batch_tiles(a.N, a.dual_F, WF), ks);
     FP_LAUNCH((skinny_batch_kernel<WF, MT, T.ns, T.nwv>), grid, dim3(64 * T.nwv), 0, st, a);
     return hipGetLastError();
 }
 
+template <int WF, int MT>
+static hipError_t launch_batch_n(const SkinnyArgs& a, int ks, hipStream_t st) {
+    if constexpr (WF != W_BF16) {
+        if (batch_narrow(a.N, a.dual_F, WF)) return launch_batch<WF, MT, true>(a, ks, st);
+    }
+    return launch_batch<WF, MT, false>(a, ks, st);
+}
+
 template <int WF>
 static hipError_t launch_batch_w(const SkinnyArgs& a, int ks, hipStream_t st) {
     switch ((a.M + 15) / 16) {
-        case 1: return launch_batch<WF, 1>(a, ks, st);
-        case 2: return launch_batch<WF, 2>(a, ks, st);
-        case 3: return launch_batch<WF, 3>(a, ks, st);
-        case 4: return launch_batch<WF, 4>(a, ks, st);
+        case 1: return launch_batch_n<WF, 1>(a, ks, st);
+        case 2: return launch_batch_n<WF, 2>(a, ks, st);
+        case 3: return launch_batch_n<WF, 3>(a, ks, st);
+        case 4: return launch_batch_n<WF, 4>(a, ks, st);
         default: return hipErrorInvalidValue;
     }
 }
 
-int skinny_batch_rows(int wf) {
-    const BatchTiling T = batch_tiling(wf);
+int skinny_batch_rows(int N, int dual_F, int wf) {
+    const BatchTiling T = batch_tiling(wf, batch_narrow(N, dual_F, wf));
     return T.nwv * 16 * T.ns;
 }
 
 int skinny_batch_tiles(int N, int dual_F, int wf) {
-    const int rows = skinny_batch_rows(wf);
+    const int rows = skinny_batch_rows(N, dual_F, wf);
     return dual_F > 0 ? (dual_F + rows / 2 - 1) / (rows / 2) : (N + rows - 1) / rows;
 }
 
