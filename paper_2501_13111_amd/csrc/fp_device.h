@@ -194,6 +194,22 @@ __device__ __forceinline__ u32x4 buf_load_nt(__amdgpu_buffer_rsrc_t r, uint32_t 
 }
 constexpr uint32_t BUF_OOB = 0xFFFFFFF0u;   // an offset past the end of every resource
 
+// off if live, else BUF_OOB.  The mask passes through an empty asm statement, so the
+// compiler cannot turn the choice into a branch around the load: on a uniform
+// condition it otherwise does, and the wait counts it inserts at the join drain every
+// load in flight.
+__device__ __forceinline__ uint32_t off_or_oob(bool live, uint32_t off) {
+    uint32_t m = live ? 0u : 0xFFFFFFFFu;
+    asm volatile("" : "+v"(m));
+    return off + ((BUF_OOB - off) & m);
+}
+// the same for a condition that is uniform across the wave (the mask stays scalar)
+__device__ __forceinline__ uint32_t off_or_oob_uniform(bool live, uint32_t off) {
+    uint32_t m = __builtin_amdgcn_readfirstlane(live ? 0u : 0xFFFFFFFFu);
+    asm volatile("" : "+s"(m));
+    return off + ((BUF_OOB - off) & m);
+}
+
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
 
 }  // namespace fpk

@@ -303,6 +303,7 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     a.W = m.codes;
     a.scales = m.scales;
     a.zeros = m.zeros;
+    a.sz = m.sz;
     a.M = M;
     a.N = m.N;
     a.K = m.K;

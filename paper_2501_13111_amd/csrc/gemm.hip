@@ -333,7 +333,7 @@ hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st)
 // Large prefill GEMMs: 256 x 256 tiles, 8 waves of 128 x 64 (4 x 2 32x32 MFMA tiles),
 // operands copied global -> LDS by buffer loads that write LDS directly (16 B per
 // lane), two LDS stages; the next stage's copies are issued in parts between the
-// current stage's MFMA steps.  A rows are stored with an XOR swizzle of their 16-byte
+// MFMA steps of the first half of the current stage.  A rows are stored with an XOR swizzle of their 16-byte
 // chunks so that MFMA fragment reads are free of bank conflicts; weight blocks
 // keep their fragment-major order, so a fragment is one contiguous 1 KiB read.
 // Quantised weights stay packed in LDS and are converted to fp16 per fragment.
@@ -477,13 +477,17 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
 
     const int l32 = lane & 31, h32 = lane >> 5;
     // multiply stage `stage` out of LDS; with nk0 >= 0, issue the copies of the stage at
-    // k offset nk0 into the other buffer, one part per 16-k step
+    // k offset nk0 into the other buffer, two parts per 16-k step over the first half of
+    // the steps (the second half covers their latency before the stage's closing wait)
     auto compute = [&](int stage, int nk0) {
         const char* sA = smem + stage * T::STAGE;
         const char* sB = sA + T::A_BYTES;
 #pragma unroll
         for (int kk = 0; kk < T::TK / 16; ++kk) {            // 16-k MFMA steps
-            if (nk0 >= 0) issue_part(stage ^ 1, nk0, kk);
+            if (nk0 >= 0 && kk < T::TK / 32) {
+                issue_part(stage ^ 1, nk0, 2 * kk);
+                issue_part(stage ^ 1, nk0, 2 * kk + 1);
+            }
             const int s = kk >> 1, hh = kk & 1;              // 32-k sub-step, half
             u32x4 af[4], bop[2];
             const int chunk = 2 * kk + h32;                  // 16-byte chunk of the A row

@@ -86,23 +86,30 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
         }
     }
 
-    // ---- weight loads of one K-step: one 1 KiB block per wave (16 rows x one K-step).
+    // ---- weight loads of one K-step: one 1 KiB block per wave (16 rows x one K-step),
+    // and for int4 the row's scale | zero << 16 word of the step's 128-input group.
     // Rows past the matrix and steps past the k-range read past the end of the buffer
-    // resource (zeros, no memory access), so every load is issued unconditionally and
+    // resources (zeros, no memory access), so every load is issued unconditionally and
     // the compiler's wait counts stay exact.
     const int nrows = a.dual_F > 0 ? 2 * a.dual_F : a.N;
+    const int ngr = a.K / 128;
     const __amdgpu_buffer_rsrc_t wres = buf_rsrc(a.W, (uint32_t)((nrows / 16) * a.kst * 1024));
-    auto load_w = [&](int kk, u32x4* dst) {
+    const __amdgpu_buffer_rsrc_t szres = buf_rsrc(a.sz, WF == W_INT4 ? (uint32_t)(nrows * ngr * 4) : 0u);
+    auto load_w = [&](int kk, u32x4* dst, uint32_t* szd) {
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
             const uint32_t blk = (uint32_t)((row[s] >> 4) * a.kst + kk / KS);
-            dst[s] = buf_load_nt(wres, (rv[s] && kk < ke) ? (blk * 64 + lane) * 16 : BUF_OOB);
+            dst[s] = buf_load_nt(wres, off_or_oob(rv[s] && kk < ke, (blk * 64 + lane) * 16));
+            if constexpr (WF == W_INT4)
+                szd[s] = __builtin_amdgcn_raw_buffer_load_b32(
+                    szres, off_or_oob(rv[s] && kk < ke, (uint32_t)(row[s] * ngr + kk / 128) * 4u), 0, 0);
         }
     };
 
     u32x4 wa[UNR][NS], wb[UNR][NS];
+    uint32_t sza[UNR][NS], szb[UNR][NS];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) load_w(kb + u * KS, wa[u]);
+    for (int u = 0; u < UNR; ++u) load_w(kb + u * KS, wa[u], sza[u]);
 
     // ---- stage the activation slice (with its transform) into LDS
     if constexpr (XF == XF_NORM) {
@@ -208,7 +215,7 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) mv[t] = (16 * t + r) < a.M;
 
-    auto compute = [&](int kk, const u32x4* wv) {
+    auto compute = [&](int kk, const u32x4* wv, const uint32_t* sz) {
         if (kk >= ke) return;
         const bool kin = kk + KL * g < ke;
         u32x4 bop[NJ][NS];
@@ -222,12 +229,7 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
                 bop[0][s] = u32x4{c0.x, c0.y, c1.x, c1.y};
                 bop[1][s] = u32x4{c2.x, c2.y, c3.x, c3.y};
             } else {
-                const int grp = kk / 128;
-                float sc = 0.f, zz = 0.f;
-                if (rv[s]) {
-                    sc = h2f(a.scales[(int64_t)row[s] * (a.K / 128) + grp]);
-                    zz = h2f(a.zeros[(int64_t)row[s] * (a.K / 128) + grp]);
-                }
+                const float sc = h2f((uint16_t)(sz[s] & 0xFFFFu)), zz = h2f((uint16_t)(sz[s] >> 16));
                 const _Float16 bz = (_Float16)(1024.0f + zz);
                 const f16x2 bias = {bz, bz};
                 const _Float16 sh = (_Float16)sc;
@@ -258,13 +260,13 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 
     for (int base = kb; base < ke; base += 2 * UNR * KS) {
 #pragma unroll
-        for (int u = 0; u < UNR; ++u) load_w(base + (UNR + u) * KS, wb[u]);
+        for (int u = 0; u < UNR; ++u) load_w(base + (UNR + u) * KS, wb[u], szb[u]);
 #pragma unroll
-        for (int u = 0; u < UNR; ++u) compute(base + u * KS, wa[u]);
+        for (int u = 0; u < UNR; ++u) compute(base + u * KS, wa[u], sza[u]);
 #pragma unroll
-        for (int u = 0; u < UNR; ++u) load_w(base + (2 * UNR + u) * KS, wa[u]);
+        for (int u = 0; u < UNR; ++u) load_w(base + (2 * UNR + u) * KS, wa[u], sza[u]);
 #pragma unroll
-        for (int u = 0; u < UNR; ++u) compute(base + (UNR + u) * KS, wb[u]);
+        for (int u = 0; u < UNR; ++u) compute(base + (UNR + u) * KS, wb[u], szb[u]);
     }
 
     // ---- partial sums of this split
@@ -389,7 +391,7 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 const uint32_t blk = (uint32_t)((row[s] >> 4) * a.kst + min(st0 + u, a.kst - 1));
-                wv[u][s] = buf_load_nt(wres, ci < nch ? (blk * 64 + lane) * 16 : BUF_OOB);
+                wv[u][s] = buf_load_nt(wres, off_or_oob_uniform(ci < nch, (blk * 64 + lane) * 16));
             }
         if constexpr (WF == W_INT4) {
 #pragma unroll
