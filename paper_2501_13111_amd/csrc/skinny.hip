@@ -309,8 +309,14 @@ constexpr int SB_KC = 128;              // k per activation chunk (one int4 grou
 constexpr int SB_PD = SKINNY_BATCH_PD;  // chunks of loads in flight (even: the LDS buffer is the chunk's parity)
 static_assert(SB_PD >= 2 && SB_PD % 2 == 0, "load depth");
 
-template <int WF, int MT, int NS, int NWV>
+// M32: 32x32x16 MFMA (batches of 17 to 64: MT = 2 or 4 sixteen-row tiles of the
+// activation chunk).  Each wave's two 16-row weight blocks form one 32-column tile; lane
+// l takes the weight row (l % 32) and, of its block's fragment pieces, the two whose
+// k-groups are (l / 32) and (l / 32) + 2.  The k order inside an MFMA only has to agree
+// between the two operands, so the activation fragments follow the pieces' k.
+template <int WF, int MT, int NS, int NWV, bool M32>
 __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a) {
+    static_assert(!M32 || (NS == 2 && MT % 2 == 0), "32-row tiles: two blocks per wave, whole 32-row activation tiles");
     constexpr int NT = 64 * NWV;                     // threads
     constexpr int NPA = (256 * MT + NT - 1) / NT;    // activation pieces per thread
     constexpr int KS = SkinnyTraits<WF>::KS;
@@ -349,6 +355,9 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
         }
     }
 
+    const int h32 = lane >> 5, bsel = (lane & 31) >> 4;   // M32: k half, block of the lane's row
+    const int myrow = row[bsel & (NS - 1)];
+    const bool myrv = rv[bsel & (NS - 1)];
     // activation chunk ci: thread piece c = tid + NT i is row c / 16, LDS slot c % 16,
     // which holds the row's 16-byte piece slot ^ (row % 16)
     // Loads are unconditional (clamped addresses): rows past M only feed output rows
@@ -390,12 +399,22 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
         for (int u = 0; u < SPC; ++u)
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-                const uint32_t blk = (uint32_t)((row[s] >> 4) * a.kst + min(st0 + u, a.kst - 1));
-                wv[u][s] = buf_load_nt(wres, off_or_oob_uniform(ci < nch, (blk * 64 + lane) * 16));
+                if constexpr (M32) {
+                    // piece (r, group h32 + 2 s) of the block holding the lane's row
+                    const uint32_t blk = (uint32_t)((myrow >> 4) * a.kst + min(st0 + u, a.kst - 1));
+                    wv[u][s] = buf_load_nt(wres, off_or_oob_uniform(ci < nch, (blk * 64 + r + 16 * (h32 + 2 * s)) * 16));
+                } else {
+                    const uint32_t blk = (uint32_t)((row[s] >> 4) * a.kst + min(st0 + u, a.kst - 1));
+                    wv[u][s] = buf_load_nt(wres, off_or_oob_uniform(ci < nch, (blk * 64 + lane) * 16));
+                }
             }
         if constexpr (WF == W_INT4) {
+            if constexpr (M32) {
+                sz[0] = a.sz[(int64_t)myrow * (a.K / 128) + st0];
+            } else {
 #pragma unroll
-            for (int s = 0; s < NS; ++s) sz[s] = a.sz[(int64_t)row[s] * (a.K / 128) + st0];
+                for (int s = 0; s < NS; ++s) sz[s] = a.sz[(int64_t)row[s] * (a.K / 128) + st0];
+            }
         }
     };
 
@@ -491,6 +510,81 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
             }
         }
     };
+    // M32: eight 16-k MFMA steps per chunk.  Step j of the lane's data (h = l / 32):
+    // bf16 K-step j / 2, piece j % 2, k 16 j + 8 h; int8 K-step j / 4, piece (j / 2) % 2,
+    // half j % 2, k 64 (j / 4) + 32 ((j / 2) % 2) + 16 h + 8 (j % 2); int4 piece j / 4,
+    // dword j % 4, k 64 (j / 4) + 32 h + 8 (j % 4).
+    constexpr int MT32 = MT / 2;
+    f32x16 acc32[M32 ? MT32 : 1];
+#pragma unroll
+    for (int t = 0; t < (M32 ? MT32 : 1); ++t) acc32[t] = f32x16{};
+    auto a_frag32 = [&](const char* Ab, int j, int t) {
+        int koff;
+        if constexpr (WF == W_BF16) koff = 16 * j + 8 * h32;
+        else if constexpr (WF == W_INT8) koff = 64 * (j >> 2) + 32 * ((j >> 1) & 1) + 16 * h32 + 8 * (j & 1);
+        else koff = 64 * (j >> 2) + 32 * h32 + 8 * (j & 3);
+        const int piece = koff >> 3;
+        const int rr = 32 * t + (lane & 31);
+        return *(const u32x4*)(Ab + rr * 256 + ((piece ^ (rr & 15)) << 4));
+    };
+    auto b_op32 = [&](const u32x4 (*wv)[NS], const uint32_t* sz, int j) {
+        if constexpr (WF == W_BF16) {
+            return wv[j >> 1][(j & 1) & (NS - 1)];
+        } else if constexpr (WF == W_INT8) {
+            const u32x4 w = wv[j >> 2][((j >> 1) & 1) & (NS - 1)];
+            const uint32_t d0 = (j & 1) ? w.z : w.x, d1 = (j & 1) ? w.w : w.y;
+            const u32x2 c0 = i8x4_to_f16x4(d0), c1 = i8x4_to_f16x4(d1);
+            return u32x4{c0.x, c0.y, c1.x, c1.y};
+        } else {
+            const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(sz[0] >> 16)));
+            const f16x2 bias = {bz, bz};
+            const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(sz[0] & 0xFFFFu));
+            const f16x2 s2 = {sh, sh};
+            const u32x4 w = wv[0][(j >> 2) & (NS - 1)];
+            const int dd = j & 3;
+            const uint32_t d = dd == 0 ? w.x : dd == 1 ? w.y : dd == 2 ? w.z : w.w;
+            const u32x4 q = i4x8_to_f16x8(d, bias);
+            if constexpr (I4_POST) return q;
+            return u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
+        }
+    };
+    constexpr int VPS32 = M32 ? (VALU_PER_B + MT32 - 1) / (MT32 > 0 ? MT32 : 1) : 0;   // VALU per MFMA slot
+    auto compute32 = [&](const char* Ab, const u32x4 (*wv)[NS], const uint32_t* sz) {
+        u32x4 av[2][MT32 > 0 ? MT32 : 1], bq[2];
+        f32x16 grp[I4_POST && MT32 > 0 ? MT32 : 1];
+#pragma unroll
+        for (int t = 0; t < MT32; ++t) av[0][t] = a_frag32(Ab, 0, t);
+        bq[0] = b_op32(wv, sz, 0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int c = j & 1, n = c ^ 1;
+            __builtin_amdgcn_sched_barrier(0);
+            if (j + 1 < 8) {
+#pragma unroll
+                for (int t = 0; t < MT32; ++t) av[n][t] = a_frag32(Ab, j + 1, t);
+                bq[n] = b_op32(wv, sz, j + 1);
+            }
+#pragma unroll
+            for (int t = 0; t < MT32; ++t) {
+                if constexpr (I4_POST) grp[t] = mfma32<AF>(av[c][t], bq[c], j == 0 ? f32x16{} : grp[t]);
+                else acc32[t] = mfma32<AF>(av[c][t], bq[c], acc32[t]);
+            }
+            if (j + 1 < 8) {
+#pragma unroll
+                for (int i = 0; i < MT32; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // one LDS read
+                    if (VPS32 > 0) __builtin_amdgcn_sched_group_barrier(0x002, VPS32, 0);   // unpacking
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if constexpr (I4_POST) {
+            const float sc = h2f((uint16_t)(sz[0] & 0xFFFFu));
+#pragma unroll
+            for (int t = 0; t < MT32; ++t) acc32[t] += grp[t] * sc;
+        }
+    };
     // LDS writes done, then a bare barrier (no drain of the global loads in flight)
     auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
@@ -509,7 +603,8 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
     // ci + PD, move chunk ci + 1 into the other LDS buffer (whose last reader was
     // chunk ci - 1: every wave has passed the barrier since) and refill its ring slot
     auto step = [&](int ci, int p) {
-        compute(As + (p & 1) * ABUF, wr[p], szr[p]);
+        if constexpr (M32) compute32(As + (p & 1) * ABUF, wr[p], szr[p]);
+        else compute(As + (p & 1) * ABUF, wr[p], szr[p]);
         load_w(ci + PD, wr[p], szr[p]);
         const int q = (p + 1) % PD;
         store_a(As + ((p + 1) & 1) * ABUF, ra[q], ci + 1);
@@ -529,18 +624,34 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
 
     const int ncols = a.dual_F > 0 ? 2 * a.dual_F : a.N;
     float* out = a.part + (int64_t)blockIdx.y * a.M * ncols;
+    if constexpr (M32) {
+        // accumulator element e of lane l: activation row 8 (e / 4) + 4 (l / 32) + e % 4,
+        // weight row of column l % 32
+        if (myrv) {
+            float rs = 1.f;
+            if constexpr (WF == W_INT8) rs = h2f(a.scales[myrow]);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        if (!rv[s]) continue;
-        float rs = 1.f;
-        if constexpr (WF == W_INT8) rs = h2f(a.scales[row[s]]);
+            for (int t = 0; t < MT32; ++t)
 #pragma unroll
-        for (int t = 0; t < MT; ++t)
+                for (int e = 0; e < 16; ++e) {
+                    const int m = 32 * t + 8 * (e >> 2) + 4 * h32 + (e & 3);
+                    if (m < a.M) out[(int64_t)m * ncols + myrow] = acc32[t][e] * rs;
+                }
+        }
+    } else {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int m = 16 * t + 4 * g + i;
-                if (m < a.M) out[(int64_t)m * ncols + row[s]] = acc[t][s][i] * rs;
-            }
+        for (int s = 0; s < NS; ++s) {
+            if (!rv[s]) continue;
+            float rs = 1.f;
+            if constexpr (WF == W_INT8) rs = h2f(a.scales[row[s]]);
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int m = 16 * t + 4 * g + i;
+                    if (m < a.M) out[(int64_t)m * ncols + row[s]] = acc[t][s][i] * rs;
+                }
+        }
     }
 }
 
@@ -564,12 +675,18 @@ static bool batch_narrow(int N, int dual_F, int wf) {
     return wf != W_BF16 && dual_F == 0 && (N + T.nwv * 16 * T.ns - 1) / (T.nwv * 16 * T.ns) < SB_NARROW_TILES;
 }
 
+#ifndef SB_M32
+#define SB_M32 1
+#endif
 template <int WF, int MT, bool NARROW>
 static hipError_t launch_batch(const SkinnyArgs& a, int ks, hipStream_t st) {
     constexpr BatchTiling T = batch_tiling(WF, NARROW);
     static_assert((NARROW || T.ns % 2 == 0) && T.nwv * 64 <= 1024, "tiling");
+    // batches above 16 on two-block waves: 32x32x16 MFMA over whole 32-row activation tiles
+    constexpr bool M32 = SB_M32 && !NARROW && MT >= 2;
+    constexpr int MTL = M32 ? (MT + 1) / 2 * 2 : MT;
     dim3 grid(skinny_batch_tiles(a.N, a.dual_F, WF), ks);
-    FP_LAUNCH((skinny_batch_kernel<WF, MT, T.ns, T.nwv>), grid, dim3(64 * T.nwv), 0, st, a);
+    FP_LAUNCH((skinny_batch_kernel<WF, MTL, T.ns, T.nwv, M32>), grid, dim3(64 * T.nwv), 0, st, a);
     return hipGetLastError();
 }
 

@@ -93,6 +93,10 @@ CASES = [
     ("batch40-int8", Shape(1, 256, 2, 2, 128, 384, 40, 20, 23), "int8", "int8", 40, 20, 3),
     ("batch64-int4", Shape(1, 256, 2, 2, 128, 384, 64, 9, 12), "int4", "bf16", 64, 9, 3),
     ("long-ctx-bf16", Shape(1, 256, 2, 2, 128, 384, 2, 520, 530), "bf16", "bf16", 2, 520, 3),
+    # batches of 17 to 64 on two-block waves take 32x32x16 MFMA tiles: bf16 weights, and
+    # int8 with a wide qkv (42 tiles of 256 rows) over a ragged 64-row activation tile
+    ("batch24-bf16", Shape(1, 256, 2, 2, 128, 384, 24, 12, 15), "bf16", "bf16", 24, 12, 3),
+    ("batch33-int8-wide", Shape(1, 3584, 28, 28, 128, 512, 33, 8, 11), "int8", "int8", 33, 8, 3),
     # prefill GEMMs with too few 256 x 256 tiles run split-K with reduction kernels
     # (M >= 256; M = 300 leaves a ragged row tile)
     ("splitk-bf16", Shape(2, 512, 4, 4, 128, 1024, 2, 160, 164), "bf16", "bf16", 2, 160, 2),
