@@ -96,6 +96,12 @@ CASES = [
     # batches of 17 to 64 on two-block waves take 32x32x16 MFMA tiles: bf16 weights, and
     # int8 with a wide qkv (42 tiles of 256 rows) over a ragged 64-row activation tile
     ("batch24-bf16", Shape(1, 256, 2, 2, 128, 384, 24, 12, 15), "bf16", "bf16", 24, 12, 3),
+    # one sequence takes the single-sequence projections: int4 (its scale | zero words ride
+    # with the weight loads) under GQA 4:1 with an int8 cache, and at head_dim 64
+    ("single-int4-gqa4-int8kv", Shape(2, 1024, 8, 2, 128, 1408, 1, 70, 76), "int4", "int8", 1, 70, 4),
+    ("single-int4-d64", Shape(1, 512, 8, 8, 64, 768, 1, 33, 40), "int4", "bf16", 1, 33, 5),
+    # decode that ends exactly at the cache capacity (P + S = max_seq)
+    ("full-capacity-int8", Shape(1, 256, 2, 2, 128, 384, 3, 29, 32), "int8", "int8", 3, 29, 3),
     ("batch33-int8-wide", Shape(1, 3584, 28, 28, 128, 512, 33, 8, 11), "int8", "int8", 33, 8, 3),
     # prefill GEMMs with too few 256 x 256 tiles run split-K with reduction kernels
     # (M >= 256; M = 300 leaves a ragged row tile)
