@@ -169,14 +169,15 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
     // The workgroup whose range holds the new position appends its k and v first (one
     // wave; the barrier below publishes the row to the other waves, and no other
     // workgroup reads that position).  Every workgroup reduces and rotates the queries
-    // of its group into LDS, in the MFMA operand format.
+    // of its group into LDS, in the MFMA operand format, starting from wave 1 so that a
+    // small group's queries are staged while wave 0 appends.
     const int pos = len - 1;
     if (pos / (4 * kps) == (int)blockIdx.x && w == 0) append_kv<D, KV8>(a, b, kvh, pos, lane);
     {
         const int Nqkv = (a.nh + 2 * a.nkv) * D;
         const int64_t pstride = (int64_t)a.batch * Nqkv;
         const float* prow = a.qkv_part + (int64_t)b * Nqkv + (int64_t)kvh * G * D;
-        for (int i = tid; i < G * (D / 2); i += 256) {
+        for (int i = (tid + 192) & 255; i < G * (D / 2); i += 256) {
             const int c = i / (D / 2), j = i % (D / 2);
             const float cs = a.cos_t[(int64_t)pos * (D / 2) + j], sn = a.sin_t[(int64_t)pos * (D / 2) + j];
             const float u = sum_parts(prow + c * D + j, a.ks, pstride);
