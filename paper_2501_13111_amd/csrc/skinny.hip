@@ -106,6 +106,60 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
         }
     };
 
+    // ---- activation-side loads go out before the weight loads: wait counts are in issue
+    // order, so the staging below then does not wait for the weights.  Each thread takes
+    // its first staged piece (and gain) and one of the rows' sum-of-squares partials.
+    const int chunks = klen / 8;                     // 8-element chunks per row
+    u32x4 xv0 = u32x4{0u, 0u, 0u, 0u}, gv0 = u32x4{0u, 0u, 0u, 0u};
+    if constexpr (XF == XF_COPY || XF == XF_NORM) {
+        if (tid < a.M * chunks) {
+            const int k = kb + (tid % chunks) * 8;
+            xv0 = *(const u32x4*)(a.X + (int64_t)(tid / chunks) * a.K + k);
+            if constexpr (XF == XF_NORM) gv0 = *(const u32x4*)(a.gain + k);
+        }
+    }
+    // XF_MERGE: the first piece's attention partials (the first NVP splits) likewise
+    constexpr int NVP = XF == XF_MERGE ? 4 : 1;
+    float pm[NVP], pl[NVP];
+    float4 po0[NVP], po1[NVP];
+    if constexpr (XF == XF_MERGE) {
+        if (tid < a.M * chunks) {
+            const int D = a.head_dim, nhd = a.K / D;
+            const int k = kb + (tid % chunks) * 8, h = k / D, dd = k % D;
+            const int nv = (*a.d_pos + a.att_kps) / a.att_kps;
+            const float* src = a.att_ws + ((int64_t)(tid / chunks) * nhd + h) * a.att_nsplit * (D + 4);
+#pragma unroll
+            for (int i = 0; i < NVP; ++i)
+                if (i < nv) {
+                    const float* q = src + i * (D + 4);
+                    pm[i] = q[D];
+                    pl[i] = q[D + 1];
+                    po0[i] = *(const float4*)(q + dd);
+                    po1[i] = *(const float4*)(q + dd + 4);
+                }
+        }
+    }
+    // XF_SWIGLU: the first piece's gate / up partials of the first KSP splits likewise
+    constexpr int KSP = XF == XF_SWIGLU ? 2 : 1;
+    float4 sg0[KSP], sg1[KSP], su0[KSP], su1[KSP];
+    if constexpr (XF == XF_SWIGLU) {
+        if (tid < a.M * chunks) {
+            const int F = a.K, k = kb + (tid % chunks) * 8;
+#pragma unroll
+            for (int i = 0; i < KSP; ++i)
+                if (i < a.src_ks) {
+                    const float* p = a.src_part + ((int64_t)i * a.M + tid / chunks) * (2 * (int64_t)F);
+                    sg0[i] = *(const float4*)(p + k);
+                    sg1[i] = *(const float4*)(p + k + 4);
+                    su0[i] = *(const float4*)(p + F + k);
+                    su1[i] = *(const float4*)(p + F + k + 4);
+                }
+        }
+    }
+    const bool ssq_lds = XF == XF_NORM && a.ssq != nullptr && a.M * a.ssq_blocks <= 256;
+    float ssp = 0.f;
+    if (ssq_lds && tid < a.M * a.ssq_blocks) ssp = a.ssq[tid];
+
     u32x4 wa[UNR][NS], wb[UNR][NS];
     uint32_t sza[UNR][NS], szb[UNR][NS];
 #pragma unroll
@@ -113,7 +167,16 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 
     // ---- stage the activation slice (with its transform) into LDS
     if constexpr (XF == XF_NORM) {
-        if (a.ssq != nullptr) {
+        if (ssq_lds) {
+            __shared__ float ssl[256];
+            ssl[tid] = ssp;
+            __syncthreads();
+            if (tid < a.M) {
+                float ss = 0.f;
+                for (int b = 0; b < a.ssq_blocks; ++b) ss += ssl[tid * a.ssq_blocks + b];
+                rrow[tid] = 1.0f / __fsqrt_rn(ss / (float)a.K + a.eps);
+            }
+        } else if (a.ssq != nullptr) {
             if (tid < a.M) {
                 float ss = 0.f;
                 for (int b = 0; b < a.ssq_blocks; ++b) ss += a.ssq[tid * a.ssq_blocks + b];
@@ -139,17 +202,18 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
         __syncthreads();
     }
     {
-        const int chunks = klen / 8;                 // 8-element chunks per row
-        for (int c = tid; c < a.M * chunks; c += 256) {
+        // the thread's first piece uses the values loaded before the weights; the loop
+        // takes the rest (several per thread only for long slices)
+        auto stage = [&](int c, bool pre) {
             const int m = c / chunks, kc = (c % chunks) * 8;
             const int k = kb + kc;
             uint32_t o[4];
             if constexpr (XF == XF_COPY) {
-                const u32x4 v = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+                const u32x4 v = pre ? xv0 : *(const u32x4*)(a.X + (int64_t)m * a.K + k);
                 o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
             } else if constexpr (XF == XF_NORM) {
-                const u32x4 v = *(const u32x4*)(a.X + (int64_t)m * a.K + k);
-                const u32x4 gg = *(const u32x4*)(a.gain + k);
+                const u32x4 v = pre ? xv0 : *(const u32x4*)(a.X + (int64_t)m * a.K + k);
+                const u32x4 gg = pre ? gv0 : *(const u32x4*)(a.gain + k);
                 const uint32_t vv[4] = {v.x, v.y, v.z, v.w}, gv[4] = {gg.x, gg.y, gg.z, gg.w};
                 const float rm = rrow[m];
 #pragma unroll
@@ -165,17 +229,32 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
                 const int nv = (*a.d_pos + a.att_kps) / a.att_kps;     // splits holding keys
                 const float* src = a.att_ws + ((int64_t)m * nhd + h) * a.att_nsplit * (D + 4);
                 float mx = -INFINITY;
-                for (int sp2 = 0; sp2 < nv; ++sp2) mx = fmaxf(mx, src[sp2 * (D + 4) + D]);
+#pragma unroll
+                for (int i = 0; i < NVP; ++i)
+                    if (i < nv) mx = fmaxf(mx, pre ? pm[i] : src[i * (D + 4) + D]);
+                for (int sp2 = NVP; sp2 < nv; ++sp2) mx = fmaxf(mx, src[sp2 * (D + 4) + D]);
                 float L = 0.f, ov[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) ov[j] = 0.f;
-                for (int sp2 = 0; sp2 < nv; ++sp2) {
-                    const float* q = src + sp2 * (D + 4);
-                    const float e = __expf(q[D] - mx);
-                    L += q[D + 1] * e;
-                    const float4 o0 = *(const float4*)(q + dd), o1 = *(const float4*)(q + dd + 4);
+                auto add = [&](float mv, float lv, float4 o0, float4 o1) {
+                    const float e = __expf(mv - mx);
+                    L += lv * e;
                     ov[0] += o0.x * e; ov[1] += o0.y * e; ov[2] += o0.z * e; ov[3] += o0.w * e;
                     ov[4] += o1.x * e; ov[5] += o1.y * e; ov[6] += o1.z * e; ov[7] += o1.w * e;
+                };
+#pragma unroll
+                for (int i = 0; i < NVP; ++i)
+                    if (i < nv) {
+                        if (pre) {
+                            add(pm[i], pl[i], po0[i], po1[i]);
+                        } else {
+                            const float* q = src + i * (D + 4);
+                            add(q[D], q[D + 1], *(const float4*)(q + dd), *(const float4*)(q + dd + 4));
+                        }
+                    }
+                for (int sp2 = NVP; sp2 < nv; ++sp2) {
+                    const float* q = src + sp2 * (D + 4);
+                    add(q[D], q[D + 1], *(const float4*)(q + dd), *(const float4*)(q + dd + 4));
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
@@ -186,14 +265,40 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
                 float gs[8], us[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) { gs[j] = 0.f; us[j] = 0.f; }
-                for (int s = 0; s < a.src_ks; ++s) {
-                    const float* p = a.src_part + ((int64_t)s * a.M + m) * (2 * (int64_t)F);
-                    const float4 g0 = *(const float4*)(p + k), g1 = *(const float4*)(p + k + 4);
-                    const float4 u0 = *(const float4*)(p + F + k), u1 = *(const float4*)(p + F + k + 4);
+                auto add = [&](float4 g0, float4 g1, float4 u0, float4 u1) {
                     gs[0] += g0.x; gs[1] += g0.y; gs[2] += g0.z; gs[3] += g0.w;
                     gs[4] += g1.x; gs[5] += g1.y; gs[6] += g1.z; gs[7] += g1.w;
                     us[0] += u0.x; us[1] += u0.y; us[2] += u0.z; us[3] += u0.w;
                     us[4] += u1.x; us[5] += u1.y; us[6] += u1.z; us[7] += u1.w;
+                };
+                auto part = [&](int s2) { return a.src_part + ((int64_t)s2 * a.M + m) * (2 * (int64_t)F); };
+#pragma unroll
+                for (int i = 0; i < KSP; ++i)
+                    if (i < a.src_ks) {
+                        if (pre) {
+                            add(sg0[i], sg1[i], su0[i], su1[i]);
+                        } else {
+                            const float* p = part(i);
+                            add(*(const float4*)(p + k), *(const float4*)(p + k + 4), *(const float4*)(p + F + k),
+                                *(const float4*)(p + F + k + 4));
+                        }
+                    }
+                // the rest two splits at a time (one memory round trip per pair), added in order
+                int s2 = KSP;
+                for (; s2 + 1 < a.src_ks; s2 += 2) {
+                    const float* p = part(s2);
+                    const float* p1 = part(s2 + 1);
+                    const float4 g0 = *(const float4*)(p + k), g1 = *(const float4*)(p + k + 4);
+                    const float4 u0 = *(const float4*)(p + F + k), u1 = *(const float4*)(p + F + k + 4);
+                    const float4 h0 = *(const float4*)(p1 + k), h1 = *(const float4*)(p1 + k + 4);
+                    const float4 v0 = *(const float4*)(p1 + F + k), v1 = *(const float4*)(p1 + F + k + 4);
+                    add(g0, g1, u0, u1);
+                    add(h0, h1, v0, v1);
+                }
+                if (s2 < a.src_ks) {
+                    const float* p = part(s2);
+                    add(*(const float4*)(p + k), *(const float4*)(p + k + 4), *(const float4*)(p + F + k),
+                        *(const float4*)(p + F + k + 4));
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
@@ -201,7 +306,9 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
                            ((uint32_t)act_store(bfround(silu_f(gs[2 * j + 1]) * us[2 * j + 1]), AF) << 16);
             }
             *(u32x4*)(As + m * ld + kc) = u32x4{o[0], o[1], o[2], o[3]};
-        }
+        };
+        if (tid < a.M * chunks) stage(tid, true);
+        for (int c = tid + 256; c < a.M * chunks; c += 256) stage(c, false);
     }
     __syncthreads();
 
