@@ -850,7 +850,7 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
         if ((st = synth_rows(h, &W.down, 0, H, l, FP_T_DOWN, tmp, tmpq))) return bail(st);
         if (h->wq == FP_WQ_INT4_G128) {
             for (Mat* m : {&W.qkv, &W.o, &W.gu, &W.down})
-                if ((st = chk(launch_pack_sz(m->scales, m->zeros, (int64_t)m->N * (m->K / 128), m->sz, 0)))) return bail(st);
+                if ((st = chk(launch_pack_sz(m->scales, m->zeros, m->N, m->K / 128, m->sz, 0)))) return bail(st);
         }
     }
     if (hipDeviceSynchronize() != hipSuccess) return bail(fail(FP_ERR_HIP, "weight synthesis failed"));

@@ -57,7 +57,7 @@ struct SkinnyArgs {
     const void* W;            // fragment-major tiles (bf16 / int8 / int4 in device nibble order)
     const uint16_t* scales;   // fp16: int8 [N]; int4 [N, K/128]
     const uint16_t* zeros;    // fp16 [N, K/128] (int4)
-    const uint32_t* sz;       // int4: scale | zero << 16 per (row, group) [N, K/128]
+    const uint32_t* sz;       // int4: scale | zero << 16 per (row, group), group-major [K/128, N]
     int M, N, K;
     int kst;                  // K-steps per 16-row block row of W (ceil(K / KS))
     int dual_F;
@@ -81,7 +81,7 @@ struct GemmArgs {
     const void* W;            // fragment-major tiles
     const uint16_t* scales;
     const uint16_t* zeros;
-    const uint32_t* sz;       // int4: scale | zero << 16 per (row, group)
+    const uint32_t* sz;       // int4: scale | zero << 16 per (row, group), group-major [K/128, N]
     int M, N, K, F;           // F: SwiGLU width (N = 2F rows of [gate; up])
     int kst;                  // K-steps per 16-row block row of W
     float* out32;             // EPI_F32: [M, N]
@@ -169,7 +169,7 @@ hipError_t launch_quant_int8(const uint16_t* w, int N, int K, int8_t* codes, uin
                              hipStream_t st);
 hipError_t launch_quant_int4(const uint16_t* w, int N, int K, uint32_t* codes, uint16_t* scales,
                              uint16_t* zeros, hipStream_t st);
-hipError_t launch_pack_sz(const uint16_t* scales, const uint16_t* zeros, int64_t n, uint32_t* sz,
+hipError_t launch_pack_sz(const uint16_t* scales, const uint16_t* zeros, int N, int ng, uint32_t* sz,
                           hipStream_t st);
 
 hipError_t launch_rmsnorm(const uint16_t* x, int M, int H, const uint16_t* g, float eps, uint16_t* out,

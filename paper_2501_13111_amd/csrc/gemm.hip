@@ -149,7 +149,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
             int n = brow(lr, v);
             n = v ? n : 0;
             rb[0] = Wt[((int64_t)(n >> 4) * a.kst + k0 / 128) * 64 + (j & 15) + 16 * g];
-            sg.sz = a.sz[(int64_t)n * (a.K / 128) + k0 / 128];
+            sg.sz = a.sz[(int64_t)(k0 / 128) * a.N + n];
         }
     };
     auto store_tile = [&](uint16_t* As, uint16_t* Bs, const Stage& sg) {
@@ -451,13 +451,13 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             if (q == 0) {
                 // raw words, not converted here: a conversion would wait for them (and
                 // for the stage's copies issued before them)
-                const int grp = k0 / 128, ng = a.K / 128;
+                const int grp = k0 / 128;
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
                     bool v;
                     const int gb = grow_block(col_rb(2 * j + ((lane & 31) >> 4)), v);
                     nsz[j] = 0u;
-                    if (v) nsz[j] = a.sz[((int64_t)gb * 16 + r) * ng + grp];
+                    if (v) nsz[j] = a.sz[(int64_t)grp * a.N + gb * 16 + r];
                 }
             }
         }

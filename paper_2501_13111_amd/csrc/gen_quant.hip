@@ -152,18 +152,25 @@ hipError_t launch_quant_int8(const uint16_t* w, int N, int K, int8_t* codes, uin
 }
 
 // int4 groups: scale and zero point of each (row, group) packed into one word
-// (scale bits low, zero bits high), so a kernel fetches both with one load.
+// (scale bits low, zero bits high), so a kernel fetches both with one load.  The words
+// are stored group-major, sz[g * N + n]: the rows a wave streams through one group are
+// consecutive words (one cache line for 32 rows) rather than one line per row.
 __global__ void __launch_bounds__(256) pack_sz_kernel(const uint16_t* __restrict__ scales,
-                                                      const uint16_t* __restrict__ zeros, int64_t n,
+                                                      const uint16_t* __restrict__ zeros, int N, int ng,
                                                       uint32_t* __restrict__ sz) {
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
-        sz[i] = (uint32_t)scales[i] | ((uint32_t)zeros[i] << 16);
+    const int64_t n_all = (int64_t)N * ng;
+    for (int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x; o < n_all; o += (int64_t)gridDim.x * 256) {
+        const int64_t g = o / N, n = o % N;
+        const int64_t i = n * ng + g;                 // [N, ng] index of scales and zeros
+        sz[o] = (uint32_t)scales[i] | ((uint32_t)zeros[i] << 16);
+    }
 }
 
-hipError_t launch_pack_sz(const uint16_t* scales, const uint16_t* zeros, int64_t n, uint32_t* sz,
+hipError_t launch_pack_sz(const uint16_t* scales, const uint16_t* zeros, int N, int ng, uint32_t* sz,
                           hipStream_t st) {
+    const int64_t n = (int64_t)N * ng;
     const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
-    FP_LAUNCH(pack_sz_kernel, dim3((unsigned)blocks), dim3(256), 0, st, scales, zeros, n, sz);
+    FP_LAUNCH(pack_sz_kernel, dim3((unsigned)blocks), dim3(256), 0, st, scales, zeros, N, ng, sz);
     return hipGetLastError();
 }
 

@@ -94,7 +94,7 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
     const int nrows = a.dual_F > 0 ? 2 * a.dual_F : a.N;
     const int ngr = a.K / 128;
     const __amdgpu_buffer_rsrc_t wres = buf_rsrc(a.W, (uint32_t)((nrows / 16) * a.kst * 1024));
-    const __amdgpu_buffer_rsrc_t szres = buf_rsrc(a.sz, WF == W_INT4 ? (uint32_t)(nrows * ngr * 4) : 0u);
+    const __amdgpu_buffer_rsrc_t szres = buf_rsrc(a.sz, WF == W_INT4 ? (uint32_t)(ngr * nrows * 4) : 0u);
     auto load_w = [&](int kk, u32x4* dst, uint32_t* szd) {
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
@@ -102,7 +102,7 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
             dst[s] = buf_load_nt(wres, off_or_oob(rv[s] && kk < ke, (blk * 64 + lane) * 16));
             if constexpr (WF == W_INT4)
                 szd[s] = __builtin_amdgcn_raw_buffer_load_b32(
-                    szres, off_or_oob(rv[s] && kk < ke, (uint32_t)(row[s] * ngr + kk / 128) * 4u), 0, 0);
+                    szres, off_or_oob(rv[s] && kk < ke, (uint32_t)((kk / 128) * nrows + row[s]) * 4u), 0, 0);
         }
     };
 
@@ -517,10 +517,10 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
             }
         if constexpr (WF == W_INT4) {
             if constexpr (M32) {
-                sz[0] = a.sz[(int64_t)myrow * (a.K / 128) + st0];
+                sz[0] = a.sz[(int64_t)st0 * nrows + myrow];
             } else {
 #pragma unroll
-                for (int s = 0; s < NS; ++s) sz[s] = a.sz[(int64_t)row[s] * (a.K / 128) + st0];
+                for (int s = 0; s < NS; ++s) sz[s] = a.sz[(int64_t)st0 * nrows + row[s]];
             }
         }
     };
