@@ -3,25 +3,26 @@
 // per-(position, kv head) scales -- the INT8 KV cache of paper Sec. 3.2), so
 // that prefill sees exactly what later decode steps see.
 //
-// Flash-style on MFMA 16x16x32, written in the transposed form
-//     S^T = K Q^T          (A = key rows from LDS, B = the wave's 16 queries)
+// Flash-style on MFMA 32x32x16, written in the transposed form
+//     S^T = K Q^T          (A = key rows from LDS, B = the wave's 32 queries)
 //     O^T += V^T P^T       (A = value columns, B = the probabilities already in
 //                           the lanes)
-// so the probabilities never leave registers: after S^T, lane (q, g) holds the
-// scores of keys 16t + 4g + i for its query column q, which are exactly the 8
-// k-values it must supply as B for a 32-key MFMA step (subtiles t, t+1).  The
-// value cache is stored transposed in 32-position blocks whose slots follow that
-// order (vt_slot), so the value tile is copied into LDS as it is and each A
+// so the probabilities never leave registers: after S^T, lane l holds the scores of
+// 16 keys of a 32-key subtile for its query column l % 32 (element e: key
+// 8 (e / 4) + 4 (l / 32) + e % 4).  A 16-key P.V step j takes elements 4j .. 4j+3
+// and 4j+8 .. 4j+11, whose keys sit in slots 16 j + 8 (l / 32) .. + 7 of the
+// value cache's transposed 32-position blocks (vt_slot order), so each value
 // fragment is one contiguous 16-byte LDS read.
-// Online softmax per query column (max / sum across the 4 lane groups by
-// shuffles).  int8 caches: codes are exact in fp16; s_k scales the scores and
-// s_v the probabilities.  Heaviest (latest) query tiles are launched first.
+// Online softmax per query column (max / sum across the two lane halves by one
+// shuffle).  int8 caches: codes are exact in fp16; s_k scales the scores and s_v
+// the probabilities.  Heaviest (latest) query tiles are launched first.
 #include "fp_device.h"
 #include "fp_internal.h"
 
 namespace fpk {
 
-// Workgroup = 8 waves x 16 queries of one head; key tiles of 64 are staged in LDS
+// Workgroup = NW waves x 32 queries of one head (8 waves, or 4 when 8-wave workgroups
+// would leave CUs idle); key tiles of 64 are staged in LDS
 // (double buffered: the next tile is loaded into registers while the current one is
 // multiplied, then written to the other buffer; a bare barrier keeps those loads in
 // flight).  A bf16 cache runs on bf16 MFMA; an int8 cache is converted to exact fp16
@@ -29,11 +30,12 @@ namespace fpk {
 // Scores are kept in the base-2 domain (scaled by log2 e) so each probability is
 // one exp2; the causal mask is applied only on tiles that reach past the wave's
 // first query.
-constexpr int PQ = 128;          // queries per workgroup
 constexpr int PKT = 64;          // keys per tile
 
-template <int D, bool KV8>
-__global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
+template <int D, bool KV8, int NW>
+__global__ void __launch_bounds__(64 * NW, 8 / NW) attn_prefill_kernel(AttnPreArgs a) {
+    constexpr int NT = 64 * NW;   // threads
+    constexpr int PQ = 32 * NW;   // queries per workgroup
     constexpr int AF = KV8 ? ACT_F16 : ACT_BF16;
     constexpr int KP = D + 8;     // padded row of the key tile (u16)
     constexpr int VP = PKT + 8;   // padded row of the value tile (u16), slots in vt_slot order
@@ -43,7 +45,7 @@ __global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
     __shared__ float ksc[2][PKT], vsc[2][PKT];
     // register staging: 16-byte pieces of the K tile and of the two value blocks
     constexpr int KPC = PKT * D * (KV8 ? 1 : 2) / 16;
-    constexpr int NKP = (KPC + 511) / 512;
+    constexpr int NKP = (KPC + NT - 1) / NT;
     constexpr int EPP = KV8 ? 16 : 8;            // elements per piece
 
     const int nqt = (a.P + PQ - 1) / PQ;
@@ -51,24 +53,25 @@ __global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
     const int h = blockIdx.y, b = blockIdx.z;
     const int kvh = (h * a.nkv) / a.nh;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int r = lane & 15, g = lane >> 4;
+    const int l32 = lane & 31, h32 = lane >> 5;
     const int p0 = qt * PQ;
-    const int qpos = p0 + 16 * w + r;             // this lane's query column
+    const int qpos = p0 + 32 * w + l32;           // this lane's query column
     const bool qvalid = qpos < a.P;
-    const int wfirst = p0 + 16 * w;               // first and last query of this wave
-    const int wlast = min(a.P - 1, wfirst + 15);
+    const int wfirst = p0 + 32 * w;               // first and last query of this wave
+    const int wlast = min(a.P - 1, wfirst + 31);
     const float sl2 = a.scale * 1.4426950408889634f;   // scores in the base-2 domain
 
-    // Q^T fragments for the D/32 MFMA k-steps
-    u32x4 qf[D / 32];
+    // Q^T fragments for the D/16 MFMA k-steps: lane l supplies query l % 32, dims
+    // 16 s + 8 (l / 32) .. + 7
+    u32x4 qf[D / 16];
     {
         const float* qrow = a.q + ((int64_t)b * a.P + (qvalid ? qpos : 0)) * a.nh * D + h * D;
 #pragma unroll
-        for (int j = 0; j < D / 32; ++j) {
+        for (int j = 0; j < D / 16; ++j) {
             uint32_t v[4] = {0u, 0u, 0u, 0u};
             if (qvalid) {
-                const float4 x0 = *(const float4*)(qrow + 32 * j + 8 * g);
-                const float4 x1 = *(const float4*)(qrow + 32 * j + 8 * g + 4);
+                const float4 x0 = *(const float4*)(qrow + 16 * j + 8 * h32);
+                const float4 x1 = *(const float4*)(qrow + 16 * j + 8 * h32 + 4);
                 if constexpr (KV8) {
                     v[0] = pack_f16_hw(x0.x, x0.y); v[1] = pack_f16_hw(x0.z, x0.w);
                     v[2] = pack_f16_hw(x1.x, x1.y); v[3] = pack_f16_hw(x1.z, x1.w);
@@ -81,9 +84,9 @@ __global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
         }
     }
 
-    f32x4 oacc[D / 16];
+    f32x16 oacc[D / 32];                          // O^T: dim 32 dt + 8 (e / 4) + 4 (l / 32) + e % 4
 #pragma unroll
-    for (int dd = 0; dd < D / 16; ++dd) oacc[dd] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = f32x16{};
     float m_run = -INFINITY, l_run = 0.f;
 
     const int64_t crow0 = ((int64_t)b * a.nkv + kvh) * a.kv_stride; // key row of position 0
@@ -101,7 +104,7 @@ __global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
     auto load = [&](int kt, Stage& sg) {
 #pragma unroll
         for (int i = 0; i < NKP; ++i) {
-            const int c = tid + 512 * i;
+            const int c = tid + NT * i;
             sg.k[i] = u32x4{0u, 0u, 0u, 0u};
             sg.v[i] = u32x4{0u, 0u, 0u, 0u};
             if (c < KPC) {
@@ -126,7 +129,7 @@ __global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
     auto store = [&](int st, const Stage& sg) {
 #pragma unroll
         for (int i = 0; i < NKP; ++i) {
-            const int c = tid + 512 * i;
+            const int c = tid + NT * i;
             if (c < KPC) {
                 const int key = c / (D / EPP), dc = (c % (D / EPP)) * EPP;
                 const int q = c % VPD, dd = (c / VPD) % D, blk = c / (VPD * D);
@@ -156,83 +159,84 @@ __global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
     };
 
     auto compute = [&](int kt, int st, bool masked) {
-        // ---- S^T = K Q^T for the 4 key subtiles (base-2 domain)
-        float s[4][4];
+        // ---- S^T = K Q^T for the two 32-key subtiles (base-2 domain)
+        f32x16 sc[2];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kk = 0; kk < 2; ++kk) {
+            f32x16 acc = f32x16{};
 #pragma unroll
-            for (int j = 0; j < D / 32; ++j) {
-                const u32x4 ka = *(const u32x4*)(&Ks[st][(16 * kk + r) * KP + 32 * j + 8 * g]);
-                acc = mfma16<AF>(ka, qf[j], acc);
+            for (int j = 0; j < D / 16; ++j) {
+                const u32x4 ka = *(const u32x4*)(&Ks[st][(32 * kk + l32) * KP + 16 * j + 8 * h32]);
+                acc = mfma32<AF>(ka, qf[j], acc);
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key = 16 * kk + 4 * g + i;
+            for (int e = 0; e < 16; ++e) {
+                const int key = 32 * kk + 8 * (e >> 2) + 4 * h32 + (e & 3);
                 float v;
-                if constexpr (KV8) v = acc[i] * ksc[st][key];
-                else v = acc[i] * sl2;
+                if constexpr (KV8) v = acc[e] * ksc[st][key];
+                else v = acc[e] * sl2;
                 if (masked) {
                     const int kpos = kt * PKT + key;
                     v = (kpos <= qpos && kpos < a.P) ? v : -INFINITY;
                 }
-                s[kk][i] = v;
+                acc[e] = v;
             }
+            sc[kk] = acc;
         }
-        // ---- online softmax for this lane's query column
+        // ---- online softmax for this lane's query column (the other 32 keys of the tile
+        // are in lane l ^ 32)
         float tmax = -INFINITY;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, s[kk][i]);
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+            for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sc[kk][e]);
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
         const float m_new = fmaxf(m_run, tmax);
         const float alpha = exp2f(m_run - m_new);
         float psum = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float p = exp2f(s[kk][i] - m_new);
-                s[kk][i] = p;
+            for (int e = 0; e < 16; ++e) {
+                const float p = exp2f(sc[kk][e] - m_new);
+                sc[kk][e] = p;
                 psum += p;
             }
-        psum += __shfl_xor(psum, 16, 64);
         psum += __shfl_xor(psum, 32, 64);
         l_run = l_run * alpha + psum;
         m_run = m_new;
 #pragma unroll
-        for (int dd = 0; dd < D / 16; ++dd) oacc[dd] *= alpha;
+        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
 
-        // ---- O^T += V^T P^T, two 32-key steps
+        // ---- O^T += V^T P^T, two 16-key steps per subtile
 #pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2) {
-            uint32_t pb[4];
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int kk = 2 * k2 + half;
-                float pv[4];
+            for (int j = 0; j < 2; ++j) {
+                float pv[8];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    pv[i] = s[kk][i];
-                    if constexpr (KV8) pv[i] *= vsc[st][16 * kk + 4 * g + i];
+                    pv[i] = sc[kk][4 * j + i];
+                    pv[4 + i] = sc[kk][4 * j + 8 + i];
                 }
                 if constexpr (KV8) {
-                    pb[2 * half] = pack_f16_hw(pv[0], pv[1]);
-                    pb[2 * half + 1] = pack_f16_hw(pv[2], pv[3]);
-                } else {
-                    pb[2 * half] = pack_bf16_hw(pv[0], pv[1]);
-                    pb[2 * half + 1] = pack_bf16_hw(pv[2], pv[3]);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i)
+                        pv[i] *= vsc[st][32 * kk + 8 * (j + 2 * (i >> 2)) + 4 * h32 + (i & 3)];
+                }
+                u32x4 pfrag;
+                if constexpr (KV8)
+                    pfrag = u32x4{pack_f16_hw(pv[0], pv[1]), pack_f16_hw(pv[2], pv[3]), pack_f16_hw(pv[4], pv[5]),
+                                  pack_f16_hw(pv[6], pv[7])};
+                else
+                    pfrag = u32x4{pack_bf16_hw(pv[0], pv[1]), pack_bf16_hw(pv[2], pv[3]), pack_bf16_hw(pv[4], pv[5]),
+                                  pack_bf16_hw(pv[6], pv[7])};
+#pragma unroll
+                for (int dt = 0; dt < D / 32; ++dt) {
+                    const u32x4 vf = *(const u32x4*)(&Vt[st][(32 * dt + l32) * VP + 32 * kk + 16 * j + 8 * h32]);
+                    oacc[dt] = mfma32<AF>(vf, pfrag, oacc[dt]);
                 }
             }
-            const u32x4 pfrag = u32x4{pb[0], pb[1], pb[2], pb[3]};
-#pragma unroll
-            for (int dd = 0; dd < D / 16; ++dd) {
-                const u32x4 vf = *(const u32x4*)(&Vt[st][(16 * dd + r) * VP + 32 * k2 + 8 * g]);
-                oacc[dd] = mfma16<AF>(vf, pfrag, oacc[dd]);
-            }
-        }
     };
     auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
@@ -255,24 +259,34 @@ __global__ void __launch_bounds__(512) attn_prefill_kernel(AttnPreArgs a) {
     const float inv = 1.0f / l_run;
     uint16_t* orow = a.out + ((int64_t)b * a.P + qpos) * a.nh * D + h * D;
 #pragma unroll
-    for (int dd = 0; dd < D / 16; ++dd) {
-        uint16_t v[4];
+    for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = act_store(bfround(oacc[dd][i] * inv), a.out_fmt);
-        *(u32x2*)(orow + 16 * dd + 4 * g) =
-            u32x2{(uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | ((uint32_t)v[3] << 16)};
-    }
+        for (int e4 = 0; e4 < 4; ++e4) {
+            uint16_t v[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = act_store(bfround(oacc[dt][4 * e4 + i] * inv), a.out_fmt);
+            *(u32x2*)(orow + 32 * dt + 8 * e4 + 4 * h32) =
+                u32x2{(uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | ((uint32_t)v[3] << 16)};
+        }
+}
+
+template <int D, bool KV8>
+static void launch_ap(const AttnPreArgs& a, int B, hipStream_t st) {
+    // 8 waves (256 queries) per workgroup when that still gives every CU a workgroup;
+    // 4 waves otherwise (2-wave workgroups measured slower still)
+    if ((int64_t)((a.P + 255) / 256) * a.nh * B >= 256)
+        FP_LAUNCH((attn_prefill_kernel<D, KV8, 8>), dim3((a.P + 255) / 256, a.nh, B), dim3(512), 0, st, a);
+    else
+        FP_LAUNCH((attn_prefill_kernel<D, KV8, 4>), dim3((a.P + 127) / 128, a.nh, B), dim3(256), 0, st, a);
 }
 
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st) {
-    const int nqt = (a.P + PQ - 1) / PQ;
-    dim3 grid(nqt, a.nh, B);
     if (a.d == 128) {
-        if (a.kv_int8) FP_LAUNCH((attn_prefill_kernel<128, true>), grid, dim3(512), 0, st, a);
-        else FP_LAUNCH((attn_prefill_kernel<128, false>), grid, dim3(512), 0, st, a);
+        if (a.kv_int8) launch_ap<128, true>(a, B, st);
+        else launch_ap<128, false>(a, B, st);
     } else if (a.d == 64) {
-        if (a.kv_int8) FP_LAUNCH((attn_prefill_kernel<64, true>), grid, dim3(512), 0, st, a);
-        else FP_LAUNCH((attn_prefill_kernel<64, false>), grid, dim3(512), 0, st, a);
+        if (a.kv_int8) launch_ap<64, true>(a, B, st);
+        else launch_ap<64, false>(a, B, st);
     } else {
         return hipErrorInvalidValue;
     }
