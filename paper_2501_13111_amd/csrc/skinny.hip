@@ -17,7 +17,9 @@
 // B, each with 8 consecutive k from the lane's k-slice (l / 16); the output lane
 // holds C[4 (l/16) + i][l % 16].  A and B use the same k assignment, so the order
 // of k inside a K-step is free; the int4 nibble order on the device makes nibble
-// pairs come out as consecutive k.
+// pairs come out as consecutive k.  Batches of 17 to 64 use 32x32x16 instead (see
+// skinny_batch_kernel).  int4 scale / zero words are stored group-major, so the words
+// of consecutive rows for one group are consecutive in memory.
 //
 // Weights are stored fragment-major: the 64 lanes' 16-byte operands of one 16-row
 // subtile and one K-step form a contiguous 1 KiB block, and a row of blocks runs
