@@ -41,7 +41,7 @@ typedef enum {
     FP_ERR_CAPACITY = -3,      /* batch / prompt / sequence beyond what the handle was created for */
     FP_ERR_OOM = -4,           /* device allocation failed */
     FP_ERR_HIP = -5,           /* HIP runtime error (no device, launch failure, ...) */
-    FP_ERR_UNSUPPORTED = -6    /* valid request this build does not implement */
+    FP_ERR_UNSUPPORTED = -6    /* valid request the library does not implement */
 } fp_status;
 
 /* Weight compression (Sec. 3.2). */
