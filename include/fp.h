@@ -120,6 +120,20 @@ fp_status fp_prefill(fp_layer* layer, const void* x, int32_t B, int32_t P, void*
 fp_status fp_decode_step(fp_layer* layer, const void* x, void* y, void* stream);
 
 /*
+ * n consecutive decode steps, each step's output fed back as the next step's input
+ * (the fingerprint generating n tokens, Sec. 5.3).  Step 1 reads x and writes y,
+ * step 2 reads y and writes x, and so on: the last step's output ends in y when n
+ * is odd and in x when n is even.  x and y: device bf16 [B, hidden] each, both
+ * written, no aliasing.  With the decode graph on (fp_set_decode_graph), the n
+ * steps are captured once per (x, y, n) and replayed as one graph, which saves a
+ * graph launch per step; the results equal n calls of fp_decode_step.  The
+ * position advances by n.  FP_ERR_INVALID_ARG for n < 1, NULL or overlapping
+ * buffers; FP_ERR_STATE before a prefill; FP_ERR_CAPACITY when fewer than n
+ * positions remain before max_seq (nothing runs).
+ */
+fp_status fp_decode_steps(fp_layer* layer, void* x, void* y, int32_t n, void* stream);
+
+/*
  * Replay decode steps as a captured HIP graph (1, the default) or launch the
  * kernels one by one (0).  Results are identical.
  */

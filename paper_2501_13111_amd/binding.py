@@ -71,6 +71,7 @@ def load(path: str | None = None):
         "fp_layer_destroy": [vp],
         "fp_prefill": [vp, vp, i32, i32, vp, vp],
         "fp_decode_step": [vp, vp, vp, vp],
+        "fp_decode_steps": [vp, vp, vp, i32, vp],
         "fp_set_decode_graph": [vp, i32],
         "fp_fill_normal": [vp, i64, u64, i32, i32, ctypes.c_float, ctypes.c_float, vp],
         "fp_export_weight": [vp, i32, i32, vp, vp, vp],
@@ -179,6 +180,18 @@ class Fingerprint:
         xp = _dev_ptr(x, numel=self.B * H, name="x")
         yp = _dev_ptr(y, numel=self.B * H, name="y")
         _check(load().fp_decode_step(self._h, xp, yp, _stream(stream)), "fp_decode_step")
+
+    def decode_steps(self, x, y, n: int, stream=None):
+        """n decode steps alternating between x and y (step 1 writes y); returns the
+        buffer holding the last step's output (y for odd n, x for even n)."""
+        H = self.shape.hidden
+        xp = _dev_ptr(x, numel=self.B * H, name="x")
+        yp = _dev_ptr(y, numel=self.B * H, name="y")
+        _check(load().fp_decode_steps(self._h, xp, yp, int(n), _stream(stream)), "fp_decode_steps")
+        return y if n % 2 == 1 else x
+
+    def decode_steps_ptr(self, x_ptr: int, y_ptr: int, n: int, stream_ptr: int = 0):
+        _check(load().fp_decode_steps(self._h, x_ptr, y_ptr, int(n), stream_ptr), "fp_decode_steps")
 
     def prefill_ptr(self, x_ptr: int, y_ptr: int, B: int, P: int, stream_ptr: int = 0):
         """Raw-pointer form (host-side tests with unbacked handles)."""

@@ -25,6 +25,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <tuple>
 #include <string>
 #include <utility>
 #include <vector>
@@ -162,6 +163,7 @@ struct fp_layer {
     uint16_t* ldump = nullptr;      // per-layer outputs [n_layers, B, T, hidden] (debug)
     hipStream_t cap_stream = nullptr;
     std::map<std::pair<const void*, void*>, hipGraphExec_t> graphs;
+    std::map<std::tuple<void*, void*, int>, hipGraphExec_t> mgraphs;   // fp_decode_steps: (x, y, n)
     Prof prof;
     size_t bytes_w = 0, bytes_kv = 0, bytes_ws = 0;
     std::vector<void*> allocs;
@@ -193,6 +195,8 @@ fp_status alloc_t(fp_layer* h, T** p, size_t count, size_t* counter) {
 void free_all(fp_layer* h) {
     for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
     h->graphs.clear();
+    for (auto& kv : h->mgraphs) (void)hipGraphExecDestroy(kv.second);
+    h->mgraphs.clear();
     if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
     h->cap_stream = nullptr;
     for (void* p : h->allocs) (void)hipFree(p);
@@ -949,6 +953,56 @@ fp_status fp_decode_step(fp_layer* h, const void* x, void* y, void* stream) {
         }
     }
     h->pos += 1;
+    return FP_OK;
+}
+
+fp_status fp_decode_steps(fp_layer* h, void* x, void* y, int32_t n, void* stream) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (!x || !y) return fail(FP_ERR_INVALID_ARG, "x and y must be device pointers");
+    if (n < 1) return fail(FP_ERR_INVALID_ARG, "n = %d steps", n);
+    if (!h->prefilled) return fail(FP_ERR_STATE, "decode steps before prefill");
+    if (h->pos + (int64_t)n > h->s.max_seq)
+        return fail(FP_ERR_CAPACITY, "%d steps from position %d pass max_seq %d", n, h->pos, h->s.max_seq);
+    const size_t bytes = (size_t)h->B * h->s.hidden * 2;
+    if (overlap(x, bytes, y, bytes)) return fail(FP_ERR_INVALID_ARG, "x and y overlap");
+    if (!h->unbacked) {
+        // the step kernels advance the device-side position, so the steps chain as they are
+        auto run = [&](hipStream_t s) -> fp_status {
+            for (int i = 0; i < n; ++i) {
+                const uint16_t* src = (const uint16_t*)((i & 1) ? y : x);
+                uint16_t* dst = (uint16_t*)((i & 1) ? x : y);
+                fp_status rc = enqueue_decode(h, src, dst, s);
+                if (rc) return rc;
+            }
+            return FP_OK;
+        };
+        hipStream_t st = (hipStream_t)stream;
+        fp_status rc;
+        if (h->use_graph && !h->dump && !h->ldump) {
+            const auto key = std::make_tuple(x, y, (int)n);
+            auto it = h->mgraphs.find(key);
+            if (it == h->mgraphs.end()) {
+                hipGraph_t g = nullptr;
+                hipGraphExec_t ge = nullptr;
+                HIPCHK(hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal));
+                rc = run(h->cap_stream);
+                hipError_t e = hipStreamEndCapture(h->cap_stream, &g);
+                if (rc) {
+                    if (g) (void)hipGraphDestroy(g);
+                    return rc;
+                }
+                if (e != hipSuccess) return fail(FP_ERR_HIP, "graph capture failed: %s", hipGetErrorString(e));
+                e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+                (void)hipGraphDestroy(g);
+                if (e != hipSuccess) return fail(FP_ERR_HIP, "graph instantiate failed: %s", hipGetErrorString(e));
+                it = h->mgraphs.emplace(key, ge).first;
+            }
+            HIPCHK(hipGraphLaunch(it->second, st));
+        } else {
+            if ((rc = run(st))) return rc;
+        }
+    }
+    h->pos += n;
     return FP_OK;
 }
 

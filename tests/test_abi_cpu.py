@@ -84,6 +84,9 @@ def test_state_machine_on_unbacked_handle():
         fp.decode_ptr(X, Y)
     assert e.value.code == -2        # decode before prefill
     with pytest.raises(FpError) as e:
+        fp.decode_steps_ptr(X, Y, 2)
+    assert e.value.code == -2
+    with pytest.raises(FpError) as e:
         fp.prefill_ptr(X, Y, 2, 8)
     assert e.value.code == -3        # batch beyond capacity
     with pytest.raises(FpError) as e:
@@ -107,6 +110,19 @@ def test_state_machine_on_unbacked_handle():
     assert fp.position() == (48, 1)  # nothing changed on error
     fp.prefill_ptr(X, Y, 1, 4)       # a new prefill resets the position
     assert fp.position() == (4, 1)
+    # n steps at once: all or nothing against the capacity
+    with pytest.raises(FpError) as e:
+        fp.decode_steps_ptr(X, Y, 0)
+    assert e.value.code == -1        # n < 1
+    with pytest.raises(FpError) as e:
+        fp.decode_steps_ptr(X, X + 100, 3)
+    assert e.value.code == -1        # x and y overlap
+    with pytest.raises(FpError) as e:
+        fp.decode_steps_ptr(X, Y, 45)
+    assert e.value.code == -3        # 4 + 45 > 48
+    assert fp.position() == (4, 1)
+    fp.decode_steps_ptr(X, Y, 44)
+    assert fp.position() == (48, 1)
     with pytest.raises(FpError) as e:
         fp.export_kv(0)
     assert e.value.code == -2
