@@ -67,7 +67,7 @@ def skinny_traffic(config):
 
 
 def cfg_of(name):
-    from oracle.layer import CONFIGS
+    from fpgen.workloads import CONFIGS
     return CONFIGS[name]
 
 

@@ -30,11 +30,14 @@ closed form for constant rows; RoPE against complex multiplication and its
 identity / norm / relative-position properties; attention against brute-force
 loops and torch's scaled_dot_product_attention; SiLU against torch; the layer
 against the identity special case, causality, batch independence and
-KV-cached decode == full recompute.
+KV-cached decode == full recompute; the whole two-layer stack against the same
+layer composed from torch library routines (F.linear, F.rms_norm, complex
+rotation, scaled_dot_product_attention, F.silu) for every weight format with a
+bf16 and with an int8 cache; and the int8 cache's codes and scales against an
+independent torch rebuild (keys quantised after the rotary embedding, both keys
+and values from their fp32 values).
 """
 from __future__ import annotations
-
-import dataclasses
 
 import numpy as np
 
@@ -43,44 +46,11 @@ from .numerics import bf16_round
 from .quant import (quant_int8_channel, dequant_int8_channel, quant_int4_g128,
                     dequant_int4_g128, pack_int4, quant_kv_int8)
 
+# The layer-stack shape and the five workloads live in the data-only table shared
+# with the benchmark.
+from fpgen.workloads import Shape, CONFIGS  # noqa: F401
+
 F32 = np.float32
-
-
-@dataclasses.dataclass(frozen=True)
-class Shape:
-    n_layers: int
-    hidden: int
-    n_heads: int
-    n_kv_heads: int
-    head_dim: int
-    ffn: int
-    max_batch: int
-    max_prompt: int
-    max_seq: int
-    rms_eps: float = 1e-5
-    rope_theta: float = 1e4
-
-    @property
-    def q_dim(self):
-        return self.n_heads * self.head_dim
-
-    @property
-    def kv_dim(self):
-        return self.n_kv_heads * self.head_dim
-
-
-# The five fingerprint workloads: (shape, weight quant, kv quant, batch, prompt, steps)
-def _cfg(L, H, nh, nkv, d, F, wq, kvq, B, P, S):
-    return dict(shape=Shape(L, H, nh, nkv, d, F, B, P, P + S), wq=wq, kvq=kvq, B=B, P=P, S=S)
-
-
-CONFIGS = {
-    "tiny": _cfg(1, 256, 4, 4, 64, 688, "bf16", "bf16", 1, 32, 16),
-    "llama2-7b-bf16": _cfg(2, 4096, 32, 32, 128, 11008, "bf16", "bf16", 1, 512, 100),
-    "llama2-7b-int8": _cfg(2, 4096, 32, 32, 128, 11008, "int8", "int8", 16, 512, 100),
-    "llama2-13b-int4": _cfg(4, 5120, 40, 40, 128, 13824, "int4", "bf16", 32, 1024, 100),
-    "llama2-70b-tp8-int4": _cfg(4, 8192, 8, 1, 128, 3584, "int4", "int8", 64, 2048, 100),
-}
 
 WEIGHT_NAMES = ("q", "k", "v", "o", "gate", "up", "down")
 TENSOR_ID = {"attn_norm": 0, "q": 1, "k": 2, "v": 3, "o": 4, "mlp_norm": 5,

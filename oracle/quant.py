@@ -21,7 +21,10 @@ the readings below are the ones the build fixes:
   rotary embedding) and V, the int8 rule above over the head_dim elements.
 
 Pins (tests/test_oracle_quant.py): brute-force nearest-code search over every
-code, the |w - w_hat| <= s/2 bound, exact grids, pack/unpack round trips.
+code, the |w - w_hat| <= s/2 bound, exact grids, pack/unpack round trips, and
+exact ties (w / s = k + 1/2 with power-of-two scales): int8 codes and int8 KV
+codes go to the even neighbour, int4 rounds to the even integer before the odd
+zero point is added, and a tie in -lo / s gives the even zero point.
 """
 import numpy as np
 

@@ -6,7 +6,7 @@ import pytest
 
 from paper_2501_13111_amd import binding
 from paper_2501_13111_amd.binding import Fingerprint, FpError, FpShape
-from oracle.layer import Shape, CONFIGS
+from fpgen.workloads import Shape, CONFIGS
 
 
 @pytest.fixture(scope="module")

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 
 import bench  # noqa: E402
-from oracle.layer import CONFIGS  # noqa: E402
+from fpgen.workloads import CONFIGS  # noqa: E402
 
 
 def test_more_than_one_gpu_is_refused_before_any_gpu_work():

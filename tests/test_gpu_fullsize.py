@@ -12,7 +12,7 @@ oracle drifts 1.7e-2 from the fp64 one at the 70B-shard shape)."""
 import numpy as np
 import pytest
 
-from oracle.layer import CONFIGS
+from fpgen.workloads import CONFIGS
 from tests.gpu_harness import TOL, log, run_parity
 
 pytestmark = pytest.mark.gpu

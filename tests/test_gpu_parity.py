@@ -7,7 +7,8 @@ import numpy as np
 import pytest
 
 import fpgen
-from oracle.layer import Shape, CONFIGS, Fingerprint as OracleFingerprint
+from fpgen.workloads import Shape, CONFIGS
+from oracle.layer import Fingerprint as OracleFingerprint
 from oracle.quant import quant_kv_int8
 from tests.gpu_harness import TOL, log, run_parity, bf16_to_np
 

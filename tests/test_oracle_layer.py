@@ -241,10 +241,26 @@ def test_configs_are_the_five_workloads():
     assert c5["shape"].hidden == 8192 and c5["shape"].n_heads == 8 and c5["shape"].n_kv_heads == 1
 
 
-def _torch_layer_stack(fp, x, P):
+def _torch_kv_int8(u):
+    """int8 KV store written with torch ops: u [B, P, n, d] fp32 (keys after the rotary
+    embedding, or values) -> dequantised float64 values, with the codes and scales.
+    One fp16 scale per (sequence, position, head): absmax / 127 rounded to fp16;
+    codes = round-half-even(u / scale) clamped to +-127."""
+    u = u.to(torch.float32)
+    amax = u.abs().amax(dim=-1, keepdim=True)
+    sc = (amax / 127.0).to(torch.float16).to(torch.float32)
+    safe = torch.where(sc == 0, torch.ones_like(sc), sc)
+    codes = torch.clamp(torch.round(u / safe), -127, 127)
+    codes = torch.where(sc == 0, torch.zeros_like(codes), codes)
+    return (codes * sc).double(), codes.to(torch.int8), sc[..., 0]
+
+
+def _torch_layer_stack(fp, x, P, kvq="bf16", kv_out=None):
     """The same layer built from torch library routines: F.linear (weight [out, in]),
     F.rms_norm, rotary embedding as complex multiplication (torch.polar),
-    F.scaled_dot_product_attention and F.silu, rounding to bf16 at the same points."""
+    F.scaled_dot_product_attention and F.silu, rounding to bf16 at the same points.
+    With kvq = "int8" the keys (after the rotary embedding) and values go through the
+    int8 store of ``_torch_kv_int8`` from fp32; ``kv_out`` collects its codes and scales."""
     s = fp.s
     t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
     rb = lambda a: torch.from_numpy(bf16_round(a.numpy()).astype(np.float64))
@@ -265,7 +281,13 @@ def _torch_layer_stack(fp, x, P):
         q = rope(Fnn.linear(xn, t(L["q"])).view(B, P, s.n_heads, s.head_dim))
         k = rope(Fnn.linear(xn, t(L["k"])).view(B, P, s.n_kv_heads, s.head_dim))
         v = Fnn.linear(xn, t(L["v"])).view(B, P, s.n_kv_heads, s.head_dim)
-        k, v = rb(k), rb(v)
+        if kvq == "int8":
+            k, kc, ksc = _torch_kv_int8(k)
+            v, vc, vsc = _torch_kv_int8(v)
+            if kv_out is not None:
+                kv_out.append((kc, ksc, vc, vsc))
+        else:
+            k, v = rb(k), rb(v)
         g = s.n_heads // s.n_kv_heads
         o = Fnn.scaled_dot_product_attention(
             q.transpose(1, 2), k.transpose(1, 2).repeat_interleave(g, 1),
@@ -279,12 +301,34 @@ def _torch_layer_stack(fp, x, P):
     return xx.numpy()
 
 
-@pytest.mark.parametrize("wq", ["bf16", "int8"])
-def test_layer_matches_torch_functional_composition(wq):
-    s = Shape(2, 128, 4, 2, 32, 192, 2, 10, 10)
-    fp = Fingerprint(s, wq, "bf16")
+@pytest.mark.parametrize("wq,kvq", [("bf16", "bf16"), ("int8", "bf16"), ("int4", "bf16"),
+                                    ("bf16", "int8"), ("int8", "int8"), ("int4", "int8")])
+def test_layer_matches_torch_functional_composition(wq, kvq):
+    s = Shape(2, 128, 4, 2, 32, 256, 2, 10, 10)
+    fp = Fingerprint(s, wq, kvq)
     x = _prompt(2, 10, s.hidden, seed=3)
     ours = fp.prefill(x)
-    ref = _torch_layer_stack(fp, x, 10)
+    ref = _torch_layer_stack(fp, x, 10, kvq)
     err = np.abs(ours - ref).max() / np.abs(ref).max()
     assert err <= 1e-6, err
+
+
+def test_int8_kv_codes_rebuilt_from_torch_ops():
+    """The int8 cache the oracle writes (codes and fp16 scales per sequence, position and
+    kv head) equals the one rebuilt independently with torch ops: keys quantised after
+    the rotary embedding, both keys and values quantised from their fp32 values (no
+    bf16 rounding first), for every layer of a two-layer stack."""
+    s = Shape(2, 256, 4, 2, 64, 256, 2, 12, 12)
+    for wq in ("bf16", "int4"):
+        fp = Fingerprint(s, wq, "int8")
+        x = _prompt(2, 12, s.hidden, seed=6)
+        fp.prefill(x)
+        kv = []
+        _torch_layer_stack(fp, x, 12, "int8", kv_out=kv)
+        for l, (kc, ksc, vc, vsc) in enumerate(kv):
+            cc = fp.kv_codes[l]
+            # torch [B, P, nkv, d] -> oracle layout [B, nkv, P, d]
+            assert np.array_equal(cc["k"][:, :, :12], kc.permute(0, 2, 1, 3).numpy()), (wq, l)
+            assert np.array_equal(cc["v"][:, :, :12], vc.permute(0, 2, 1, 3).numpy()), (wq, l)
+            assert np.array_equal(cc["ks"][:, :, :12], ksc.permute(0, 2, 1).numpy()), (wq, l)
+            assert np.array_equal(cc["vs"][:, :, :12], vsc.permute(0, 2, 1).numpy()), (wq, l)

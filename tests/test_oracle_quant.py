@@ -107,3 +107,57 @@ def test_kv_int8_per_head_bound():
     assert c.shape == k.shape and s.shape == k.shape[:-1]
     assert np.all(np.abs(k - c.astype(np.float32) * s[..., None]) <= s[..., None] / 2)
     assert np.all(np.abs(c).max(axis=-1) == 127)
+
+
+def test_int8_exact_ties_round_to_even():
+    """w / s landing exactly on k + 1/2 goes to the even neighbour (round half to even),
+    for both signs.  s = 2^-7 is exact in fp16, and the row's absmax 127 s makes
+    fp16(absmax / 127) = s exactly, so every w / s below is an exact fp32 quotient."""
+    s0 = np.float32(2.0 ** -7)
+    half = np.arange(-126, 126, dtype=np.float64) + 0.5          # -125.5 .. 125.5
+    w = np.concatenate([[127.0], half]) * float(s0)
+    c, s = quant_int8_channel(w.astype(np.float32)[None, :])
+    assert s[0] == s0
+    want = 2.0 * np.round(half / 2.0)                               # the even neighbour
+    assert np.all(np.abs(want - half) == 0.5) and np.all(want % 2 == 0)
+    assert np.array_equal(c[0, 1:].astype(np.float64), want)
+    # e.g. 0.5 -> 0, 1.5 -> 2, 2.5 -> 2, -0.5 -> 0, -1.5 -> -2, -2.5 -> -2
+    idx = {v: i for i, v in enumerate(half)}
+    assert [int(c[0, 1 + idx[v]]) for v in (0.5, 1.5, 2.5, -0.5, -1.5, -2.5)] == [0, 2, 2, 0, -2, -2]
+
+
+def test_int4_ties_round_before_the_zero_point_is_added():
+    """One 128-input group with lo = -5 s and hi = 10 s for s = 2^-6: the scale is
+    fp16((hi - lo) / 15) = s exactly and the zero point z = 5 is odd.  Inputs at
+    w / s = m + 1/2 round to the even m first and then add z; rounding after adding z
+    (an odd offset) would pick the other neighbour every time."""
+    s0 = np.float32(2.0 ** -6)
+    ties = np.array([-4.5, -3.5, -2.5, -1.5, -0.5, 0.5, 1.5, 2.5, 3.5, 4.5, 5.5, 6.5, 7.5, 8.5, 9.5])
+    vals = np.concatenate([[-5.0, 10.0], ties, np.zeros(128 - 2 - len(ties))])
+    w = (vals * float(s0)).astype(np.float32)[None, :]
+    q, s, z = quant_int4_g128(w)
+    assert s[0, 0] == s0 and z[0, 0] == 5
+    want = 2.0 * np.round(ties / 2.0) + 5                             # rint first, then + z
+    assert np.array_equal(q[0, 2:2 + len(ties)].astype(np.float64), want)
+    assert np.all(q[0, 2:2 + len(ties)] != np.round(ties + 5))       # the other order differs
+    # a tie in the zero point itself: lo = -2.5 s, hi = 12.5 s -> s exact, z = rint(2.5) = 2
+    vals2 = np.concatenate([[-2.5, 12.5, 1.5, -1.5], np.zeros(124)])
+    q2, s2, z2 = quant_int4_g128((vals2 * float(s0)).astype(np.float32)[None, :])
+    assert s2[0, 0] == s0 and z2[0, 0] == 2
+    assert [int(v) for v in q2[0, :4]] == [0, 14, 4, 0]               # -2->0, 12->14, 2->4, -2->0
+
+
+def test_kv_int8_ties_and_fp32_input():
+    """The KV quantiser is the int8 row rule over head_dim: an exact tie goes to the even
+    code, and the scale comes from the fp32 values as given (no prior bf16 rounding:
+    1 + 2^-10 is not a bf16 value and must survive into the quotient)."""
+    s0 = np.float32(2.0 ** -7)
+    row = np.zeros(16, np.float64)
+    row[0], row[1], row[2] = 127.0, 2.5, -3.5
+    c, s = quant_kv_int8((row * float(s0)).astype(np.float32)[None, None, :])
+    assert s[0, 0] == s0 and int(c[0, 0, 1]) == 2 and int(c[0, 0, 2]) == -4
+    # 100.5 + 2^-3: above the tie in fp32, exactly the tie once rounded to bf16 (ulp 0.5 at 100)
+    v = np.float32((100.5 + 2.0 ** -3) * float(s0))
+    row2 = np.array([127.0 * float(s0), v] + [0.0] * 14, np.float32)
+    c2, _ = quant_kv_int8(row2[None, None, :])
+    assert int(c2[0, 0, 1]) == 101
