@@ -58,10 +58,15 @@ typedef enum {
 } fp_kv_quant;
 
 /* Layer-stack shape and capacity, fixed at creation.
- * Requirements: n_heads % n_kv_heads == 0; head_dim even and <= 256;
- * hidden, n_heads*head_dim and ffn multiples of 16 (of 128 for int4 weights,
- * whose groups run along every projection's input dimension);
- * max_seq >= max_prompt + 1. */
+ * Requirements (checked by fp_layer_create on the host):
+ *  - every field > 0, rms_eps > 0, rope_theta > 0                 (else FP_ERR_INVALID_ARG)
+ *  - n_heads % n_kv_heads == 0                                      (FP_ERR_INVALID_ARG)
+ *  - hidden, n_heads*head_dim and ffn multiples of 16, of 128 for int4 weights (their
+ *    groups run along every projection's input dimension)          (FP_ERR_INVALID_ARG)
+ *  - max_seq >= max_prompt (max_seq == max_prompt leaves no room for a decode step
+ *    after a full-length prompt)                                    (FP_ERR_INVALID_ARG)
+ *  - head_dim 64 or 128; query group n_heads / n_kv_heads from 1 to 16;
+ *    max_batch <= 64; max_batch * max_prompt <= 2^24               (FP_ERR_UNSUPPORTED) */
 typedef struct {
     int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn;
     int32_t max_batch, max_prompt, max_seq;
@@ -97,14 +102,19 @@ fp_status fp_layer_create(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant
 fp_status fp_layer_create_unbacked(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant kvq,
                                    uint64_t seed, fp_layer** out);
 
-/* Free everything the handle owns (synchronises the device first).  NULL is a no-op. */
+/* Free everything the handle owns: weights, KV cache, workspace and captured decode
+ * graphs (synchronises the device first).  NULL is a no-op.  The handle is the
+ * fingerprint the Profiler deploys (Sec. 4.2, Sec. 5.1); destroying it ends its
+ * deployment. */
 fp_status fp_layer_destroy(fp_layer* layer);
 
 /*
  * Prefill (time to first token, Sec. 5.3): run the layer stack over a prompt.
  * x: device bf16 [B, P, hidden], y: device bf16 [B, P, hidden] (may not alias x).
  * Resets the KV cache of the B sequences and sets the position to P.
- * 1 <= B <= max_batch, 1 <= P <= max_prompt.
+ * 1 <= B <= max_batch, 1 <= P <= max_prompt.  A prefill with a batch other than
+ * the previous one drops the decode graphs captured for that batch (it waits for
+ * the device to finish their replays first).
  */
 fp_status fp_prefill(fp_layer* layer, const void* x, int32_t B, int32_t P, void* y, void* stream);
 
@@ -135,7 +145,10 @@ fp_status fp_decode_steps(fp_layer* layer, void* x, void* y, int32_t n, void* st
 
 /*
  * Replay decode steps as a captured HIP graph (1, the default) or launch the
- * kernels one by one (0).  Results are identical.
+ * kernels one by one (0).  Results are identical.  Graphs are captured on first
+ * use per (x, y, active batch) for fp_decode_step and per (x, y, n, active batch)
+ * for fp_decode_steps; each cache holds at most 16 graphs and is emptied (after a
+ * device synchronisation) when a new capture would exceed that.
  */
 fp_status fp_set_decode_graph(fp_layer* layer, int32_t enable);
 
@@ -152,7 +165,9 @@ fp_status fp_fill_normal(void* dst, int64_t n, uint64_t seed, int32_t layer, int
                          float mean, float sigma, void* stream);
 
 /*
- * Copy one weight tensor to host memory in its canonical layout (synchronous):
+ * Copy one weight tensor to host memory in its canonical layout (synchronous).
+ * For parity checks of the quantised formats of Sec. 3.2 / Table A.1 (INT8 per
+ * channel, INT4 group-128) against an independent implementation:
  *  bf16:  codes = bf16 [N, K] (scales, zeros unused, may be NULL)
  *  int8:  codes = int8 [N, K], scales = fp16 [N]
  *  int4:  codes = int32 [N, K/8] with nibble j of word w holding column 8w+j,
@@ -165,7 +180,9 @@ fp_status fp_export_weight(fp_layer* layer, int32_t l, int32_t tensor, void* cod
                            void* zeros);
 
 /*
- * Copy layer l's KV cache for the active batch to host memory (synchronous):
+ * Copy layer l's KV cache (the cache that keeps per-token decode cost constant,
+ * Sec. 5.3; int8 per Table A.1's KV-cache quantisation) for the active batch to
+ * host memory (synchronous).  FP_ERR_STATE before a prefill:
  * k, v: [B, n_kv_heads, max_seq, head_dim] of bf16 or int8; k_scales, v_scales:
  * fp16 [B, n_kv_heads, max_seq] (int8 cache only, else may be NULL).
  */
@@ -217,10 +234,18 @@ fp_status fp_profile_prefill(fp_layer* layer, const void* x, int32_t B, int32_t 
 fp_status fp_profile_decode_step(fp_layer* layer, const void* x, void* y, void* stream,
                                  fp_kernel_time* out, int32_t cap, int32_t* count);
 
-/* Bytes of device memory held for weights, KV cache and workspace. */
+/*
+ * Bytes of device memory the handle holds for weights (W), KV cache and workspace
+ * (the activations A of the memory breakdown mem_base = W + A, Sec. 5.2).  On an
+ * unbacked handle: the bytes a real handle of the same shape and formats holds.
+ * Weight bytes count the fragment-major codes (K padded to a whole 1 KiB block
+ * row-slice), the fp16 scales and zeros, the packed int4 scale/zero words and the
+ * bf16 norm gains.  Any output pointer may be NULL.
+ */
 fp_status fp_memory_bytes(const fp_layer* layer, size_t* weights, size_t* kv, size_t* workspace);
 
-/* Current position (tokens in the cache) and active batch of the handle. */
+/* Current position (tokens in the cache, Sec. 5.3) and active batch of the handle;
+ * both 0 before the first prefill.  Any output pointer may be NULL. */
 fp_status fp_get_position(const fp_layer* layer, int32_t* pos, int32_t* batch);
 
 const char* fp_status_str(fp_status status);

@@ -162,8 +162,12 @@ struct fp_layer {
     float* dump = nullptr;
     uint16_t* ldump = nullptr;      // per-layer outputs [n_layers, B, T, hidden] (debug)
     hipStream_t cap_stream = nullptr;
-    std::map<std::pair<const void*, void*>, hipGraphExec_t> graphs;
-    std::map<std::tuple<void*, void*, int>, hipGraphExec_t> mgraphs;   // fp_decode_steps: (x, y, n)
+    // Captured decode graphs.  A capture bakes in the buffers and everything that depends
+    // on the active batch (grids, split factors, the single-sequence or batch schedule,
+    // the rows written), so both caches are keyed by the batch too, and a prefill that
+    // changes the batch drops them.  At most GRAPH_CACHE_MAX entries each.
+    std::map<std::tuple<const void*, void*, int>, hipGraphExec_t> graphs;     // (x, y, B)
+    std::map<std::tuple<void*, void*, int, int>, hipGraphExec_t> mgraphs;     // (x, y, n, B)
     Prof prof;
     size_t bytes_w = 0, bytes_kv = 0, bytes_ws = 0;
     std::vector<void*> allocs;
@@ -173,6 +177,11 @@ namespace {
 
 fp_status dev_alloc(fp_layer* h, void** p, size_t bytes, size_t* counter) {
     if (bytes == 0) bytes = 256;
+    if (h->unbacked) {               // validation-only handle: count the bytes, allocate nothing
+        *p = nullptr;
+        *counter += bytes;
+        return FP_OK;
+    }
     hipError_t e = hipMalloc(p, bytes);
     if (e != hipSuccess) {
         *p = nullptr;
@@ -192,11 +201,21 @@ fp_status alloc_t(fp_layer* h, T** p, size_t count, size_t* counter) {
     return st;
 }
 
-void free_all(fp_layer* h) {
+constexpr size_t GRAPH_CACHE_MAX = 16;
+
+// Destroy every captured decode graph.  A replay may still be in flight on some stream,
+// so the device is synchronised first (only when there is something to destroy).
+void drop_graphs(fp_layer* h) {
+    if (h->graphs.empty() && h->mgraphs.empty()) return;
+    (void)hipDeviceSynchronize();
     for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
     h->graphs.clear();
     for (auto& kv : h->mgraphs) (void)hipGraphExecDestroy(kv.second);
     h->mgraphs.clear();
+}
+
+void free_all(fp_layer* h) {
+    drop_graphs(h);
     if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
     h->cap_stream = nullptr;
     for (void* p : h->allocs) (void)hipFree(p);
@@ -706,6 +725,81 @@ const char* fp_status_str(fp_status s) {
 
 const char* fp_last_error(void) { return g_err.c_str(); }
 
+// Allocate the handle's weights, KV cache and workspace (an unbacked handle only counts
+// the bytes: fp_memory_bytes then reports what a real handle of the shape holds).
+fp_status alloc_storage(fp_layer* h) {
+    const fp_shape& s = h->s;
+    const int kvq = h->kvq;
+    fp_status st;
+    const int H = s.hidden, F = s.ffn;
+    h->L.resize(s.n_layers);
+    for (auto& W : h->L) {
+        if ((st = alloc_t(h, &W.attn_norm, H, &h->bytes_w))) return st;
+        if ((st = alloc_t(h, &W.mlp_norm, H, &h->bytes_w))) return st;
+        if ((st = alloc_mat(h, &W.qkv, h->nqkv, H))) return st;
+        if ((st = alloc_mat(h, &W.o, H, h->q_dim))) return st;
+        if ((st = alloc_mat(h, &W.gu, 2 * F, H))) return st;
+        if ((st = alloc_mat(h, &W.down, H, F))) return st;
+    }
+    // KV cache
+    // keys [Bmax, nkv, kv_stride, d]; values in transposed blocks [Bmax, nkv, nblk, d, VT_BLK];
+    // int8 scales [Bmax, nkv, kv_stride]
+    const size_t esz = kvq == FP_KV_INT8 ? 1 : 2;
+    const size_t kvs = (size_t)kv_row_stride(s.max_seq);
+    const size_t kv_bytes = (size_t)s.max_batch * s.n_kv_heads * kvs * s.head_dim * esz;
+    const size_t v_bytes = (size_t)s.max_batch * s.n_kv_heads * vt_blocks(s.max_seq) * VT_BLK * s.head_dim * esz;
+    const size_t sc_elems = (size_t)s.max_batch * s.n_kv_heads * kvs;
+    h->kc.assign(s.n_layers, nullptr);
+    h->vc.assign(s.n_layers, nullptr);
+    h->ksc.assign(s.n_layers, nullptr);
+    h->vsc.assign(s.n_layers, nullptr);
+    for (int l = 0; l < s.n_layers; ++l) {
+        if ((st = dev_alloc(h, &h->kc[l], kv_bytes, &h->bytes_kv))) return st;
+        if ((st = dev_alloc(h, &h->vc[l], v_bytes, &h->bytes_kv))) return st;
+        if (kvq == FP_KV_INT8) {
+            if ((st = alloc_t(h, &h->ksc[l], sc_elems, &h->bytes_kv))) return st;
+            if ((st = alloc_t(h, &h->vsc[l], sc_elems, &h->bytes_kv))) return st;
+        }
+    }
+    // workspace
+    const size_t Mmax = std::max(act_elems(h), (size_t)s.max_batch);
+    const int ncol = std::max({h->nqkv, H, 2 * F});
+    if ((st = alloc_t(h, &h->act_in, Mmax * H, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->act_o, Mmax * h->q_dim, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->act_f, Mmax * F, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->hbuf, Mmax * H, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->xbuf, Mmax * H, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->qkv32, Mmax * h->nqkv, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->q32, Mmax * h->q_dim, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->part2, (size_t)KSMAX * s.max_batch * 2 * F, &h->bytes_ws))) return st;
+    {
+        // the largest split-K partial buffer any prefill size up to Mmax asks for (the split
+        // factor depends on the number of 256-row tiles, so the worst case is at a whole tile)
+        size_t pp = 0;
+        const int Mp = (int)act_elems(h);
+        for (int tm = 1; (int64_t)(tm - 1) * 256 < Mp; ++tm) {
+            const int M = std::min(tm * 256, Mp);
+            int kr;
+            const int ko = prefill_split(h, M, H, h->q_dim, 0, &kr);
+            const int kg = prefill_split(h, M, 2 * F, H, F, &kr);
+            const int kd = prefill_split(h, M, H, F, 0, &kr);
+            pp = std::max({pp, (size_t)(ko > 1 ? ko : 0) * M * H, (size_t)(kg > 1 ? kg : 0) * M * 2 * F,
+                           (size_t)(kd > 1 ? kd : 0) * M * H});
+        }
+        if (pp > 0 && (st = alloc_t(h, &h->ppart, pp, &h->bytes_ws))) return st;
+    }
+    const size_t nch = attn_decode_max_splits(s.max_seq);
+    if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 4), &h->bytes_ws)))
+        return st;
+    if ((st = alloc_t(h, &h->d_pos, 1, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->ssq, (size_t)s.max_batch * resid_ssq_blocks(H), &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->cos_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->sin_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return st;
+
+    return FP_OK;
+}
+
 static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_quant kvq, uint64_t seed,
                              fp_layer** out, bool unbacked) {
     if (!out) return fail(FP_ERR_INVALID_ARG, "out is NULL");
@@ -724,6 +818,10 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     h->kv_dim = s.n_kv_heads * s.head_dim;
     h->nqkv = h->q_dim + 2 * h->kv_dim;
     if (unbacked) {
+        if ((st = alloc_storage(h))) {   // counts bytes only
+            delete h;
+            return st;
+        }
         *out = h;
         return FP_OK;
     }
@@ -749,73 +847,15 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
         delete h;
         return code;
     };
+    if ((st = alloc_storage(h))) return bail(st);
     const int H = s.hidden, F = s.ffn;
-    h->L.resize(s.n_layers);
-    size_t maxrows = 0;
-    for (auto& W : h->L) {
-        if ((st = alloc_t(h, &W.attn_norm, H, &h->bytes_w))) return bail(st);
-        if ((st = alloc_t(h, &W.mlp_norm, H, &h->bytes_w))) return bail(st);
-        if ((st = alloc_mat(h, &W.qkv, h->nqkv, H))) return bail(st);
-        if ((st = alloc_mat(h, &W.o, H, h->q_dim))) return bail(st);
-        if ((st = alloc_mat(h, &W.gu, 2 * F, H))) return bail(st);
-        if ((st = alloc_mat(h, &W.down, H, F))) return bail(st);
-    }
-    maxrows = std::max<size_t>({(size_t)h->q_dim * H, (size_t)H * h->q_dim, (size_t)F * H, (size_t)H * F});
-    // KV cache
-    // keys [Bmax, nkv, kv_stride, d]; values in transposed blocks [Bmax, nkv, nblk, d, VT_BLK];
-    // int8 scales [Bmax, nkv, kv_stride]
+    const size_t maxrows = std::max<size_t>({(size_t)h->q_dim * H, (size_t)H * h->q_dim, (size_t)F * H,
+                                             (size_t)H * F});
     const size_t esz = kvq == FP_KV_INT8 ? 1 : 2;
     const size_t kvs = (size_t)kv_row_stride(s.max_seq);
     const size_t kv_bytes = (size_t)s.max_batch * s.n_kv_heads * kvs * s.head_dim * esz;
     const size_t v_bytes = (size_t)s.max_batch * s.n_kv_heads * vt_blocks(s.max_seq) * VT_BLK * s.head_dim * esz;
     const size_t sc_elems = (size_t)s.max_batch * s.n_kv_heads * kvs;
-    h->kc.assign(s.n_layers, nullptr);
-    h->vc.assign(s.n_layers, nullptr);
-    h->ksc.assign(s.n_layers, nullptr);
-    h->vsc.assign(s.n_layers, nullptr);
-    for (int l = 0; l < s.n_layers; ++l) {
-        if ((st = dev_alloc(h, &h->kc[l], kv_bytes, &h->bytes_kv))) return bail(st);
-        if ((st = dev_alloc(h, &h->vc[l], v_bytes, &h->bytes_kv))) return bail(st);
-        if (kvq == FP_KV_INT8) {
-            if ((st = alloc_t(h, &h->ksc[l], sc_elems, &h->bytes_kv))) return bail(st);
-            if ((st = alloc_t(h, &h->vsc[l], sc_elems, &h->bytes_kv))) return bail(st);
-        }
-    }
-    // workspace
-    const size_t Mmax = std::max(act_elems(h), (size_t)s.max_batch);
-    const int ncol = std::max({h->nqkv, H, 2 * F});
-    if ((st = alloc_t(h, &h->act_in, Mmax * H, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->act_o, Mmax * h->q_dim, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->act_f, Mmax * F, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->hbuf, Mmax * H, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->xbuf, Mmax * H, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->qkv32, Mmax * h->nqkv, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->q32, Mmax * h->q_dim, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->part2, (size_t)KSMAX * s.max_batch * 2 * F, &h->bytes_ws))) return bail(st);
-    {
-        // the largest split-K partial buffer any prefill size up to Mmax asks for (the split
-        // factor depends on the number of 256-row tiles, so the worst case is at a whole tile)
-        size_t pp = 0;
-        const int Mp = (int)act_elems(h);
-        for (int tm = 1; (int64_t)(tm - 1) * 256 < Mp; ++tm) {
-            const int M = std::min(tm * 256, Mp);
-            int kr;
-            const int ko = prefill_split(h, M, H, h->q_dim, 0, &kr);
-            const int kg = prefill_split(h, M, 2 * F, H, F, &kr);
-            const int kd = prefill_split(h, M, H, F, 0, &kr);
-            pp = std::max({pp, (size_t)(ko > 1 ? ko : 0) * M * H, (size_t)(kg > 1 ? kg : 0) * M * 2 * F,
-                           (size_t)(kd > 1 ? kd : 0) * M * H});
-        }
-        if (pp > 0 && (st = alloc_t(h, &h->ppart, pp, &h->bytes_ws))) return bail(st);
-    }
-    const size_t nch = attn_decode_max_splits(s.max_seq);
-    if ((st = alloc_t(h, &h->attn_ws, (size_t)s.max_batch * s.n_heads * nch * (s.head_dim + 4), &h->bytes_ws)))
-        return bail(st);
-    if ((st = alloc_t(h, &h->d_pos, 1, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->ssq, (size_t)s.max_batch * resid_ssq_blocks(H), &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->cos_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return bail(st);
-    if ((st = alloc_t(h, &h->sin_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return bail(st);
 
     // rotary tables: angle(p, i) = p * theta^(-2i/d) in double, rounded once to float
     {
@@ -906,6 +946,7 @@ fp_status fp_prefill(fp_layer* h, const void* x, int32_t B, int32_t P, void* y, 
     const size_t bytes = (size_t)B * P * h->s.hidden * 2;
     if (overlap(x, bytes, y, bytes)) return fail(FP_ERR_INVALID_ARG, "x and y overlap");
     if (!h->unbacked) {
+        if (B != h->B) drop_graphs(h);   // captured for another batch: never valid again
         fp_status st = enqueue_prefill(h, (const uint16_t*)x, B, P, (uint16_t*)y, (hipStream_t)stream);
         if (st) {
             h->prefilled = false;
@@ -929,9 +970,10 @@ fp_status fp_decode_step(fp_layer* h, const void* x, void* y, void* stream) {
         hipStream_t st = (hipStream_t)stream;
         fp_status rc;
         if (h->use_graph && !h->dump && !h->ldump) {
-            auto key = std::make_pair(x, y);
+            const auto key = std::make_tuple(x, y, h->B);
             auto it = h->graphs.find(key);
             if (it == h->graphs.end()) {
+                if (h->graphs.size() >= GRAPH_CACHE_MAX) drop_graphs(h);
                 hipGraph_t g = nullptr;
                 hipGraphExec_t ge = nullptr;
                 HIPCHK(hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal));
@@ -979,9 +1021,10 @@ fp_status fp_decode_steps(fp_layer* h, void* x, void* y, int32_t n, void* stream
         hipStream_t st = (hipStream_t)stream;
         fp_status rc;
         if (h->use_graph && !h->dump && !h->ldump) {
-            const auto key = std::make_tuple(x, y, (int)n);
+            const auto key = std::make_tuple(x, y, (int)n, h->B);
             auto it = h->mgraphs.find(key);
             if (it == h->mgraphs.end()) {
+                if (h->mgraphs.size() >= GRAPH_CACHE_MAX) drop_graphs(h);
                 hipGraph_t g = nullptr;
                 hipGraphExec_t ge = nullptr;
                 HIPCHK(hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal));

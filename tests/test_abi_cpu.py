@@ -135,3 +135,73 @@ def test_last_error_message_is_set():
     h = ctypes.c_void_p()
     assert L.fp_layer_create_unbacked(ctypes.byref(s), 0, 0, 0, ctypes.byref(h)) == -1
     assert b"multiples of 16" in L.fp_last_error()
+
+
+def _planned_bytes(shape, wq, kvq):
+    fp = Fingerprint(shape, wq, kvq, unbacked=True)
+    try:
+        return fp.memory_bytes()
+    finally:
+        fp.close()
+
+
+def _hand_weight_bytes(s, wq):
+    """Fused matrices [q;k;v], o, [gate;up], down stored fragment-major: 1 KiB per 16 rows
+    and one k-step of 32 bf16 / 64 int8 / 128 int4 inputs (k padded to whole steps);
+    int8 adds an fp16 scale per row; int4 an fp16 scale, an fp16 zero and a packed u32
+    scale|zero word per (row, group of 128).  Plus two bf16 gains of hidden."""
+    ks = {"bf16": 32, "int8": 64, "int4": 128}[wq]
+    qd, kd = s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+    mats = [(qd + 2 * kd, s.hidden), (s.hidden, qd), (2 * s.ffn, s.hidden), (s.hidden, s.ffn)]
+    per_layer = 2 * s.hidden * 2
+    for N, K in mats:
+        per_layer += (N // 16) * (-(-K // ks)) * 1024
+        if wq == "int8":
+            per_layer += N * 2
+        elif wq == "int4":
+            per_layer += N * (K // 128) * (2 + 2 + 4)
+    return s.n_layers * per_layer
+
+
+def _hand_kv_bytes(s, kvq):
+    """Keys [B, nkv, R, d] and values in 32-position blocks [B, nkv, R/32, d, 32] with
+    R = max_seq rounded up to 32; int8 adds fp16 key and value scales [B, nkv, R]."""
+    R = -(-s.max_seq // 32) * 32
+    esz = 1 if kvq == "int8" else 2
+    per_layer = 2 * s.max_batch * s.n_kv_heads * R * s.head_dim * esz
+    if kvq == "int8":
+        per_layer += 2 * s.max_batch * s.n_kv_heads * R * 2
+    return s.n_layers * per_layer
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama2-7b-bf16", "llama2-7b-int8", "llama2-13b-int4",
+                                  "llama2-70b-tp8-int4"])
+def test_memory_bytes_match_the_storage_layout(name):
+    c = CONFIGS[name]
+    s = c["shape"]
+    w, kv, ws = _planned_bytes(s, c["wq"], c["kvq"])
+    assert w == _hand_weight_bytes(s, c["wq"])
+    assert kv == _hand_kv_bytes(s, c["kvq"])
+    # workspace: at least the prefill activations (x, h, normalised input: 3 x [B*P, hidden]
+    # bf16) and the fp32 q|k|v of the prompt
+    M = s.max_batch * s.max_prompt
+    qkv = s.n_heads * s.head_dim + 2 * s.n_kv_heads * s.head_dim
+    assert ws >= 3 * M * s.hidden * 2 + M * qkv * 4
+
+
+def test_memory_bytes_scale_with_weight_format_and_layers():
+    """Sec. 3.2: INT8 weights halve and INT4 weights quarter the memory of 16-bit weights
+    (plus their scales: 2 bytes per row for int8, 8 bytes per 128 inputs for int4), and
+    the footprint grows linearly with the number of hidden layers (Sec. 5, Fig. 7)."""
+    import dataclasses
+    s = CONFIGS["llama2-7b-bf16"]["shape"]
+    wb = _planned_bytes(s, "bf16", "bf16")[0]
+    w8 = _planned_bytes(s, "int8", "bf16")[0]
+    w4 = _planned_bytes(s, "int4", "bf16")[0]
+    gains = s.n_layers * 2 * s.hidden * 2
+    assert abs((w8 - gains) / (wb - gains) - 0.5) < 1e-3
+    assert abs((w4 - gains) / (wb - gains) - (0.25 + 8 / 256)) < 1e-3
+    one = [_planned_bytes(dataclasses.replace(s, n_layers=n), "int4", "int8") for n in (1, 2, 3)]
+    for i in range(2):       # weights and KV are linear; the workspace does not grow with layers
+        assert one[2][i] - one[1][i] == one[1][i] - one[0][i]
+    assert one[0][2] == one[1][2] == one[2][2]

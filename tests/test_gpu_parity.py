@@ -251,3 +251,106 @@ def test_kv_codes_end_to_end_within_one():
         log(f"kv code mismatch rate {rate:.2e}, max |delta| {dlt.max()}")
         assert dlt.max() <= 1
         assert rate <= 1e-3
+
+
+def test_reprefill_with_another_batch_drops_stale_graphs():
+    """Decode graphs are captured per (x, y, batch).  Prefill B = 3, graph decode steps,
+    then prefill B = 2 and B = 1 on the same handle and the same x / y buffers (sized for
+    the largest batch, with sentinel rows past the active batch): every decode output
+    equals a fresh handle's bit for bit, and the rows past the active batch are never
+    written."""
+    import torch
+    from paper_2501_13111_amd import Fingerprint, fill_normal
+    shape = Shape(2, 256, 4, 2, 64, 384, 3, 20, 40)
+    H, P, Bmax = 256, 20, 3
+    sentinel = torch.full((Bmax * H,), 7.0, dtype=torch.bfloat16, device="cuda")
+
+    def prompt(B):
+        x = torch.empty(B * P * H, dtype=torch.bfloat16, device="cuda")
+        fill_normal(x, 8, -1, 15, 0.0, 1.0)
+        return x
+
+    def fresh(B, steps):
+        with Fingerprint(shape, "int8", "int8", seed=8) as fp:
+            x = prompt(B)
+            y = torch.empty_like(x)
+            fp.prefill(x, y, B, P)
+            a = y.view(B, P, H)[:, -1, :].contiguous()
+            b = torch.empty_like(a)
+            outs = []
+            for _ in range(steps):
+                fp.decode_step(a, b)
+                outs.append(b.clone())
+                a, b = b, a
+            torch.cuda.synchronize()
+            return outs
+
+    with Fingerprint(shape, "int8", "int8", seed=8) as fp:
+        xa = sentinel.clone()
+        xb = sentinel.clone()
+        stream = torch.cuda.current_stream().cuda_stream
+        for B in (3, 2, 1, 2):
+            log(f"re-prefill B={B}")
+            x = prompt(B)
+            y = torch.empty_like(x)
+            fp.prefill(x, y, B, P)
+            xa.copy_(sentinel)
+            xb.copy_(sentinel)
+            xa[:B * H].copy_(y.view(B, P, H)[:, -1, :].reshape(-1))
+            got = []
+            for st in range(3):
+                src, dst = (xa, xb) if st % 2 == 0 else (xb, xa)
+                fp.decode_ptr(src.data_ptr(), dst.data_ptr(), stream)
+                got.append(dst[:B * H].clone())
+            # steps 4 and 5 in one call: step 4 reads xb and writes xa, step 5 writes xb
+            fp.decode_steps_ptr(xb.data_ptr(), xa.data_ptr(), 2, stream)
+            got.append(xb[:B * H].clone())
+            torch.cuda.synchronize()
+            want = fresh(B, 5)
+            for st, g in enumerate(got[:3]):
+                assert torch.equal(g.view(torch.int16), want[st].view(-1).view(torch.int16)), (B, st)
+            assert torch.equal(got[3].view(torch.int16), want[4].view(-1).view(torch.int16)), B
+            for buf in (xa, xb):
+                assert torch.equal(buf[B * H:].view(torch.int16), sentinel[B * H:].view(torch.int16)), B
+
+
+@pytest.mark.parametrize("kvq", ["bf16", "int8"])
+def test_single_sequence_decode_steps_match_single_steps(kvq):
+    """One sequence (the single-sequence schedule the 7B bf16 workload runs): n steps in
+    one call equal n calls of fp_decode_step bit for bit, graph on and off, with the last
+    call ending exactly at the cache capacity."""
+    import torch
+    from paper_2501_13111_amd import Fingerprint, fill_normal
+    shape = Shape(2, 512, 4, 4, 128, 640, 1, 33, 42)
+    P = 33
+
+    def start(fp):
+        x = torch.empty(P * 512, dtype=torch.bfloat16, device="cuda")
+        fill_normal(x, 9, -1, 15, 0.0, 1.0)
+        y = torch.empty_like(x)
+        fp.prefill(x, y, 1, P)
+        return y.view(1, P, 512)[:, -1, :].contiguous()
+
+    ref = []
+    with Fingerprint(shape, "bf16", kvq, seed=9) as fp:
+        fp.set_decode_graph(False)
+        a = start(fp)
+        b = torch.empty_like(a)
+        for _ in range(9):
+            fp.decode_step(a, b)
+            a, b = b, a
+            ref.append(a.clone())
+    for graph in (True, False):
+        with Fingerprint(shape, "bf16", kvq, seed=9) as fp:
+            fp.set_decode_graph(graph)
+            x = start(fp)
+            y = torch.empty_like(x)
+            done = 0
+            for n in (3, 2, 4):               # 9 steps: the last call ends at max_seq = 42
+                out = fp.decode_steps(x, y, n)
+                done += n
+                torch.cuda.synchronize()
+                assert torch.equal(out.view(torch.int16), ref[done - 1].view(torch.int16)), (graph, n)
+                if out is y:
+                    x, y = y, x
+            assert fp.position() == (42, 1)
