@@ -55,9 +55,30 @@ def test_prefill_flops_by_hand():
 
 
 def test_traffic_is_reported_only_for_the_sources_it_was_measured_on(monkeypatch):
-    h = bench.skinny_src_hash()
-    monkeypatch.setattr(bench, "SKINNY_TRAFFIC", {"w": {"src": h, "bytes_per_launch": 123}})
-    assert bench.skinny_traffic("w") == 123
-    assert bench.skinny_traffic("other") is None
-    monkeypatch.setattr(bench, "SKINNY_TRAFFIC", {"w": {"src": "0" * 16, "bytes_per_launch": 123}})
-    assert bench.skinny_traffic("w") is None
+    h = bench.src_hash("prefill_gemm")
+    assert h != bench.src_hash("decode_proj")
+    monkeypatch.setattr(bench, "TRAFFIC", {("prefill_gemm", "w"): {"src": h, "bytes_per_launch": 123}})
+    assert bench.measured_traffic("prefill_gemm", "w") == 123
+    assert bench.measured_traffic("prefill_gemm", "other") is None
+    assert bench.measured_traffic("decode_proj", "w") is None
+    monkeypatch.setattr(bench, "TRAFFIC", {("prefill_gemm", "w"): {"src": "0" * 16, "bytes_per_launch": 123}})
+    assert bench.measured_traffic("prefill_gemm", "w") is None
+
+
+def test_headline_is_the_largest_single_gpu_workload():
+    head, names = bench.workload_names()
+    assert head == "llama2-70b-tp8-int4" and names[0] == head and len(names) == len(CONFIGS)
+    big = max(CONFIGS, key=lambda n: (CONFIGS[n]["B"] * CONFIGS[n]["P"], CONFIGS[n]["shape"].hidden))
+    assert big == head
+
+
+def test_cpu_baseline_sample_reports_the_host(monkeypatch):
+    """The CPU baseline times the oracle's float32 mode on a one-layer, one-sequence
+    sample and scales the rate to the workload's layer count."""
+    import dataclasses
+    from fpgen.workloads import Shape
+    cfg = dict(shape=Shape(3, 128, 2, 2, 64, 256, 4, 8, 12), wq="int8", kvq="int8", B=4, P=8, S=4)
+    r = bench.cpu_baseline(cfg, 0, 0.01)
+    assert r["kind"] == "oracle" and r["unit"] == "tokens/s" and r["value"] > 0
+    assert r["cores"] >= 1 and r["nproc"] >= 1 and isinstance(r["cpu_model"], str)
+    assert "1 of 3 layers" in r["sample"] and "float32" in r["sample"]
