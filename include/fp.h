@@ -144,6 +144,21 @@ fp_status fp_decode_step(fp_layer* layer, const void* x, void* y, void* stream);
 fp_status fp_decode_steps(fp_layer* layer, void* x, void* y, int32_t n, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): one decode step exactly as
+ * fp_decode_step computes it (same kernels, same results bit for bit), launched
+ * kernel by kernel with no graph instantiation and no allocation of any kind.  The
+ * step's split-K partials, attention partials and row-norm sums live in a static
+ * 64 MiB device region per GPU (held from the first call on that GPU until the
+ * process ends) instead of the handle's workspace.  Every call on one GPU shares that
+ * GPU's region: calls that overlap on one GPU (other streams, other threads, other
+ * handles) race, so serialise them.  FP_ERR_CAPACITY, with nothing launched, when
+ * the step at the active batch needs more than 64 MiB of scratch (the message gives
+ * the size); otherwise the same argument and state errors as fp_decode_step.
+ */
+fp_status fp_decode_step_noalloc(fp_layer* layer, const void* x, void* y, void* stream);
+
+/*
  * Replay decode steps as a captured HIP graph (1, the default) or launch the
  * kernels one by one (0).  Results are identical.  Graphs are captured on first
  * use per (x, y, active batch) for fp_decode_step and per (x, y, n, active batch)

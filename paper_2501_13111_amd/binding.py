@@ -72,6 +72,7 @@ def load(path: str | None = None):
         "fp_prefill": [vp, vp, i32, i32, vp, vp],
         "fp_decode_step": [vp, vp, vp, vp],
         "fp_decode_steps": [vp, vp, vp, i32, vp],
+        "fp_decode_step_noalloc": [vp, vp, vp, vp],
         "fp_set_decode_graph": [vp, i32],
         "fp_fill_normal": [vp, i64, u64, i32, i32, ctypes.c_float, ctypes.c_float, vp],
         "fp_export_weight": [vp, i32, i32, vp, vp, vp],
@@ -180,6 +181,14 @@ class Fingerprint:
         xp = _dev_ptr(x, numel=self.B * H, name="x")
         yp = _dev_ptr(y, numel=self.B * H, name="y")
         _check(load().fp_decode_step(self._h, xp, yp, _stream(stream)), "fp_decode_step")
+
+    def decode_step_noalloc(self, x, y, stream=None):
+        """fp_decode_step_noalloc: one eager decode step whose scratch lives in the library's
+        static per-GPU region (no allocation of any kind)."""
+        H = self.shape.hidden
+        xp = _dev_ptr(x, numel=self.B * H, name="x")
+        yp = _dev_ptr(y, numel=self.B * H, name="y")
+        _check(load().fp_decode_step_noalloc(self._h, xp, yp, _stream(stream)), "fp_decode_step_noalloc")
 
     def decode_steps(self, x, y, n: int, stream=None):
         """n decode steps alternating between x and y (step 1 writes y); returns the

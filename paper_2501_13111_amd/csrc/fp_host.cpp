@@ -319,6 +319,14 @@ struct XIn {
     int att_nsplit = 0, att_kps = 0;
 };
 
+// Split of a single-sequence decode projection: wide matrices (qkv, gate/up) stream
+// faster with twice the workgroups.
+void plan_skinny(const fp_layer* h, const Mat& m, int M, int dual_F, int* ks, int* kr) {
+    const int ncols = dual_F > 0 ? 2 * dual_F : m.N;
+    choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, h->wq, ncols >= SPLIT_WIDE_N ? 2 * TARGET_WG : TARGET_WG, ks,
+                 kr);
+}
+
 fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, const XIn& xin,
                      float* part, int* ks_out, hipStream_t st) {
     SkinnyArgs a{};
@@ -346,10 +354,7 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     a.head_dim = h->s.head_dim;
     a.d_pos = h->d_pos;
     int ks, kr;
-    // wide matrices (qkv, gate/up) stream faster with twice the workgroups
-    const int ncols = dual_F > 0 ? 2 * dual_F : m.N;
-    choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, h->wq, ncols >= SPLIT_WIDE_N ? 2 * TARGET_WG : TARGET_WG, &ks,
-                 &kr);
+    plan_skinny(h, m, M, dual_F, &ks, &kr);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     a.krange = kr;
     HIPCHK(launch_skinny(a, h->wq, ks, st));
@@ -365,21 +370,7 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
 // and the consumer reads back (ks * M * N floats each way, at about 5 TB/s, against a
 // chunk time of the workgroup's weight bytes at about 25 GB/s per compute unit).
 constexpr int NCU = 256;
-fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, float* part,
-                           int* ks_out, hipStream_t st) {
-    SkinnyArgs a{};
-    a.X = X;
-    a.W = m.codes;
-    a.scales = m.scales;
-    a.zeros = m.zeros;
-    a.sz = m.sz;
-    a.M = M;
-    a.N = m.N;
-    a.K = m.K;
-    a.kst = m.kst;
-    a.dual_F = dual_F;
-    a.part = part;
-    a.xf = XF_COPY;
+void plan_skinny_batch(const fp_layer* h, const Mat& m, int M, int dual_F, int* ks_out, int* kr_out) {
     const int KC = skinny_batch_chunk();
     const int nch = (m.K + KC - 1) / KC;
     const int tiles = skinny_batch_tiles(m.N, dual_F, h->wq);
@@ -396,8 +387,27 @@ fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, 
         const double cost = rounds * (p + 2.0) * chunk_s + ksk * split_s;
         if (cost < best - 1e-12) { best = cost; per = p; }
     }
-    a.krange = per * KC;
-    int ks = (nch + per - 1) / per;
+    *kr_out = per * KC;
+    *ks_out = (nch + per - 1) / per;
+}
+
+fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, float* part,
+                           int* ks_out, hipStream_t st) {
+    SkinnyArgs a{};
+    a.X = X;
+    a.W = m.codes;
+    a.scales = m.scales;
+    a.zeros = m.zeros;
+    a.sz = m.sz;
+    a.M = M;
+    a.N = m.N;
+    a.K = m.K;
+    a.kst = m.kst;
+    a.dual_F = dual_F;
+    a.part = part;
+    a.xf = XF_COPY;
+    int ks;
+    plan_skinny_batch(h, m, M, dual_F, &ks, &a.krange);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     HIPCHK(launch_skinny_batch(a, h->wq, ks, st));
     *ks_out = ks;
@@ -705,7 +715,74 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
     return pa < pb + nb && pb < pa + na;
 }
 
+// Floats of the decode step's scratch buffers at batch B: split-K partials of the qkv / o /
+// down projections (part) and of [gate; up] (part2), attention partials and row-norm
+// block sums.  The same split plans the launchers use.
+void decode_scratch_floats(const fp_layer* h, int B, size_t* part, size_t* part2, size_t* att, size_t* ssq) {
+    const fp_shape& s = h->s;
+    const LayerW& W = h->L[0];
+    int kq, ko, kg, kd, kr;
+    if (B == 1) {
+        plan_skinny(h, W.qkv, B, 0, &kq, &kr);
+        plan_skinny(h, W.o, B, 0, &ko, &kr);
+        plan_skinny(h, W.gu, B, s.ffn, &kg, &kr);
+        plan_skinny(h, W.down, B, 0, &kd, &kr);
+    } else {
+        plan_skinny_batch(h, W.qkv, B, 0, &kq, &kr);
+        plan_skinny_batch(h, W.o, B, 0, &ko, &kr);
+        plan_skinny_batch(h, W.gu, B, s.ffn, &kg, &kr);
+        plan_skinny_batch(h, W.down, B, 0, &kd, &kr);
+    }
+    *part = std::max({(size_t)kq * B * h->nqkv, (size_t)ko * B * s.hidden, (size_t)kd * B * s.hidden});
+    *part2 = (size_t)kg * B * 2 * s.ffn;
+    *att = (size_t)B * s.n_heads * attn_decode_max_splits(s.max_seq) * (s.head_dim + 4);
+    *ssq = (size_t)B * resid_ssq_blocks(s.hidden);
+}
+
 }  // namespace
+
+// One decode step, launched kernel by kernel (no graph capture, no allocation), with its
+// scratch buffers carved from the caller-provided device region [scratch, scratch + bytes)
+// instead of the handle's workspace.  FP_ERR_CAPACITY when the step needs more than bytes.
+fp_status fpk::decode_step_scratch(fp_layer* h, const void* x, void* y, hipStream_t st, void* scratch,
+                                   size_t bytes) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (!x || !y) return fail(FP_ERR_INVALID_ARG, "x and y must be device pointers");
+    if (!h->prefilled) return fail(FP_ERR_STATE, "decode step before prefill");
+    if (h->pos >= h->s.max_seq) return fail(FP_ERR_CAPACITY, "position %d reached max_seq %d", h->pos, h->s.max_seq);
+    const size_t xbytes = (size_t)h->B * h->s.hidden * 2;
+    if (overlap(x, xbytes, y, xbytes)) return fail(FP_ERR_INVALID_ARG, "x and y overlap");
+    size_t np, np2, na, ns;
+    decode_scratch_floats(h, h->B, &np, &np2, &na, &ns);
+    auto up = [](size_t floats) { return (floats * sizeof(float) + 255) / 256 * 256; };
+    const size_t need = up(np) + up(np2) + up(na) + up(ns);
+    if (need > bytes)
+        return fail(FP_ERR_CAPACITY, "decode step at batch %d needs %zu bytes of scratch, the static region holds %zu",
+                    h->B, need, bytes);
+    if (!h->unbacked) {
+        if (!scratch) return fail(FP_ERR_INVALID_ARG, "scratch region is NULL");
+        char* p = (char*)scratch;
+        float* part = (float*)p;
+        float* part2 = (float*)(p += up(np));
+        float* att = (float*)(p += up(np2));
+        float* ssq = (float*)(p += up(na));
+        std::swap(h->part, part);
+        std::swap(h->part2, part2);
+        std::swap(h->attn_ws, att);
+        std::swap(h->ssq, ssq);
+        const fp_status rc = enqueue_decode(h, (const uint16_t*)x, (uint16_t*)y, st);
+        std::swap(h->part, part);
+        std::swap(h->part2, part2);
+        std::swap(h->attn_ws, att);
+        std::swap(h->ssq, ssq);
+        if (rc) return rc;
+    }
+    h->pos += 1;
+    return FP_OK;
+}
+
+fp_status fpk::report_error(fp_status s, const char* msg) { return fail(s, "%s", msg); }
+bool fpk::layer_unbacked(const fp_layer* h) { return h->unbacked; }
 
 // ============================================================================ C ABI
 extern "C" {

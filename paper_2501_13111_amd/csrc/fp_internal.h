@@ -1,5 +1,7 @@
 // Internal interface between the host runtime (fp_host.cpp) and the kernels.
 #pragma once
+#include "../../include/fp.h"
+
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -211,5 +213,12 @@ void attn_decode_split(int max_seq, int B, int nkv, int group, int* nsplit, int*
 bool attn_decode_supported(int d, int group);
 hipError_t launch_attn_decode(const AttnDecArgs& a, int B, hipStream_t st);
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st);
+
+// Host runtime hooks for the allocation-free decode step (noalloc.hip): one eager decode
+// step whose scratch buffers live in [scratch, scratch + bytes), and setting the
+// thread's last-error message.
+fp_status decode_step_scratch(fp_layer* h, const void* x, void* y, hipStream_t st, void* scratch, size_t bytes);
+fp_status report_error(fp_status s, const char* msg);
+bool layer_unbacked(const fp_layer* h);
 
 }  // namespace fpk
