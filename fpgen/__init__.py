@@ -34,6 +34,9 @@ MASK64 = (1 << 64) - 1
 # tensor ids used throughout (the C ABI uses the same numbering)
 T_ATTN_NORM, T_Q, T_K, T_V, T_O, T_MLP_NORM, T_GATE, T_UP, T_DOWN = range(9)
 T_INPUT = 15
+# the blocks outside the hidden layers (layer id -1): token embedding [vocab, hidden],
+# final norm gain [hidden], LM head [vocab, hidden]
+T_EMBED, T_FINAL_NORM, T_LM_HEAD = 16, 17, 18
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SO = os.path.join(_HERE, "_fpgen.so")
@@ -170,3 +173,17 @@ def prompt(seed: int, B: int, P: int, H: int, b_start: int = 0, b_count: int | N
     n = b_count * P * H
     bits = bf16_bits(seed, -1, T_INPUT, n, 0.0, 1.0, start=b_start * P * H)
     return bits_to_f32(bits).reshape(b_count, P, H)
+
+
+T_TOKENS = 19
+
+
+def token_ids(seed: int, n: int, vocab: int, start: int = 0) -> np.ndarray:
+    """Synthetic prompt token ids, uniform over [0, vocab): element i is the top 32 bits of
+    word mix64(key(seed, -1, 19) + G*(i+1)), times vocab, over 2^32 (int32 [n])."""
+    k = np.uint64(key(seed, -1, T_TOKENS))
+    i = np.arange(start, start + n, dtype=np.uint64)
+    with np.errstate(over="ignore"):
+        w = mix64_np(k + np.uint64(GAMMA) * (i + np.uint64(1)))
+    hi = (w >> np.uint64(32)).astype(np.uint64)
+    return ((hi * np.uint64(vocab)) >> np.uint64(32)).astype(np.int32)

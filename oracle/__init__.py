@@ -27,4 +27,4 @@ from .numerics import bf16_round, fp16_round, rint_even  # noqa: F401
 from .quant import (quant_int8_channel, dequant_int8_channel, quant_int4_g128,  # noqa: F401
                     dequant_int4_g128, pack_int4, unpack_int4, quant_kv_int8)
 from .layer import (Shape, Fingerprint, rope_tables, apply_rope, rmsnorm, silu,  # noqa: F401
-                    attention, CONFIGS)
+                    attention, argmax_first, CONFIGS)

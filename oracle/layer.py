@@ -23,7 +23,19 @@ LLMs it profiles) is, per layer, with x bf16 [T, H]:
     y = bf16(h + a W_down^T)
 Attention always reads K/V back from the cache (so KV-cached decode equals
 full recompute).  Decode feeds the last layer's output at the last position
-back as the next input; there is no final norm or LM head.
+back as the next input.
+
+With shape.vocab > 0 the fingerprint also keeps the blocks outside the hidden
+layers (Sec. 5.1, Fig. 2: embedding, normalisation layer, LM head), and a
+dummy request (Sec. 5.3) runs on token ids:
+    x = E[ids]                                            (embedding gather)
+    y = layers(x)                                         (prefill or decode step)
+    logits = bf16(rmsnorm(y_last) * g_final) W_lm^T       (fp64 here)
+    next id = argmax(logits), the lowest id among equal maxima (greedy)
+The embedding, final gain and LM head stay 16-bit (bf16) under every weight
+format: the weight-only quantisation applies to the hidden layers' projections.
+A request with output length n runs the prefill (which yields the first token)
+and n decode steps, each consuming the previous token.
 
 Pins (tests/test_oracle_layer.py): RMSNorm against torch's rms_norm and the
 closed form for constant rows; RoPE against complex multiplication and its
@@ -142,6 +154,10 @@ class Fingerprint:
         self.cos, self.sin = rope_tables(s.max_seq, s.head_dim, s.rope_theta)
         self.layers = [self._make_layer(l, weights) for l in range(s.n_layers)]
         self.pos = None
+        if s.vocab > 0:
+            self.embed_table = fpgen.weight(seed, -1, fpgen.T_EMBED, (s.vocab, s.hidden))
+            self.final_norm = fpgen.gain(seed, -1, fpgen.T_FINAL_NORM, s.hidden)
+            self.lm_head = fpgen.weight(seed, -1, fpgen.T_LM_HEAD, (s.vocab, s.hidden))
 
     # weights -------------------------------------------------------------
     def _make_layer(self, l, weights):
@@ -286,3 +302,38 @@ class Fingerprint:
             ys.append(y)
             xin = y
         return y0, ys
+
+    # ------------------------------------------------------------ other blocks
+    def embed(self, ids):
+        """Embedding gather: ids (int) [...] -> rows of the table [..., H] (bf16 values)."""
+        ids = np.asarray(ids)
+        assert self.s.vocab > 0 and ids.min() >= 0 and ids.max() < self.s.vocab
+        return self.embed_table[ids]
+
+    def head(self, y):
+        """Final RMSNorm and LM head of the last hidden states y [B, H]: returns
+        (logits [B, vocab] in the arithmetic type, next ids [B] by greedy argmax)."""
+        A = self.acc
+        yn = bf16_round(rmsnorm(y, self.final_norm, self.s.rms_eps, A)).astype(A)
+        logits = yn @ self.lm_head.astype(A).T
+        return logits, argmax_first(logits)
+
+    def generate(self, ids, n_out, teacher=None):
+        """One dummy request on token ids [B, P]: the prefill yields token 0, then n_out
+        decode steps each consume the previous token (or teacher[i - 1] when given) and
+        yield tokens 1..n_out.  Returns (tokens [n_out + 1, B], logits [n_out + 1, B, V])."""
+        ids = np.asarray(ids)
+        y = self.prefill(self.embed(ids))
+        lg, tok = self.head(y[:, -1, :])
+        toks, logits = [tok], [lg]
+        for i in range(n_out):
+            inp = tok if teacher is None else np.asarray(teacher[i])
+            lg, tok = self.head(self.decode(self.embed(inp)))
+            toks.append(tok)
+            logits.append(lg)
+        return np.stack(toks), np.stack(logits)
+
+
+def argmax_first(logits):
+    """Index of the largest value along the last axis; the lowest index among equal maxima."""
+    return np.argmax(np.asarray(logits), axis=-1).astype(np.int32)
