@@ -65,6 +65,7 @@ typedef enum {
  *    groups run along every projection's input dimension)          (FP_ERR_INVALID_ARG)
  *  - max_seq >= max_prompt (max_seq == max_prompt leaves no room for a decode step
  *    after a full-length prompt)                                    (FP_ERR_INVALID_ARG)
+ *  - vocab >= 0 and a multiple of 16                              (FP_ERR_INVALID_ARG)
  *  - head_dim 64 or 128; query group n_heads / n_kv_heads from 1 to 16;
  *    max_batch <= 64; max_batch * max_prompt <= 2^24               (FP_ERR_UNSUPPORTED) */
 typedef struct {
@@ -72,6 +73,9 @@ typedef struct {
     int32_t max_batch, max_prompt, max_seq;
     float rms_eps;      /* RMSNorm epsilon, inside the square root (1e-5) */
     float rope_theta;   /* rotary base (1e4) */
+    int32_t vocab;      /* 0: hidden layers only (requests on hidden states); > 0 (a multiple
+                           of 16): the fingerprint also keeps the token embedding, the final
+                           norm and the LM head (Sec. 5.1, Fig. 2) for requests on token ids */
 } fp_shape;
 
 typedef struct fp_layer fp_layer;   /* opaque: weights, KV cache, workspace, position */
@@ -80,7 +84,13 @@ typedef struct fp_layer fp_layer;   /* opaque: weights, KV cache, workspace, pos
 enum {
     FP_T_ATTN_NORM = 0, FP_T_Q = 1, FP_T_K = 2, FP_T_V = 3, FP_T_O = 4,
     FP_T_MLP_NORM = 5, FP_T_GATE = 6, FP_T_UP = 7, FP_T_DOWN = 8,
-    FP_T_INPUT = 15      /* prompt hidden states, layer id -1 */
+    FP_T_INPUT = 15,     /* prompt hidden states, layer id -1 */
+    /* the blocks outside the hidden layers (layer id -1), present when vocab > 0; all
+     * bf16 under every weight format (the weight-only quantisation of Sec. 3.2 applies
+     * to the hidden layers' projections) */
+    FP_T_EMBED = 16,     /* token embedding [vocab, hidden], ~N(0, 0.02) */
+    FP_T_FINAL_NORM = 17,/* final RMSNorm gain [hidden], 1 + N(0, 0.02) */
+    FP_T_LM_HEAD = 18    /* LM head [vocab, hidden], ~N(0, 0.02) */
 };
 
 /*
@@ -180,6 +190,85 @@ fp_status fp_fill_normal(void* dst, int64_t n, uint64_t seed, int32_t layer, int
                          float mean, float sigma, void* stream);
 
 /*
+ * The fingerprint's blocks outside the hidden layers (Sec. 5.1, Fig. 2), for handles
+ * created with vocab > 0 (FP_ERR_STATE otherwise).  Their time is the "other" share
+ * of TTFT and TPOT in Eq. 2 and Eq. 3 (Sec. 5.3).
+ *
+ * fp_embed: x[m] = row ids[m] of the embedding table, m < M.  ids: device int32 [M];
+ * x: device bf16 [M, hidden].  An id outside [0, vocab) gives a row of zeros.
+ */
+fp_status fp_embed(fp_layer* layer, const int32_t* ids, int64_t M, void* x, void* stream);
+
+/*
+ * fp_head: final RMSNorm and LM head of the last position of each of B sequences, then
+ * greedy decoding.  y: device bf16 [B, T, hidden] (a decode step's output has T = 1, a
+ * prefill's T = P); the head reads position T - 1 of each sequence:
+ *   yn = bf16(y * rsqrt(mean(y^2) + eps) * g_final),  logits = yn W_lm^T (fp32),
+ *   next_ids[b] = argmax_v logits[b, v], the lowest v among equal maxima.
+ * logits: device fp32 [B, vocab], or NULL; next_ids: device int32 [B].
+ * 1 <= B <= max_batch, T >= 1.
+ */
+fp_status fp_head(fp_layer* layer, const void* y, int32_t B, int32_t T, float* logits, int32_t* next_ids,
+                  void* stream);
+
+/*
+ * fp_generate: one dummy request on token ids (the Profiler's request, Sec. 4.2 and
+ * Sec. 5.3): embed the prompt, prefill, head -> token 0 (the first token); then n_out
+ * decode steps, step i embedding token i - 1 and producing token i.  Output length
+ * n_out is the number of decode steps (Eq. 1: latency = TTFT + n_out * TPOT).
+ *   prompt_ids: device int32 [B, P];  out_ids: device int32 [n_out + 1, B];
+ *   logits: device fp32 [n_out + 1, B, vocab], or NULL;
+ *   force_ids: NULL, or device int32 [n_out, B]: step i embeds force_ids[i - 1] instead
+ *     of its own token i - 1 (teacher forcing, for parity checks); out_ids still
+ *     receives the generated tokens;
+ *   elapsed_ms: NULL, or receives the request's device time (events recorded on
+ *     `stream` around it; the call then synchronises the stream).
+ * Resets the cache of the B sequences like fp_prefill; the position ends at P + n_out.
+ * The n_out decode steps replay as one captured graph per (out_ids, logits, force_ids,
+ * n_out, B) while the decode graph is on.  1 <= B <= max_batch, 1 <= P <= max_prompt,
+ * n_out >= 0, P + n_out <= max_seq (FP_ERR_CAPACITY).
+ */
+fp_status fp_generate(fp_layer* layer, const int32_t* prompt_ids, int32_t B, int32_t P, int32_t n_out,
+                      int32_t* out_ids, float* logits, const int32_t* force_ids, float* elapsed_ms,
+                      void* stream);
+
+/*
+ * Latency and memory estimation from fingerprints (host arithmetic, no device).
+ *
+ * Eq. 1 (Sec. 5.3): latency = TTFT + output_length * TPOT.  fp_fit_ttft_tpot solves the
+ * 2x2 system of Eq. 1 at two output lengths.  L2: two fingerprints with layers[0] and
+ * layers[1] hidden layers, each timed at the output lengths n_out[0] and n_out[1]
+ * (latency[2*i + j]: fingerprint i at length j, any time unit); fp_fit_latency_l2
+ * solves each fingerprint's 2x2, then the 4x4 system of Eq. 2 and Eq. 3
+ *   TTFT = num_layers * TTFT_layer + TTFT_other,  TPOT = num_layers * TPOT_layer + TPOT_other.
+ * fp_predict_latency evaluates Eq. 1-3 for any layer count and output length (NULL
+ * outputs skipped).  FP_ERR_INVALID_ARG for NULL inputs or a singular system (equal
+ * lengths or equal layer counts).
+ */
+typedef struct {
+    double ttft_layer, tpot_layer, ttft_other, tpot_other;
+} fp_latency_model;
+
+fp_status fp_fit_ttft_tpot(const int32_t n_out[2], const double latency[2], double* ttft, double* tpot);
+fp_status fp_fit_latency_l2(const int32_t layers[2], const int32_t n_out[2], const double latency[4],
+                            fp_latency_model* model);
+fp_status fp_predict_latency(const fp_latency_model* model, int32_t n_layers, int32_t n_out, double* ttft,
+                             double* tpot, double* latency);
+
+/*
+ * M2's layer extrapolation (Sec. 5.2): the value (e.g. a memory footprint) on the straight
+ * line through (layers[0], values[0]) and (layers[1], values[1]) at n_layers; footprints
+ * grow linearly with the number of hidden layers (Sec. 5, Fig. 7).  FP_ERR_INVALID_ARG
+ * for equal layer counts.
+ */
+fp_status fp_extrapolate_layers(const int32_t layers[2], const double values[2], int32_t n_layers,
+                                double* value);
+
+/* Device memory in use on the current device (total - free, hipMemGetInfo) and its
+ * total; the observed footprint M2 profiles (Sec. 5.2).  Either pointer may be NULL. */
+fp_status fp_device_memory(size_t* used, size_t* total);
+
+/*
  * Copy one weight tensor to host memory in its canonical layout (synchronous).
  * For parity checks of the quantised formats of Sec. 3.2 / Table A.1 (INT8 per
  * channel, INT4 group-128) against an independent implementation:
@@ -188,6 +277,8 @@ fp_status fp_fill_normal(void* dst, int64_t n, uint64_t seed, int32_t layer, int
  *  int4:  codes = int32 [N, K/8] with nibble j of word w holding column 8w+j,
  *         scales = fp16 [N, K/128], zeros = fp16 [N, K/128] (integer values)
  * Norm gains (FP_T_ATTN_NORM, FP_T_MLP_NORM): codes = bf16 [hidden].
+ * With vocab > 0 and l = -1: FP_T_EMBED and FP_T_LM_HEAD codes = bf16 [vocab, hidden],
+ * FP_T_FINAL_NORM codes = bf16 [hidden].
  * [N, K] is (out, in): q [nh*d, hidden], k/v [nkv*d, hidden], o [hidden, nh*d],
  * gate/up [ffn, hidden], down [hidden, ffn].
  */

@@ -21,7 +21,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "fp.h")
 WQ = {"bf16": 0, "int8": 1, "int4": 2}
 KVQ = {"bf16": 0, "int8": 1}
 TENSOR = {"attn_norm": 0, "q": 1, "k": 2, "v": 3, "o": 4, "mlp_norm": 5, "gate": 6, "up": 7,
-          "down": 8, "input": 15}
+          "down": 8, "input": 15, "embed": 16, "final_norm": 17, "lm_head": 18}
 STATUS = {0: "FP_OK", -1: "FP_ERR_INVALID_ARG", -2: "FP_ERR_STATE", -3: "FP_ERR_CAPACITY",
           -4: "FP_ERR_OOM", -5: "FP_ERR_HIP", -6: "FP_ERR_UNSUPPORTED"}
 
@@ -39,12 +39,19 @@ class FpShape(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
                 ("max_batch", ctypes.c_int32), ("max_prompt", ctypes.c_int32),
                 ("max_seq", ctypes.c_int32), ("rms_eps", ctypes.c_float),
-                ("rope_theta", ctypes.c_float)]
+                ("rope_theta", ctypes.c_float), ("vocab", ctypes.c_int32)]
 
     @classmethod
     def from_obj(cls, s):
-        """Build from any object with the shape's attribute names (e.g. a dataclass)."""
-        return cls(*(getattr(s, f) for f, _ in cls._fields_))
+        """Build from any object with the shape's attribute names (e.g. a dataclass); a
+        missing vocab means 0 (hidden layers only)."""
+        return cls(*(getattr(s, f, 0) for f, _ in cls._fields_))
+
+
+class LatencyModel(ctypes.Structure):
+    """fp_latency_model: the four unknowns of Eq. 2 and Eq. 3."""
+    _fields_ = [("ttft_layer", ctypes.c_double), ("tpot_layer", ctypes.c_double),
+                ("ttft_other", ctypes.c_double), ("tpot_other", ctypes.c_double)]
 
 
 _lib = None
@@ -82,6 +89,18 @@ def load(path: str | None = None):
         "fp_memory_bytes": [vp, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
                             ctypes.POINTER(ctypes.c_size_t)],
         "fp_get_position": [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "fp_embed": [vp, vp, i64, vp, vp],
+        "fp_head": [vp, vp, i32, i32, vp, vp, vp],
+        "fp_generate": [vp, vp, i32, i32, i32, vp, vp, vp, ctypes.POINTER(ctypes.c_float), vp],
+        "fp_fit_ttft_tpot": [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double),
+                             ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)],
+        "fp_fit_latency_l2": [ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double),
+                              ctypes.POINTER(LatencyModel)],
+        "fp_predict_latency": [ctypes.POINTER(LatencyModel), i32, i32, ctypes.POINTER(ctypes.c_double),
+                               ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)],
+        "fp_extrapolate_layers": [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double), i32,
+                                  ctypes.POINTER(ctypes.c_double)],
+        "fp_device_memory": [ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -125,6 +144,56 @@ def _dev_ptr(t, dtype_bits: int = 16, numel: int | None = None, name: str = "ten
     if numel is not None and t.numel() != numel:
         raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
     return t.data_ptr()
+
+
+def _i32s(*v):
+    return (ctypes.c_int32 * len(v))(*[int(x) for x in v])
+
+
+def _f64s(*v):
+    return (ctypes.c_double * len(v))(*[float(x) for x in v])
+
+
+def fit_ttft_tpot(n_out, latency):
+    """Eq. 1 at two output lengths -> (TTFT, TPOT)."""
+    t, p = ctypes.c_double(), ctypes.c_double()
+    _check(load().fp_fit_ttft_tpot(_i32s(*n_out), _f64s(*latency), ctypes.byref(t), ctypes.byref(p)),
+           "fp_fit_ttft_tpot")
+    return t.value, p.value
+
+
+def fit_latency_l2(layers, n_out, latency):
+    """L2 (Eq. 1-3): latency[i][j] of the fingerprint with layers[i] layers at length n_out[j]
+    -> dict(ttft_layer, tpot_layer, ttft_other, tpot_other)."""
+    m = LatencyModel()
+    flat = [latency[0][0], latency[0][1], latency[1][0], latency[1][1]]
+    _check(load().fp_fit_latency_l2(_i32s(*layers), _i32s(*n_out), _f64s(*flat), ctypes.byref(m)),
+           "fp_fit_latency_l2")
+    return {f: getattr(m, f) for f, _ in LatencyModel._fields_}
+
+
+def predict_latency(model, n_layers, n_out):
+    """(TTFT, TPOT, latency) of n_layers hidden layers at output length n_out."""
+    m = LatencyModel(**model)
+    t, p, l = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(load().fp_predict_latency(ctypes.byref(m), int(n_layers), int(n_out), ctypes.byref(t),
+                                     ctypes.byref(p), ctypes.byref(l)), "fp_predict_latency")
+    return t.value, p.value, l.value
+
+
+def extrapolate_layers(layers, values, n_layers):
+    """M2's linear extrapolation in the layer count."""
+    v = ctypes.c_double()
+    _check(load().fp_extrapolate_layers(_i32s(*layers), _f64s(*values), int(n_layers), ctypes.byref(v)),
+           "fp_extrapolate_layers")
+    return v.value
+
+
+def device_memory():
+    """(used, total) bytes of the current device (hipMemGetInfo)."""
+    u, t = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(load().fp_device_memory(ctypes.byref(u), ctypes.byref(t)), "fp_device_memory")
+    return u.value, t.value
 
 
 def fill_normal(t, seed: int, layer: int, tensor: int, mean: float, sigma: float, stream=None):
@@ -210,6 +279,39 @@ class Fingerprint:
     def decode_ptr(self, x_ptr: int, y_ptr: int, stream_ptr: int = 0):
         _check(load().fp_decode_step(self._h, x_ptr, y_ptr, stream_ptr), "fp_decode_step")
 
+    # blocks outside the hidden layers (vocab > 0) ------------------------
+    def embed(self, ids, x, stream=None):
+        """x [M, hidden] bf16 <- embedding rows of ids (int32 CUDA tensor [M])."""
+        M = ids.numel()
+        ip = _dev_ptr(ids, dtype_bits=32, name="ids")
+        xp = _dev_ptr(x, numel=M * self.shape.hidden, name="x")
+        _check(load().fp_embed(self._h, ip, M, xp, _stream(stream)), "fp_embed")
+
+    def head(self, y, B: int, T: int, next_ids, logits=None, stream=None):
+        """Final norm + LM head + greedy argmax of position T-1 of y [B, T, hidden]."""
+        yp = _dev_ptr(y, numel=B * T * self.shape.hidden, name="y")
+        ip = _dev_ptr(next_ids, dtype_bits=32, numel=B, name="next_ids")
+        lp = None if logits is None else _dev_ptr(logits, dtype_bits=32, numel=B * self.shape.vocab,
+                                                  name="logits")
+        _check(load().fp_head(self._h, yp, B, T, lp, ip, _stream(stream)), "fp_head")
+
+    def generate(self, prompt_ids, n_out: int, out_ids, logits=None, force_ids=None, timed=False,
+                 stream=None):
+        """One dummy request: prompt_ids int32 [B, P] -> out_ids int32 [n_out + 1, B] (and the
+        logits [n_out + 1, B, vocab] when given).  Returns the device time in ms when timed."""
+        B, P = prompt_ids.shape
+        pp = _dev_ptr(prompt_ids, dtype_bits=32, name="prompt_ids")
+        op = _dev_ptr(out_ids, dtype_bits=32, numel=(n_out + 1) * B, name="out_ids")
+        lp = None if logits is None else _dev_ptr(logits, dtype_bits=32,
+                                                  numel=(n_out + 1) * B * self.shape.vocab, name="logits")
+        fp_ = None if force_ids is None else _dev_ptr(force_ids, dtype_bits=32, numel=n_out * B,
+                                                      name="force_ids")
+        ms = ctypes.c_float(-1.0)
+        _check(load().fp_generate(self._h, pp, B, P, int(n_out), op, lp, fp_,
+                                  ctypes.byref(ms) if timed else None, _stream(stream)), "fp_generate")
+        self.B = B
+        return ms.value if timed else None
+
     def set_decode_graph(self, enable: bool):
         _check(load().fp_set_decode_graph(self._h, 1 if enable else 0), "fp_set_decode_graph")
 
@@ -240,9 +342,15 @@ class Fingerprint:
                 "gate": (s.ffn, s.hidden), "up": (s.ffn, s.hidden), "down": (s.hidden, s.ffn)}[name]
 
     def export_weight(self, layer: int, name: str):
-        """(codes, scales, zeros) as numpy arrays in the canonical layouts of fp.h."""
+        """(codes, scales, zeros) as numpy arrays in the canonical layouts of fp.h (layer -1
+        for the embedding, final norm and LM head)."""
         L = load()
-        if name in ("attn_norm", "mlp_norm"):
+        if name in ("embed", "lm_head"):
+            c = np.empty((self.shape.vocab, self.shape.hidden), np.uint16)
+            _check(L.fp_export_weight(self._h, -1, TENSOR[name], c.ctypes.data, None, None),
+                   "fp_export_weight")
+            return c, None, None
+        if name in ("attn_norm", "mlp_norm", "final_norm"):
             g = np.empty(self.shape.hidden, np.uint16)
             _check(L.fp_export_weight(self._h, layer, TENSOR[name], g.ctypes.data, None, None),
                    "fp_export_weight")

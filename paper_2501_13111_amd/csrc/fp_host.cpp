@@ -77,6 +77,7 @@ constexpr int TARGET_WG = FP_TARGET_WG;   // decode workgroups per projection th
 #endif
 
 struct Mat {
+    int wf = 0;                   // weight format (W_BF16 / W_INT8 / W_INT4)
     void* codes = nullptr;        // fragment-major tiles of bf16 / int8 / int4 (device nibble order)
     uint16_t* scales = nullptr;
     uint16_t* zeros = nullptr;
@@ -155,6 +156,16 @@ struct fp_layer {
     float* attn_ws = nullptr;     // decode attention partials
     float* ssq = nullptr;         // decode row-norm block sums         [Bmax, nblk]
     int* d_pos = nullptr;
+    // blocks outside the hidden layers (vocab > 0)
+    uint16_t* embed = nullptr;    // token embedding, bf16 [vocab, H] row-major
+    uint16_t* final_norm = nullptr;
+    Mat lm;                       // LM head, bf16 [vocab, H] fragment-major
+    float* hpart = nullptr;       // LM head split-K partials            [ks, Bmax, vocab]
+    float* hbval = nullptr;       // best logit per 2048-logit block     [Bmax, nblk]
+    int* hbidx = nullptr;
+    uint16_t* hnorm = nullptr;    // final-normalised rows (batches)     [Bmax, H]
+    uint16_t* tok_x = nullptr;    // embedded tokens of a request        [Mmax, H]
+    uint16_t* tok_y = nullptr;    // layer-stack output of a request     [Mmax, H]
     // state
     int pos = 0, B = 0;
     bool prefilled = false;
@@ -168,6 +179,8 @@ struct fp_layer {
     // changes the batch drops them.  At most GRAPH_CACHE_MAX entries each.
     std::map<std::tuple<const void*, void*, int>, hipGraphExec_t> graphs;     // (x, y, B)
     std::map<std::tuple<void*, void*, int, int>, hipGraphExec_t> mgraphs;     // (x, y, n, B)
+    // fp_generate's decode loop: (out_ids, logits, force_ids, n_out, B)
+    std::map<std::tuple<int32_t*, float*, const int32_t*, int, int>, hipGraphExec_t> ggraphs;
     Prof prof;
     size_t bytes_w = 0, bytes_kv = 0, bytes_ws = 0;
     std::vector<void*> allocs;
@@ -206,12 +219,14 @@ constexpr size_t GRAPH_CACHE_MAX = 16;
 // Destroy every captured decode graph.  A replay may still be in flight on some stream,
 // so the device is synchronised first (only when there is something to destroy).
 void drop_graphs(fp_layer* h) {
-    if (h->graphs.empty() && h->mgraphs.empty()) return;
+    if (h->graphs.empty() && h->mgraphs.empty() && h->ggraphs.empty()) return;
     (void)hipDeviceSynchronize();
     for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
     h->graphs.clear();
     for (auto& kv : h->mgraphs) (void)hipGraphExecDestroy(kv.second);
     h->mgraphs.clear();
+    for (auto& kv : h->ggraphs) (void)hipGraphExecDestroy(kv.second);
+    h->ggraphs.clear();
 }
 
 void free_all(fp_layer* h) {
@@ -234,6 +249,8 @@ fp_status validate_shape(const fp_shape* s, int wq, int kvq) {
     if (s->head_dim % 2 != 0) return fail(FP_ERR_INVALID_ARG, "head_dim must be even");
     if (s->max_seq < s->max_prompt) return fail(FP_ERR_INVALID_ARG, "max_seq < max_prompt");
     if (!(s->rms_eps > 0.f) || !(s->rope_theta > 0.f)) return fail(FP_ERR_INVALID_ARG, "rms_eps and rope_theta must be > 0");
+    if (s->vocab < 0 || s->vocab % 16 != 0)
+        return fail(FP_ERR_INVALID_ARG, "vocab %d must be 0 or a positive multiple of 16", s->vocab);
     const int q_dim = s->n_heads * s->head_dim;
     const int mult = (wq == FP_WQ_INT4_G128) ? 128 : 16;
     if (s->hidden % mult || q_dim % mult || s->ffn % mult)
@@ -252,17 +269,18 @@ fp_status validate_shape(const fp_shape* s, int wq, int kvq) {
 
 size_t act_elems(const fp_layer* h) { return (size_t)h->s.max_batch * h->s.max_prompt; }
 
-// Allocate the storage of a [N, K] weight in format wq.
-fp_status alloc_mat(fp_layer* h, Mat* m, int N, int K) {
+// Allocate the storage of a [N, K] weight in format wf.
+fp_status alloc_mat(fp_layer* h, Mat* m, int N, int K, int wf) {
+    m->wf = wf;
     m->N = N;
     m->K = K;
-    const int KS = weight_kstep(h->wq);
+    const int KS = weight_kstep(wf);
     m->kst = (K + KS - 1) / KS;
     const size_t nk = (size_t)N * K;
     fp_status st;
     if ((st = dev_alloc(h, &m->codes, (size_t)(N / 16) * m->kst * 1024, &h->bytes_w))) return st;
-    if (h->wq == FP_WQ_INT8_CHANNEL) return alloc_t(h, &m->scales, (size_t)N, &h->bytes_w);
-    if (h->wq == FP_WQ_INT4_G128) {
+    if (wf == W_INT8) return alloc_t(h, &m->scales, (size_t)N, &h->bytes_w);
+    if (wf == W_INT4) {
         if ((st = alloc_t(h, &m->scales, nk / 128, &h->bytes_w))) return st;
         if ((st = alloc_t(h, &m->sz, nk / 128, &h->bytes_w))) return st;
         return alloc_t(h, &m->zeros, nk / 128, &h->bytes_w);
@@ -277,13 +295,13 @@ fp_status synth_rows(fp_layer* h, Mat* m, int row0, int n, int layer, int tensor
     const uint64_t key = stream_key(h->seed, layer, tensor);
     const int K = m->K;
     const int64_t cnt = (int64_t)n * K;
-    const int KS = weight_kstep(h->wq), eb = weight_ebits(h->wq);
+    const int KS = weight_kstep(m->wf), eb = weight_ebits(m->wf);
     HIPCHK(launch_fill_bf16(tmp, cnt, key, 0.f, 0.02f, 0));
     const void* src = tmp;
-    if (h->wq == FP_WQ_INT8_CHANNEL) {
+    if (m->wf == W_INT8) {
         HIPCHK(launch_quant_int8(tmp, n, K, (int8_t*)tmpq, m->scales + row0, 0));
         src = tmpq;
-    } else if (h->wq == FP_WQ_INT4_G128) {
+    } else if (m->wf == W_INT4) {
         HIPCHK(launch_quant_int4(tmp, n, K, (uint32_t*)tmpq, m->scales + (int64_t)row0 * (K / 128),
                                  m->zeros + (int64_t)row0 * (K / 128), 0));
         src = tmpq;
@@ -322,8 +340,9 @@ struct XIn {
 // Split of a single-sequence decode projection: wide matrices (qkv, gate/up) stream
 // faster with twice the workgroups.
 void plan_skinny(const fp_layer* h, const Mat& m, int M, int dual_F, int* ks, int* kr) {
+    (void)h;
     const int ncols = dual_F > 0 ? 2 * dual_F : m.N;
-    choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, h->wq, ncols >= SPLIT_WIDE_N ? 2 * TARGET_WG : TARGET_WG, ks,
+    choose_split(skinny_tiles(m.N, dual_F, M), m.K, M, m.wf, ncols >= SPLIT_WIDE_N ? 2 * TARGET_WG : TARGET_WG, ks,
                  kr);
 }
 
@@ -357,7 +376,7 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
     plan_skinny(h, m, M, dual_F, &ks, &kr);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     a.krange = kr;
-    HIPCHK(launch_skinny(a, h->wq, ks, st));
+    HIPCHK(launch_skinny(a, m.wf, ks, st));
     *ks_out = ks;
     return FP_OK;
 }
@@ -373,9 +392,10 @@ constexpr int NCU = 256;
 void plan_skinny_batch(const fp_layer* h, const Mat& m, int M, int dual_F, int* ks_out, int* kr_out) {
     const int KC = skinny_batch_chunk();
     const int nch = (m.K + KC - 1) / KC;
-    const int tiles = skinny_batch_tiles(m.N, dual_F, h->wq);
-    const int rows = skinny_batch_rows(m.N, dual_F, h->wq);
-    const double bpw = h->wq == FP_WQ_BF16 ? 2.0 : (h->wq == FP_WQ_INT8_CHANNEL ? 1.0 : 0.5);
+    (void)h;
+    const int tiles = skinny_batch_tiles(m.N, dual_F, m.wf);
+    const int rows = skinny_batch_rows(m.N, dual_F, m.wf);
+    const double bpw = m.wf == W_BF16 ? 2.0 : (m.wf == W_INT8 ? 1.0 : 0.5);
     const double chunk_s = rows * KC * bpw / 25e9;
     const double split_s = (double)M * (dual_F > 0 ? 2.0 * dual_F : m.N) * 8.0 / 5e12;
     int per = nch;
@@ -409,7 +429,7 @@ fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, 
     int ks;
     plan_skinny_batch(h, m, M, dual_F, &ks, &a.krange);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
-    HIPCHK(launch_skinny_batch(a, h->wq, ks, st));
+    HIPCHK(launch_skinny_batch(a, m.wf, ks, st));
     *ks_out = ks;
     return FP_OK;
 }
@@ -709,6 +729,27 @@ fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_
     return h->B == 1 ? enqueue_decode_single(h, x, y, st) : enqueue_decode_batch(h, x, y, st);
 }
 
+// Final RMSNorm, LM head and greedy argmax of position T - 1 of each of B sequences of
+// y [B, T, H].  One sequence: the projection normalises its row while staging it (the
+// workgroup sums the row's squares itself); batches: a row kernel normalises first.
+fp_status enqueue_head(fp_layer* h, const uint16_t* y, int B, int T, float* logits, int32_t* ids, hipStream_t st) {
+    const int H = h->s.hidden;
+    fp_status rc;
+    int ks;
+    if (B == 1) {
+        XIn xn;
+        xn.xf = XF_NORM;
+        xn.gain = h->final_norm;
+        xn.ssq = nullptr;
+        if ((rc = run_skinny(h, y + (size_t)(T - 1) * H, h->lm, 1, 0, xn, h->hpart, &ks, st))) return rc;
+    } else {
+        HIPCHK(launch_head_norm(y, B, T, H, h->final_norm, h->s.rms_eps, h->hnorm, st));
+        if ((rc = run_skinny_batch(h, h->hnorm, h->lm, B, 0, h->hpart, &ks, st))) return rc;
+    }
+    HIPCHK(launch_logits_argmax(h->hpart, ks, B, h->s.vocab, logits, h->hbval, h->hbidx, ids, st));
+    return FP_OK;
+}
+
 bool overlap(const void* a, size_t na, const void* b, size_t nb) {
     const char* pa = (const char*)a;
     const char* pb = (const char*)b;
@@ -813,10 +854,10 @@ fp_status alloc_storage(fp_layer* h) {
     for (auto& W : h->L) {
         if ((st = alloc_t(h, &W.attn_norm, H, &h->bytes_w))) return st;
         if ((st = alloc_t(h, &W.mlp_norm, H, &h->bytes_w))) return st;
-        if ((st = alloc_mat(h, &W.qkv, h->nqkv, H))) return st;
-        if ((st = alloc_mat(h, &W.o, H, h->q_dim))) return st;
-        if ((st = alloc_mat(h, &W.gu, 2 * F, H))) return st;
-        if ((st = alloc_mat(h, &W.down, H, F))) return st;
+        if ((st = alloc_mat(h, &W.qkv, h->nqkv, H, h->wq))) return st;
+        if ((st = alloc_mat(h, &W.o, H, h->q_dim, h->wq))) return st;
+        if ((st = alloc_mat(h, &W.gu, 2 * F, H, h->wq))) return st;
+        if ((st = alloc_mat(h, &W.down, H, F, h->wq))) return st;
     }
     // KV cache
     // keys [Bmax, nkv, kv_stride, d]; values in transposed blocks [Bmax, nkv, nblk, d, VT_BLK];
@@ -874,6 +915,28 @@ fp_status alloc_storage(fp_layer* h) {
     if ((st = alloc_t(h, &h->cos_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->sin_t, (size_t)s.max_seq * s.head_dim / 2, &h->bytes_ws))) return st;
 
+    if (s.vocab > 0) {
+        // embedding, final norm and LM head (bf16 under every weight format), and the head's
+        // workspace: split-K partials for the largest batch's split, block bests, normalised
+        // rows, and the embedded tokens / outputs of a request
+        const int V = s.vocab;
+        if ((st = alloc_t(h, &h->embed, (size_t)V * H, &h->bytes_w))) return st;
+        if ((st = alloc_t(h, &h->final_norm, H, &h->bytes_w))) return st;
+        if ((st = alloc_mat(h, &h->lm, V, H, W_BF16))) return st;
+        size_t hp = 0;
+        for (int b = 1; b <= s.max_batch; ++b) {
+            int ks, kr;
+            if (b == 1) plan_skinny(h, h->lm, b, 0, &ks, &kr);
+            else plan_skinny_batch(h, h->lm, b, 0, &ks, &kr);
+            hp = std::max(hp, (size_t)ks * b * V);
+        }
+        if ((st = alloc_t(h, &h->hpart, hp, &h->bytes_ws))) return st;
+        if ((st = alloc_t(h, &h->hbval, (size_t)s.max_batch * head_logit_blocks(V), &h->bytes_ws))) return st;
+        if ((st = alloc_t(h, &h->hbidx, (size_t)s.max_batch * head_logit_blocks(V), &h->bytes_ws))) return st;
+        if ((st = alloc_t(h, &h->hnorm, (size_t)s.max_batch * H, &h->bytes_ws))) return st;
+        if ((st = alloc_t(h, &h->tok_x, Mmax * H, &h->bytes_ws))) return st;
+        if ((st = alloc_t(h, &h->tok_y, Mmax * H, &h->bytes_ws))) return st;
+    }
     return FP_OK;
 }
 
@@ -927,7 +990,7 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     if ((st = alloc_storage(h))) return bail(st);
     const int H = s.hidden, F = s.ffn;
     const size_t maxrows = std::max<size_t>({(size_t)h->q_dim * H, (size_t)H * h->q_dim, (size_t)F * H,
-                                             (size_t)H * F});
+                                             (size_t)H * F, (size_t)s.vocab * H});
     const size_t esz = kvq == FP_KV_INT8 ? 1 : 2;
     const size_t kvs = (size_t)kv_row_stride(s.max_seq);
     const size_t kv_bytes = (size_t)s.max_batch * s.n_kv_heads * kvs * s.head_dim * esz;
@@ -973,6 +1036,14 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
             for (Mat* m : {&W.qkv, &W.o, &W.gu, &W.down})
                 if ((st = chk(launch_pack_sz(m->scales, m->zeros, m->N, m->K / 128, m->sz, 0)))) return bail(st);
         }
+    }
+    if (s.vocab > 0) {
+        auto chk = [&](hipError_t e) { return e == hipSuccess ? FP_OK : fail(FP_ERR_HIP, "head synthesis: %s", hipGetErrorString(e)); };
+        if ((st = chk(launch_fill_bf16(h->embed, (int64_t)s.vocab * H, stream_key(seed, -1, FP_T_EMBED), 0.f, 0.02f, 0))))
+            return bail(st);
+        if ((st = chk(launch_fill_bf16(h->final_norm, H, stream_key(seed, -1, FP_T_FINAL_NORM), 1.f, 0.02f, 0))))
+            return bail(st);
+        if ((st = synth_rows(h, &h->lm, 0, s.vocab, -1, FP_T_LM_HEAD, tmp, tmpq))) return bail(st);
     }
     if (hipDeviceSynchronize() != hipSuccess) return bail(fail(FP_ERR_HIP, "weight synthesis failed"));
     for (void* p : {(void*)tmp, tmpq}) {
@@ -1178,6 +1249,121 @@ fp_status fp_profile_decode_step(fp_layer* h, const void* x, void* y, void* stre
     return collect_profile(h, out, cap, count);
 }
 
+fp_status fp_embed(fp_layer* h, const int32_t* ids, int64_t M, void* x, void* stream) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (h->s.vocab == 0) return fail(FP_ERR_STATE, "the handle has no embedding (vocab = 0)");
+    if (!ids || !x) return fail(FP_ERR_INVALID_ARG, "ids and x must be device pointers");
+    if (M < 1 || M > (int64_t)1 << 30) return fail(FP_ERR_INVALID_ARG, "M = %lld tokens", (long long)M);
+    if (h->unbacked) return FP_OK;
+    HIPCHK(launch_embed((const int*)ids, M, h->embed, h->s.vocab, h->s.hidden, (uint16_t*)x, (hipStream_t)stream));
+    return FP_OK;
+}
+
+fp_status fp_head(fp_layer* h, const void* y, int32_t B, int32_t T, float* logits, int32_t* next_ids, void* stream) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (h->s.vocab == 0) return fail(FP_ERR_STATE, "the handle has no LM head (vocab = 0)");
+    if (!y || !next_ids) return fail(FP_ERR_INVALID_ARG, "y and next_ids must be device pointers");
+    if (B < 1 || T < 1) return fail(FP_ERR_INVALID_ARG, "B and T must be >= 1 (got %d, %d)", B, T);
+    if (B > h->s.max_batch) return fail(FP_ERR_CAPACITY, "B %d > max_batch %d", B, h->s.max_batch);
+    if (h->unbacked) return FP_OK;
+    return enqueue_head(h, (const uint16_t*)y, B, T, logits, next_ids, (hipStream_t)stream);
+}
+
+fp_status fp_generate(fp_layer* h, const int32_t* prompt_ids, int32_t B, int32_t P, int32_t n_out, int32_t* out_ids,
+                      float* logits, const int32_t* force_ids, float* elapsed_ms, void* stream) {
+    if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
+    if (h->s.vocab == 0) return fail(FP_ERR_STATE, "the handle has no embedding / LM head (vocab = 0)");
+    if (!prompt_ids || !out_ids) return fail(FP_ERR_INVALID_ARG, "prompt_ids and out_ids must be device pointers");
+    if (B < 1 || P < 1 || n_out < 0)
+        return fail(FP_ERR_INVALID_ARG, "B, P >= 1 and n_out >= 0 required (got %d, %d, %d)", B, P, n_out);
+    if (B > h->s.max_batch) return fail(FP_ERR_CAPACITY, "B %d > max_batch %d", B, h->s.max_batch);
+    if (P > h->s.max_prompt) return fail(FP_ERR_CAPACITY, "P %d > max_prompt %d", P, h->s.max_prompt);
+    if ((int64_t)P + n_out > h->s.max_seq)
+        return fail(FP_ERR_CAPACITY, "P %d + n_out %d > max_seq %d", P, n_out, h->s.max_seq);
+    if (h->unbacked) {
+        h->B = B;
+        h->pos = P + n_out;
+        h->prefilled = true;
+        return FP_OK;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    if (B != h->B) drop_graphs(h);
+    const int H = h->s.hidden, V = h->s.vocab;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (elapsed_ms) {
+        HIPCHK(hipEventCreate(&e0));
+        if (hipEventCreate(&e1) != hipSuccess) {
+            (void)hipEventDestroy(e0);
+            return fail(FP_ERR_HIP, "event creation failed");
+        }
+    }
+    auto finish = [&](fp_status rc) {
+        if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+        return rc;
+    };
+    if (e0 && hipEventRecord(e0, st) != hipSuccess) return finish(fail(FP_ERR_HIP, "event record failed"));
+    fp_status rc;
+    h->prefilled = false;
+    // the prompt: embed, prefill, head -> token 0
+    if (hipError_t e = launch_embed((const int*)prompt_ids, (int64_t)B * P, h->embed, V, H, h->tok_x, st))
+        return finish(fail(FP_ERR_HIP, "embedding launch failed: %s", hipGetErrorString(e)));
+    if ((rc = enqueue_prefill(h, h->tok_x, B, P, h->tok_y, st))) return finish(rc);
+    if ((rc = enqueue_head(h, h->tok_y, B, P, logits, out_ids, st))) return finish(rc);
+    h->B = B;
+    h->pos = P;
+    h->prefilled = true;
+    // n_out decode steps: embed token i - 1, decode, head -> token i
+    auto loop = [&](hipStream_t s) -> fp_status {
+        for (int i = 1; i <= n_out; ++i) {
+            const int32_t* src = force_ids ? force_ids + (size_t)(i - 1) * B : out_ids + (size_t)(i - 1) * B;
+            if (hipError_t e = launch_embed((const int*)src, B, h->embed, V, H, h->tok_x, s))
+                return fail(FP_ERR_HIP, "embedding launch failed: %s", hipGetErrorString(e));
+            fp_status r = enqueue_decode(h, h->tok_x, h->tok_y, s);
+            if (r) return r;
+            r = enqueue_head(h, h->tok_y, B, 1, logits ? logits + (size_t)i * B * V : nullptr, out_ids + (size_t)i * B, s);
+            if (r) return r;
+        }
+        return FP_OK;
+    };
+    if (n_out > 0) {
+        if (h->use_graph && !h->dump && !h->ldump) {
+            const auto key = std::make_tuple(out_ids, logits, force_ids, (int)n_out, B);
+            auto it = h->ggraphs.find(key);
+            if (it == h->ggraphs.end()) {
+                if (h->ggraphs.size() >= GRAPH_CACHE_MAX) drop_graphs(h);
+                hipGraph_t g = nullptr;
+                hipGraphExec_t ge = nullptr;
+                if (hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
+                    return finish(fail(FP_ERR_HIP, "graph capture failed to start"));
+                rc = loop(h->cap_stream);
+                hipError_t e = hipStreamEndCapture(h->cap_stream, &g);
+                if (rc) {
+                    if (g) (void)hipGraphDestroy(g);
+                    return finish(rc);
+                }
+                if (e != hipSuccess) return finish(fail(FP_ERR_HIP, "graph capture failed: %s", hipGetErrorString(e)));
+                e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+                (void)hipGraphDestroy(g);
+                if (e != hipSuccess) return finish(fail(FP_ERR_HIP, "graph instantiate failed: %s", hipGetErrorString(e)));
+                it = h->ggraphs.emplace(key, ge).first;
+            }
+            if (hipGraphLaunch(it->second, st) != hipSuccess) return finish(fail(FP_ERR_HIP, "graph launch failed"));
+        } else if ((rc = loop(st))) {
+            return finish(rc);
+        }
+    }
+    h->pos = P + n_out;
+    if (e1) {
+        float ms = 0.f;
+        if (hipEventRecord(e1, st) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+            hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+            return finish(fail(FP_ERR_HIP, "request timing failed"));
+        *elapsed_ms = ms;
+    }
+    return finish(FP_OK);
+}
+
 fp_status fp_set_decode_graph(fp_layer* h, int32_t enable) {
     if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
     h->use_graph = enable != 0;
@@ -1197,34 +1383,41 @@ fp_status fp_fill_normal(void* dst, int64_t n, uint64_t seed, int32_t layer, int
 
 fp_status fp_export_weight(fp_layer* h, int32_t l, int32_t tensor, void* codes, void* scales, void* zeros) {
     if (!h) return fail(FP_ERR_INVALID_ARG, "layer is NULL");
-    if (l < 0 || l >= h->s.n_layers) return fail(FP_ERR_INVALID_ARG, "layer index %d out of range", l);
+    const bool head = tensor == FP_T_EMBED || tensor == FP_T_FINAL_NORM || tensor == FP_T_LM_HEAD;
+    if (head ? l != -1 : (l < 0 || l >= h->s.n_layers))
+        return fail(FP_ERR_INVALID_ARG, "layer index %d out of range for tensor %d", l, tensor);
+    if (head && h->s.vocab == 0) return fail(FP_ERR_STATE, "the handle has no embedding / LM head (vocab = 0)");
     if (!codes) return fail(FP_ERR_INVALID_ARG, "codes is NULL");
     if (h->unbacked) return fail(FP_ERR_STATE, "handle has no device storage");
-    const LayerW& W = h->L[l];
     const int H = h->s.hidden;
-    if (tensor == FP_T_ATTN_NORM || tensor == FP_T_MLP_NORM) {
+    if (tensor == FP_T_ATTN_NORM || tensor == FP_T_MLP_NORM || tensor == FP_T_FINAL_NORM || tensor == FP_T_EMBED) {
+        const uint16_t* src = tensor == FP_T_ATTN_NORM ? h->L[l].attn_norm
+                            : tensor == FP_T_MLP_NORM  ? h->L[l].mlp_norm
+                            : tensor == FP_T_FINAL_NORM ? h->final_norm : h->embed;
+        const size_t n = tensor == FP_T_EMBED ? (size_t)h->s.vocab * H : (size_t)H;
         HIPCHK(hipDeviceSynchronize());
-        HIPCHK(hipMemcpy(codes, tensor == FP_T_ATTN_NORM ? W.attn_norm : W.mlp_norm, (size_t)H * 2, hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(codes, src, n * 2, hipMemcpyDeviceToHost));
         return FP_OK;
     }
     const Mat* m = nullptr;
     int row0 = 0, n = 0;
     switch (tensor) {
-        case FP_T_Q: m = &W.qkv; row0 = 0; n = h->q_dim; break;
-        case FP_T_K: m = &W.qkv; row0 = h->q_dim; n = h->kv_dim; break;
-        case FP_T_V: m = &W.qkv; row0 = h->q_dim + h->kv_dim; n = h->kv_dim; break;
-        case FP_T_O: m = &W.o; row0 = 0; n = H; break;
-        case FP_T_GATE: m = &W.gu; row0 = 0; n = h->s.ffn; break;
-        case FP_T_UP: m = &W.gu; row0 = h->s.ffn; n = h->s.ffn; break;
-        case FP_T_DOWN: m = &W.down; row0 = 0; n = H; break;
+        case FP_T_Q: m = &h->L[l].qkv; row0 = 0; n = h->q_dim; break;
+        case FP_T_K: m = &h->L[l].qkv; row0 = h->q_dim; n = h->kv_dim; break;
+        case FP_T_V: m = &h->L[l].qkv; row0 = h->q_dim + h->kv_dim; n = h->kv_dim; break;
+        case FP_T_O: m = &h->L[l].o; row0 = 0; n = H; break;
+        case FP_T_GATE: m = &h->L[l].gu; row0 = 0; n = h->s.ffn; break;
+        case FP_T_UP: m = &h->L[l].gu; row0 = h->s.ffn; n = h->s.ffn; break;
+        case FP_T_DOWN: m = &h->L[l].down; row0 = 0; n = H; break;
+        case FP_T_LM_HEAD: m = &h->lm; row0 = 0; n = h->s.vocab; break;
         default: return fail(FP_ERR_INVALID_ARG, "unknown tensor id %d", tensor);
     }
-    const int K = m->K;
+    const int K = m->K, wf = m->wf;
+    if (wf != W_BF16 && !scales) return fail(FP_ERR_INVALID_ARG, "scales is NULL");
+    if (wf == W_INT4 && !zeros) return fail(FP_ERR_INVALID_ARG, "zeros is NULL");
     HIPCHK(hipDeviceSynchronize());
-    if (h->wq != FP_WQ_BF16 && !scales) return fail(FP_ERR_INVALID_ARG, "scales is NULL");
-    if (h->wq == FP_WQ_INT4_G128 && !zeros) return fail(FP_ERR_INVALID_ARG, "zeros is NULL");
     // fragment-major tiles -> row-major canonical layout
-    const int KS = weight_kstep(h->wq), eb = weight_ebits(h->wq);
+    const int KS = weight_kstep(wf), eb = weight_ebits(wf);
     const size_t blk_bytes = 1024, nblk = (size_t)(n / 16) * m->kst;
     std::vector<uint8_t> tiles(nblk * blk_bytes);
     HIPCHK(hipMemcpy(tiles.data(), (const uint8_t*)m->codes + (size_t)(row0 / 16) * m->kst * blk_bytes,
@@ -1240,8 +1433,8 @@ fp_status fp_export_weight(fp_layer* h, int32_t l, int32_t tensor, void* codes, 
                 std::memcpy(dst + (size_t)(16 * nt + r) * rowbytes + (size_t)k0 * eb / 8,
                             tiles.data() + ((size_t)nt * m->kst + st) * blk_bytes + (size_t)L * chunk, chunk);
             }
-    if (h->wq == FP_WQ_BF16) return FP_OK;
-    if (h->wq == FP_WQ_INT8_CHANNEL) {
+    if (wf == W_BF16) return FP_OK;
+    if (wf == W_INT8) {
         HIPCHK(hipMemcpy(scales, m->scales + row0, (size_t)n * 2, hipMemcpyDeviceToHost));
         return FP_OK;
     }

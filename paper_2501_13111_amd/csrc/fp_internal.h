@@ -214,6 +214,14 @@ bool attn_decode_supported(int d, int group);
 hipError_t launch_attn_decode(const AttnDecArgs& a, int B, hipStream_t st);
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st);
 
+// The blocks outside the hidden layers (head.hip).
+hipError_t launch_embed(const int* ids, int64_t M, const uint16_t* E, int V, int H, uint16_t* x, hipStream_t st);
+hipError_t launch_head_norm(const uint16_t* y, int B, int T, int H, const uint16_t* g, float eps, uint16_t* out,
+                            hipStream_t st);
+int head_logit_blocks(int V);
+hipError_t launch_logits_argmax(const float* part, int ks, int B, int V, float* logits, float* bval, int* bidx,
+                                int* out_ids, hipStream_t st);
+
 // Host runtime hooks for the allocation-free decode step (noalloc.hip): one eager decode
 // step whose scratch buffers live in [scratch, scratch + bytes), and setting the
 // thread's last-error message.

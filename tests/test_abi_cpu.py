@@ -205,3 +205,76 @@ def test_memory_bytes_scale_with_weight_format_and_layers():
     for i in range(2):       # weights and KV are linear; the workspace does not grow with layers
         assert one[2][i] - one[1][i] == one[1][i] - one[0][i]
     assert one[0][2] == one[1][2] == one[2][2]
+
+
+@pytest.mark.parametrize("vocab,code", [(8, -1), (-16, -1), (32000, 0), (0, 0)])
+def test_vocab_validation(vocab, code):
+    import dataclasses
+    s = dataclasses.replace(CONFIGS["tiny"]["shape"], vocab=vocab)
+    assert _create_status(s, unbacked=True) == code
+
+
+def test_head_calls_on_unbacked_handles():
+    import dataclasses
+    X, Y = 1 << 20, 1 << 30
+    L = binding.load()
+    plain = Fingerprint(CONFIGS["tiny"]["shape"], "bf16", "bf16", unbacked=True)
+    assert L.fp_embed(plain._h, X, 4, Y, None) == -2            # no embedding (vocab = 0)
+    assert L.fp_head(plain._h, X, 1, 1, None, Y, None) == -2
+    assert L.fp_generate(plain._h, X, 1, 4, 2, Y, None, None, None, None) == -2
+    plain.close()
+    s = dataclasses.replace(CONFIGS["tiny"]["shape"], vocab=512)   # max_batch 1, prompt 32, seq 48
+    fp = Fingerprint(s, "int8", "int8", unbacked=True)
+    assert L.fp_embed(fp._h, X, 0, Y, None) == -1
+    assert L.fp_embed(fp._h, None, 4, Y, None) == -1
+    assert L.fp_embed(fp._h, X, 4, Y, None) == 0
+    assert L.fp_head(fp._h, X, 2, 1, None, Y, None) == -3       # beyond max_batch
+    assert L.fp_head(fp._h, X, 1, 0, None, Y, None) == -1
+    assert L.fp_head(fp._h, X, 1, 5, None, None, None) == -1
+    assert L.fp_generate(fp._h, X, 1, 33, 2, Y, None, None, None, None) == -3    # prompt
+    assert L.fp_generate(fp._h, X, 1, 32, 17, Y, None, None, None, None) == -3   # 32 + 17 > 48
+    assert L.fp_generate(fp._h, X, 1, 32, -1, Y, None, None, None, None) == -1
+    assert L.fp_generate(fp._h, X, 1, 32, 16, Y, None, None, None, None) == 0
+    assert fp.position() == (48, 1)
+    fp.close()
+
+
+def test_memory_bytes_with_the_other_blocks():
+    """Embedding [vocab, hidden] and LM head [vocab, hidden] in bf16 plus the final gain,
+    under every weight format."""
+    import dataclasses
+    for wq in ("bf16", "int4"):
+        s0 = CONFIGS["llama2-7b-bf16"]["shape"]
+        s1 = dataclasses.replace(s0, vocab=32000)
+        w0 = _planned_bytes(s0, wq, "bf16")[0]
+        w1 = _planned_bytes(s1, wq, "bf16")[0]
+        assert w1 - w0 == 2 * 32000 * 4096 * 2 + 4096 * 2
+
+
+def test_estimators_agree_with_the_oracle():
+    import numpy as np
+    from oracle import estimate as E
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        layers = tuple(int(v) for v in rng.choice([1, 2, 3, 4, 8], size=2, replace=False))
+        n_out = tuple(int(v) for v in rng.choice([8, 16, 50, 64, 100, 128], size=2, replace=False))
+        lat = rng.uniform(5, 500, size=(2, 2)).tolist()
+        got = binding.fit_latency_l2(layers, n_out, lat)
+        want = E.fit_l2(layers, n_out, lat)
+        for k in want:
+            assert abs(got[k] - want[k]) <= 1e-9 * (1 + abs(want[k])), k
+        n, o = int(rng.integers(1, 100)), int(rng.integers(0, 500))
+        assert np.allclose(binding.predict_latency(got, n, o), E.predict(want, n, o), rtol=1e-10)
+        t, p = binding.fit_ttft_tpot(n_out, lat[0])
+        assert np.allclose((t, p), E.fit_ttft_tpot(n_out, lat[0]), rtol=1e-10, atol=1e-10)
+        vals = rng.uniform(1e8, 1e10, size=2).tolist()
+        m = int(rng.integers(1, 100))
+        assert np.isclose(binding.extrapolate_layers(layers, vals, m), E.extrapolate_layers(layers, vals, m),
+                          rtol=1e-12)
+    with pytest.raises(FpError) as e:
+        binding.fit_ttft_tpot((32, 32), (1.0, 2.0))
+    assert e.value.code == -1
+    with pytest.raises(FpError):
+        binding.fit_latency_l2((2, 2), (16, 64), [[1.0, 2.0], [1.0, 2.0]])
+    with pytest.raises(FpError):
+        binding.extrapolate_layers((3, 3), (1.0, 2.0), 5)
