@@ -9,7 +9,8 @@
 // after the LDS read (large tiling, where LDS holds the packed codes):
 //   bf16 W: copied; A operand bf16                   (bf16 MFMA)
 //   int8 W: codes -> exact fp16; per-row scale in the epilogue    (fp16 MFMA)
-//   int4 W: fp16((q - z) * s), one rounding per weight            (fp16 MFMA)
+//   int4 W: small tiling fp16((q - z) * s), one rounding per weight; large tiling
+//           exact q - z with the group scale on the fp32 accumulators  (fp16 MFMA)
 // Epilogues: fp32 store (q, k, v before the rotary embedding), residual
 // out = bf16(resid + acc), and SwiGLU a = bf16(silu(gate) * up) where each wave
 // holds gate and up columns of the same f (dual tiles over [gate; up]).
@@ -336,7 +337,12 @@ hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st)
 // MFMA steps of the first half of the current stage.  A rows are stored with an XOR swizzle of their 16-byte
 // chunks so that MFMA fragment reads are free of bank conflicts; weight blocks
 // keep their fragment-major order, so a fragment is one contiguous 1 KiB read.
-// Quantised weights stay packed in LDS and are converted to fp16 per fragment.
+// Quantised weights stay packed in LDS and are converted to fp16 per fragment.  For int4
+// the fragments hold the exact integers q - z, and the group scale goes to the fp32
+// accumulators instead: a stage is one 128-input group, and a lane's accumulators of a
+// 32x32 tile all belong to one output column (one scale), so before each stage the lane
+// re-expresses them in units of that stage's scale (acc *= s_prev / s_cur) and the
+// epilogue multiplies by the last one.  No weight is rounded to fp16.
 typedef __attribute__((address_space(3))) void lvoid_t;
 
 constexpr int BT = 256;
@@ -400,6 +406,9 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     };
 
     uint32_t nsz[2], csz[2];       // int4: scale | zero << 16 of the lane's two columns, next / current stage
+    float s_unit[2] = {1.f, 1.f};  // int4: the scale the lane's accumulators of column tile j are in
+    f16x2 qbias[2];                // int4: fp16 1024 + z of the current group (1024 for a zero scale)
+    bool qzero[2] = {false, false};// int4: the current group's scale is zero (its weights are zero)
 
     // Copies of one stage, issued in parts from inside the previous stage's MFMA loop so
     // that no wave stalls on a burst of copies.  They go through buffer resources: rows
@@ -482,6 +491,22 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     auto compute = [&](int stage, int nk0) {
         const char* sA = smem + stage * T::STAGE;
         const char* sB = sA + T::A_BYTES;
+        if constexpr (WF == W_INT4) {
+            // the stage is one group: accumulators to units of its scale
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const float sc = h2f((uint16_t)(csz[j] & 0xFFFFu));
+                qzero[j] = sc == 0.f;
+                const float s_new = qzero[j] ? s_unit[j] : sc;
+                const float ratio = s_unit[j] / s_new;
+                s_unit[j] = s_new;
+                const _Float16 bz = qzero[j] ? (_Float16)1024.0f
+                                             : (_Float16)(1024.0f + h2f((uint16_t)(csz[j] >> 16)));
+                qbias[j] = f16x2{bz, bz};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i][j] *= ratio;
+            }
+        }
 #pragma unroll
         for (int kk = 0; kk < T::TK / 16; ++kk) {            // 16-k MFMA steps
             if (nk0 >= 0 && kk < T::TK / 32) {
@@ -509,13 +534,10 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                     bop[j] = u32x4{c0.x, c0.y, c1.x, c1.y};
                 } else {
                     // one 128-k block: lane r + 16 g holds k 32 g .. 32 g + 31, 8 per dword
-                    const uint32_t wd = *(const uint32_t*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 4 * (2 * hh + h32));
-                    const _Float16 bz = (_Float16)(1024.0f + h2f((uint16_t)(csz[j] >> 16)));
-                    const f16x2 bias = {bz, bz};
-                    const _Float16 sh = __builtin_bit_cast(_Float16, (uint16_t)(csz[j] & 0xFFFFu));
-                    const f16x2 s2 = {sh, sh};
-                    const u32x4 q = i4x8_to_f16x8(wd, bias);
-                    bop[j] = u32x4{mul_h2(q.x, s2), mul_h2(q.y, s2), mul_h2(q.z, s2), mul_h2(q.w, s2)};
+                    // exact q - z (a zero-scale group contributes nothing: codes 0, bias 1024)
+                    uint32_t wd = *(const uint32_t*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 4 * (2 * hh + h32));
+                    if (qzero[j]) wd = 0u;
+                    bop[j] = i4x8_to_f16x8(wd, qbias[j]);
                 }
             }
 #pragma unroll
@@ -555,6 +577,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             if (DUAL ? nt * 128 + wn * 32 + l32 >= a.F : n >= a.N) continue;
             float sn = 1.f;
             if constexpr (WF == W_INT8) sn = h2f(a.scales[n]);
+            if constexpr (WF == W_INT4) sn = s_unit[j];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -570,6 +593,10 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             if constexpr (WF == W_INT8) {
                 sg = h2f(a.scales[f]);
                 su = h2f(a.scales[a.F + f]);
+            }
+            if constexpr (WF == W_INT4) {
+                sg = s_unit[0];
+                su = s_unit[1];
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -588,6 +615,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             if (n >= a.N) continue;
             float sn = 1.f;
             if constexpr (WF == W_INT8) sn = h2f(a.scales[n]);
+            if constexpr (WF == W_INT4) sn = s_unit[j];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll

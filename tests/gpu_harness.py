@@ -57,6 +57,7 @@ class ParityResult:
     prefill_err2: float = 0.0
     decode_errs2: list = dataclasses.field(default_factory=list)
     layer_errs: list = dataclasses.field(default_factory=list)   # prefill, layer-wise teacher-forced
+    chained_ref: np.ndarray = None  # the oracle's chained prefill output of the compared rows
 
 
 def run_parity(shape, wq, kvq, B, P, S, rows=None, seed=0, graph=True, acc=np.float64,
@@ -92,6 +93,7 @@ def run_parity(shape, wq, kvq, B, P, S, rows=None, seed=0, graph=True, acc=np.fl
     yo = orc.prefill(xo)
     yg = bf16_to_np(y).reshape(B, P, H)
     res = ParityResult(rel_inf(yg[rows], yo), [], rel_2(yg[rows], yo), [])
+    res.chained_ref = yo
     if layerwise:
         ridx = torch.tensor(rows, device="cuda")
         gl = [bf16_to_np(dump[l].index_select(0, ridx)).reshape(len(rows), P, H) for l in range(shape.n_layers)]
