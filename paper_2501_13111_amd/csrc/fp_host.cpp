@@ -14,7 +14,7 @@
 //     skinny[down] -> residual + next layer's rmsnorm
 // All weights of a layer live in three fused matrices: [q; k; v], o, [gate; up],
 // down, each [N, K] row-major (out x in).
-#include "../../include/fp.h"
+#include "fp.h"
 #include "fp_internal.h"
 
 #include <hip/hip_runtime.h>

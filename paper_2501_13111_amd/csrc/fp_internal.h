@@ -1,6 +1,6 @@
 // Internal interface between the host runtime (fp_host.cpp) and the kernels.
 #pragma once
-#include "../../include/fp.h"
+#include "fp.h"
 
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>

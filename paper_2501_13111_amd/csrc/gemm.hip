@@ -356,6 +356,10 @@ struct BigT {
     static constexpr int STAGE = A_BYTES + B_BYTES;
     static constexpr int CPR = TK / 8;                                               // 16-byte chunks per A row
     static constexpr int NSUB = TK / 32;                                             // MFMA k-steps per stage
+    // LDS: two stages, reused by the epilogue (the residual epilogue stages 8 waves x 64 rows
+    // x 72 floats; one workgroup per CU either way)
+    static constexpr int EPI_BYTES = 8 * 64 * 72 * 4;
+    static constexpr int SMEM = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
 };
 
 template <int CPR>
@@ -366,7 +370,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     using T = BigT<WF>;
     constexpr int AF = (WF == W_BF16) ? ACT_BF16 : ACT_F16;
     static_assert(DUAL == (EPI == EPI_SWIGLU) || EPI == EPI_PART, "dual tiling");
-    __shared__ __attribute__((aligned(1024))) char smem[2 * T::STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem[T::SMEM];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -587,28 +591,42 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                 }
         }
     } else if constexpr (DUAL) {
-        const int f = nt * 128 + wn * 32 + l32;
-        if (f < a.F) {
-            float sg = 1.f, su = 1.f;
-            if constexpr (WF == W_INT8) {
+        // SwiGLU: a = act(bf16(silu(gate) * up)) per (m, f); the tile's 256 x 128 outputs are
+        // staged in LDS (the stage buffers are free now) and written as 16-byte pieces of
+        // whole 256-byte rows
+        constexpr int FS = 136;                               // LDS row stride (u16)
+        static_assert(256 * FS * 2 <= T::SMEM, "SwiGLU staging fits the LDS");
+        uint16_t* st16 = (uint16_t*)smem;
+        const int fl = wn * 32 + l32;                         // the lane's column in the tile
+        const int f = nt * 128 + fl;
+        float sg = 1.f, su = 1.f;
+        if constexpr (WF == W_INT8) {
+            if (f < a.F) {
                 sg = h2f(a.scales[f]);
                 su = h2f(a.scales[a.F + f]);
             }
-            if constexpr (WF == W_INT4) {
-                sg = s_unit[0];
-                su = s_unit[1];
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int m = m0 + wm * 128 + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
-                    if (m >= a.M) continue;
-                    const float gv = acc[i][0][e] * sg, uv = acc[i][1][e] * su;
-                    a.out16[(int64_t)m * a.F + f] = act_store(bfround(silu_f(gv) * uv), a.out_fmt);
-                }
         }
-    } else {
+        if constexpr (WF == W_INT4) {
+            sg = s_unit[0];
+            su = s_unit[1];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = wm * 128 + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
+                const float gv = acc[i][0][e] * sg, uv = acc[i][1][e] * su;
+                st16[row * FS + fl] = act_store(bfround(silu_f(gv) * uv), a.out_fmt);
+            }
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {                         // 256 rows x 16 pieces of 8 columns
+            const int idx = t * 512 + tid, row = idx >> 4, c = (idx & 15) * 8;
+            const int m = m0 + row, f0 = nt * 128 + c;
+            if (m < a.M && f0 < a.F)
+                *(u32x4*)(a.out16 + (int64_t)m * a.F + f0) = *(const u32x4*)(st16 + row * FS + c);
+        }
+    } else if constexpr (EPI == EPI_F32) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             const int n = nt * 256 + wn * 64 + 32 * j + l32;
@@ -621,11 +639,61 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
                     const int m = m0 + wm * 128 + 32 * i + 8 * (e >> 2) + 4 * h32 + (e & 3);
-                    if (m >= a.M) continue;
-                    const float v = acc[i][j][e] * sn;
-                    if constexpr (EPI == EPI_F32) a.out32[(int64_t)m * a.N + n] = v;
-                    else a.out16[(int64_t)m * a.N + n] = f2bf(bf2f(a.resid[(int64_t)m * a.N + n]) + v);
+                    if (m < a.M) a.out32[(int64_t)m * a.N + n] = acc[i][j][e] * sn;
                 }
+        }
+    } else {
+        // residual: out = bf16(resid + acc).  Each wave stages its 128 x 64 results in two
+        // passes of 64 rows through its own LDS region (fp32), then reads 8 consecutive
+        // columns per lane and writes them, with the matching resid piece, as 16-byte
+        // pieces of 128-byte row segments; a pass's resid loads go out first.
+        constexpr int ES = 72;                                // LDS row stride (floats): rows r, r + 4 are 32 banks apart
+        static_assert(8 * 64 * ES * 4 <= T::SMEM, "residual staging fits the LDS");
+        float* reg = (float*)smem + w * 64 * ES;
+        float sn[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int n = nt * 256 + wn * 64 + 32 * j + l32;
+            sn[j] = 1.f;
+            if constexpr (WF == W_INT8) sn[j] = n < a.N ? h2f(a.scales[n]) : 0.f;
+            if constexpr (WF == W_INT4) sn[j] = s_unit[j];
+        }
+        const int rl = lane >> 3, c8 = (lane & 7) * 8;        // 8 rows x 8 pieces per instruction
+        const int n8 = nt * 256 + wn * 64 + c8;
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            u32x4 rv[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int m = m0 + wm * 128 + 64 * p + 8 * t + rl;
+                rv[t] = u32x4{0u, 0u, 0u, 0u};
+                if (m < a.M && n8 < a.N) rv[t] = *(const u32x4*)(a.resid + (int64_t)m * a.N + n8);
+            }
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int row = 32 * ii + 8 * (e >> 2) + 4 * h32 + (e & 3);
+                        reg[row * ES + 32 * j + l32] = acc[2 * p + ii][j][e] * sn[j];
+                    }
+            __syncthreads();
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int row = 8 * t + rl, m = m0 + wm * 128 + 64 * p + row;
+                if (m >= a.M || n8 >= a.N) continue;
+                const f32x4 v0 = *(const f32x4*)(reg + row * ES + c8), v1 = *(const f32x4*)(reg + row * ES + c8 + 4);
+                const uint32_t r4[4] = {rv[t].x, rv[t].y, rv[t].z, rv[t].w};
+                const float vv[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+                uint32_t o[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    o[q] = (uint32_t)f2bf(bf2f(r4[q] & 0xFFFFu) + vv[2 * q]) |
+                           ((uint32_t)f2bf(bf2f(r4[q] >> 16) + vv[2 * q + 1]) << 16);
+                *(u32x4*)(a.out16 + (int64_t)m * a.N + n8) = u32x4{o[0], o[1], o[2], o[3]};
+            }
+            __syncthreads();                                  // before the next pass overwrites the region
         }
     }
 }

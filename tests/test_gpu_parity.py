@@ -354,3 +354,23 @@ def test_single_sequence_decode_steps_match_single_steps(kvq):
                 if out is y:
                     x, y = y, x
             assert fp.position() == (42, 1)
+
+
+# prompts long enough for the 256 x 256 prefill tiling (>= 128 tiles) with its fused
+# residual and SwiGLU epilogues: ragged last row tile (M = 8000) and column tile (hidden
+# 1152), and a [gate; up] tile count that is not a multiple of the wave layout
+BIG_CASES = [
+    ("big-int4-ragged", Shape(1, 1152, 9, 9, 128, 2176, 8, 1000, 1002), "int4", "int8", 8, 1000, 2, (0, 7)),
+    ("big-bf16", Shape(1, 1024, 8, 8, 128, 2560, 8, 1024, 1026), "bf16", "bf16", 8, 1024, 2, (3,)),
+    ("big-int8-gqa", Shape(1, 1024, 8, 2, 128, 2048, 8, 1024, 1026), "int8", "int8", 8, 1024, 2, (5,)),
+]
+
+
+@pytest.mark.parametrize("case", BIG_CASES, ids=[c[0] for c in BIG_CASES])
+def test_parity_large_prefill_tiles(case):
+    name, shape, wq, kvq, B, P, S, rows = case
+    log(f"case {name}: {shape} {wq}/{kvq} B={B} P={P} S={S} rows={rows}")
+    res = run_parity(shape, wq, kvq, B, P, S, rows=rows)
+    _report(name, res)
+    assert res.prefill_err <= TOL
+    assert max(res.decode_errs) <= TOL
