@@ -47,6 +47,8 @@ CONFIGS = {
     "llama2-7b-int8": _cfg(2, 4096, 32, 32, 128, 11008, "int8", "int8", 16, 512, 100),
     "llama2-13b-int4": _cfg(4, 5120, 40, 40, 128, 13824, "int4", "bf16", 32, 1024, 100),
     "llama2-70b-tp8-int4": _cfg(4, 8192, 8, 1, 128, 3584, "int4", "int8", 64, 2048, 100),
+    # 2:4 semi-structured sparse bf16 weights (pruning, Sec. 3.3), the 7B shape at batch 16
+    "llama2-7b-sp24": _cfg(2, 4096, 32, 32, 128, 11008, "sp24", "bf16", 16, 512, 100),
 }
 
 # The workload the benchmark's headline is quoted on: the largest model, prompt, batch

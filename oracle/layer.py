@@ -8,7 +8,9 @@ Paper passages followed:
   token, then each output token is one decode step that reuses the KV cache,
   so per-token cost stays constant (Sec. 5.3);
 * INT8 / INT4 weight-only quantisation and an INT8 KV cache are searched
-  (Sec. 3.2, Table A.1).
+  (Sec. 3.2, Table A.1), and so is pruning (Sec. 3.3, Table A.1), here the 2:4
+  semi-structured form with magnitude scores ("sp24": every projection keeps 2 of
+  every 4 consecutive weights of a row, bf16).
 
 The paper writes none of the layer's math.  The reading (Llama-2 style, the
 LLMs it profiles) is, per layer, with x bf16 [T, H]:
@@ -56,7 +58,7 @@ import numpy as np
 import fpgen
 from .numerics import bf16_round
 from .quant import (quant_int8_channel, dequant_int8_channel, quant_int4_g128,
-                    dequant_int4_g128, pack_int4, quant_kv_int8)
+                    dequant_int4_g128, pack_int4, quant_kv_int8, prune_2of4)
 
 # The layer-stack shape and the five workloads live in the data-only table shared
 # with the benchmark.
@@ -147,7 +149,7 @@ class Fingerprint:
 
     def __init__(self, shape: Shape, wq: str = "bf16", kvq: str = "bf16", seed: int = 0,
                  acc=np.float64, weights=None):
-        assert wq in ("bf16", "int8", "int4") and kvq in ("bf16", "int8")
+        assert wq in ("bf16", "int8", "int4", "sp24") and kvq in ("bf16", "int8")
         self.s, self.wq, self.kvq, self.seed, self.acc = shape, wq, kvq, seed, acc
         s = shape
         assert s.n_heads % s.n_kv_heads == 0 and s.head_dim % 2 == 0
@@ -173,6 +175,9 @@ class Fingerprint:
             if self.wq == "bf16":
                 deq = w
                 quant[name] = (w, None, None)
+            elif self.wq == "sp24":
+                deq = np.where(prune_2of4(w), w, F32(0.0)).astype(F32)
+                quant[name] = (deq, None, None)
             elif self.wq == "int8":
                 c, sc = quant_int8_channel(w)
                 deq = dequant_int8_channel(c, sc)
@@ -188,7 +193,7 @@ class Fingerprint:
     def export_weight(self, layer: int, name: str):
         """(codes, scales, zeros) in the canonical layouts: bf16 weights as float32
         values; int8 codes [N, K] with scales [N]; int4 packed words [N, K/8] int32
-        with scales / zeros [N, K/128]."""
+        with scales / zeros [N, K/128]; 2:4 sparse weights dense, pruned ones zero."""
         return self.layers[layer]["quant"][name]
 
     # cache ---------------------------------------------------------------

@@ -20,6 +20,13 @@ the readings below are the ones the build fixes:
 * int8 KV: per (sequence, position, kv head), separately for K (after the
   rotary embedding) and V, the int8 rule above over the head_dim elements.
 
+* 2:4 semi-structured sparsity (the pruning of Sec. 3.3, Table A.1: 2 of every 4
+  weights zero), scored by magnitude: in each group of 4 consecutive k of a row the
+  2 weights of largest |w| are kept, the lower k first among equal magnitudes, and
+  the other 2 set to zero.  The kept weights stay bf16.  Compressed form: the kept
+  values of each group in k order, [N, K/2], and their positions in the group
+  (0..3, first < second), [N, K/2].
+
 Pins (tests/test_oracle_quant.py): brute-force nearest-code search over every
 code, the |w - w_hat| <= s/2 bound, exact grids, pack/unpack round trips, and
 exact ties (w / s = k + 1/2 with power-of-two scales): int8 codes and int8 KV
@@ -103,3 +110,32 @@ def quant_kv_int8(x: np.ndarray):
 
     Returns (codes int8, scales fp16-valued float32 with the last axis removed)."""
     return quant_int8_rows(np.asarray(x, dtype=F32))
+
+
+def prune_2of4(w: np.ndarray) -> np.ndarray:
+    """Magnitude 2:4 mask of W[N, K] (K a multiple of 4): True for the two weights of
+    largest |w| in each group of 4 consecutive k, the lower k first among equal |w|."""
+    w = np.asarray(w, dtype=F32)
+    N, K = w.shape
+    assert K % 4 == 0
+    g = np.abs(w).reshape(N, K // 4, 4)
+    # rank by (-|w|, k): a stable sort on -|w| keeps the lower k first among ties
+    order = np.argsort(-g, axis=-1, kind="stable")
+    mask = np.zeros_like(g, dtype=bool)
+    np.put_along_axis(mask, order[..., :2], True, axis=-1)
+    return mask.reshape(N, K)
+
+
+def compress_2of4(w: np.ndarray, mask: np.ndarray):
+    """(values [N, K/2], positions [N, K/2]) of the kept weights, in k order per group."""
+    N, K = w.shape
+    pos = np.nonzero(mask.reshape(N, K // 4, 4))[2].reshape(N, K // 4, 2)
+    vals = np.take_along_axis(np.asarray(w, dtype=F32).reshape(N, K // 4, 4), pos, axis=-1)
+    return vals.reshape(N, K // 2), pos.reshape(N, K // 2).astype(np.uint8)
+
+
+def decompress_2of4(vals: np.ndarray, pos: np.ndarray) -> np.ndarray:
+    N, K2 = vals.shape
+    out = np.zeros((N, K2 // 2, 4), dtype=F32)
+    np.put_along_axis(out, pos.reshape(N, K2 // 2, 2).astype(np.int64), vals.reshape(N, K2 // 2, 2), axis=-1)
+    return out.reshape(N, 2 * K2)

@@ -163,7 +163,7 @@ def test_causality_and_batch_independence():
 
 
 @pytest.mark.parametrize("wq,kvq", [("bf16", "bf16"), ("int8", "int8"), ("int4", "bf16"),
-                                    ("int4", "int8")])
+                                    ("int4", "int8"), ("sp24", "int8")])
 def test_kv_cached_decode_equals_full_recompute(wq, kvq):
     s = SMALL
     P, S = 8, 6
@@ -234,9 +234,9 @@ def test_layerwise_prefill_reproduces_chain(kvq):
     assert np.array_equal(ys3[0], y0) and not np.array_equal(ys3[1], y)
 
 
-def test_configs_are_the_five_workloads():
+def test_configs_are_the_workloads():
     assert set(CONFIGS) == {"tiny", "llama2-7b-bf16", "llama2-7b-int8", "llama2-13b-int4",
-                            "llama2-70b-tp8-int4"}
+                            "llama2-70b-tp8-int4", "llama2-7b-sp24"}
     c5 = CONFIGS["llama2-70b-tp8-int4"]
     assert c5["shape"].hidden == 8192 and c5["shape"].n_heads == 8 and c5["shape"].n_kv_heads == 1
 
@@ -302,7 +302,8 @@ def _torch_layer_stack(fp, x, P, kvq="bf16", kv_out=None):
 
 
 @pytest.mark.parametrize("wq,kvq", [("bf16", "bf16"), ("int8", "bf16"), ("int4", "bf16"),
-                                    ("bf16", "int8"), ("int8", "int8"), ("int4", "int8")])
+                                    ("bf16", "int8"), ("int8", "int8"), ("int4", "int8"),
+                                    ("sp24", "bf16")])
 def test_layer_matches_torch_functional_composition(wq, kvq):
     s = Shape(2, 128, 4, 2, 32, 256, 2, 10, 10)
     fp = Fingerprint(s, wq, kvq)
@@ -332,3 +333,16 @@ def test_int8_kv_codes_rebuilt_from_torch_ops():
             assert np.array_equal(cc["v"][:, :, :12], vc.permute(0, 2, 1, 3).numpy()), (wq, l)
             assert np.array_equal(cc["ks"][:, :, :12], ksc.permute(0, 2, 1).numpy()), (wq, l)
             assert np.array_equal(cc["vs"][:, :, :12], vsc.permute(0, 2, 1).numpy()), (wq, l)
+
+
+def test_sp24_layer_weights_are_the_pruned_generator_weights():
+    """Each projection of a 2:4 fingerprint is the bf16 generator weight with the magnitude
+    2:4 mask applied: half of every row zero, the kept values unchanged."""
+    from oracle.quant import prune_2of4
+    s = Shape(1, 128, 4, 2, 32, 256, 1, 8, 8)
+    fp = Fingerprint(s, "sp24", "bf16")
+    for name, shp in weight_shapes(s).items():
+        w = fpgen.weight(0, 0, {"q": 1, "k": 2, "v": 3, "o": 4, "gate": 6, "up": 7, "down": 8}[name], shp)
+        got = fp.export_weight(0, name)[0]
+        assert np.array_equal(got, np.where(prune_2of4(w), w, 0)), name
+        assert np.count_nonzero(got == 0) >= got.size // 2

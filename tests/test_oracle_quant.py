@@ -161,3 +161,44 @@ def test_kv_int8_ties_and_fp32_input():
     row2 = np.array([127.0 * float(s0), v] + [0.0] * 14, np.float32)
     c2, _ = quant_kv_int8(row2[None, None, :])
     assert int(c2[0, 0, 1]) == 101
+
+
+def test_2of4_mask_keeps_the_two_largest_magnitudes_brute_force():
+    """Every group of 4 keeps exactly 2; the kept pair has the largest sum of |w| among the
+    6 possible pairs, and among pairs with the same kept magnitudes the lower positions
+    win (the k order tie rule)."""
+    import itertools
+    from oracle.quant import prune_2of4
+    rng = np.random.default_rng(11)
+    w = _bf16_weights(rng, (40, 64))
+    w[0, :8] = [0.5, -0.5, 0.5, 0.25, 0, 0, 0, 0]      # ties in magnitude and all-zero group
+    w[1, :4] = [-1.0, 1.0, 1.0, -1.0]
+    m = prune_2of4(w)
+    assert m.shape == w.shape and np.all(m.reshape(40, 16, 4).sum(-1) == 2)
+    pairs = list(itertools.combinations(range(4), 2))
+    for n in range(w.shape[0]):
+        for g in range(16):
+            grp = np.abs(w[n, 4 * g:4 * g + 4]).astype(np.float64)
+            # the best pair: sort positions by (-|w|, k) and take the first two
+            want = tuple(sorted(sorted(range(4), key=lambda k: (-grp[k], k))[:2]))
+            assert want in pairs
+            got = tuple(np.nonzero(m[n, 4 * g:4 * g + 4])[0])
+            assert got == want, (n, g, grp, got)
+            kept = grp[list(got)].sum()
+            assert all(kept >= grp[list(p)].sum() for p in pairs)
+    assert tuple(np.nonzero(m[0, :4])[0]) == (0, 1) and tuple(np.nonzero(m[0, 4:8])[0]) == (0, 1)
+    assert tuple(np.nonzero(m[1, :4])[0]) == (0, 1)
+
+
+def test_2of4_compress_round_trip_and_bytes():
+    from oracle.quant import prune_2of4, compress_2of4, decompress_2of4
+    rng = np.random.default_rng(12)
+    w = _bf16_weights(rng, (32, 256))
+    m = prune_2of4(w)
+    dense = np.where(m, w, 0).astype(np.float32)
+    v, p = compress_2of4(dense, m)
+    assert v.shape == (32, 128) and p.shape == (32, 128)
+    assert np.all(p.reshape(32, 64, 2)[..., 0] < p.reshape(32, 64, 2)[..., 1]) and p.max() <= 3
+    assert np.array_equal(decompress_2of4(v, p), dense)
+    # half the bf16 values plus 2 bits per kept value: 9/16 of the dense bf16 bytes
+    assert (v.size * 2 + p.size * 2 / 8) / (w.size * 2) == 9 / 16
