@@ -30,7 +30,10 @@ sys.path.insert(0, ROOT)
 METRIC = "fingerprint decode tokens/s + % HBM roofline; prefill MFMA utilisation"
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 MFMA16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 MFMA
-WBYTES = {"bf16": 2.0, "int8": 1.0, "int4": 0.5}
+# weight bytes per dense weight; 2:4 sparse: half the weights kept as bf16 plus a 2-bit
+# position each (1.125 B), the algorithmic multiply work is that of the kept half
+WBYTES = {"bf16": 2.0, "int8": 1.0, "int4": 0.5, "sp24": 1.125}
+WFLOPS = {"bf16": 1.0, "int8": 1.0, "int4": 1.0, "sp24": 0.5}
 
 KIND = {0: "rmsnorm", 1: "qkv", 2: "rope_kv", 3: "attn", 4: "o", 5: "resid_norm", 6: "gate_up",
         7: "swiglu", 8: "down", 9: "pos"}
@@ -130,9 +133,9 @@ def decode_step_bytes(s, wq, kvq, B, t):
     return s.n_layers * per_layer
 
 
-def prefill_flops(s, B, P):
-    params = sum(N * K for N, K in proj_dims(s).values())
-    return s.n_layers * (2 * B * P * params + 4 * s.head_dim * s.n_heads * B * P * (P + 1) // 2)
+def prefill_flops(s, B, P, wq="bf16"):
+    params = sum(N * K for N, K in proj_dims(s).values()) * WFLOPS[wq]
+    return s.n_layers * int(2 * B * P * params + 4 * s.head_dim * s.n_heads * B * P * (P + 1) // 2)
 
 
 def profile_decode(fp, x, y, stream_ptr):
@@ -235,9 +238,9 @@ def cpu_baseline(cfg, seed, budget_s):
             "cpu_model": model, "nproc": nproc, "blas_threads": threads}
 
 
-def gemm_flops(kind, s, M):
+def gemm_flops(kind, s, M, wq="bf16"):
     N, K = proj_dims(s)[kind]
-    return 2 * M * N * K
+    return int(2 * M * N * K * WFLOPS[wq])
 
 
 def attn_kv_bytes(s, kvq, B, t):
@@ -331,7 +334,7 @@ def run_workload(name, args, torch, timed_out=None):
     # decode projections (the weight-streaming kernels): bytes per launch over time per launch
     proj_ms = [ms for prof in dec_profs for kind, _, ms in prof if kind in PROJ]
     proj_b = [proj_bytes(kind, s, wq, B) for prof in dec_profs for kind, _, _ in prof if kind in PROJ]
-    dec_kernel = "skinny_kernel" if B == 1 else "skinny_batch_kernel"
+    dec_kernel = "sp24_gemv_kernel" if wq == "sp24" else ("skinny_kernel" if B == 1 else "skinny_batch_kernel")
     roof_dec = roofline_entry(f"{dec_kernel} (decode projections qkv/o/gate_up/down)", "hbm",
                               sum(proj_b) / (sum(proj_ms) / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s",
                               statistics.fmean(proj_ms), statistics.fmean(proj_b),
@@ -346,8 +349,9 @@ def run_workload(name, args, torch, timed_out=None):
     # prefill GEMMs: flops per launch over time per launch (the kinds' split-K reductions
     # included when a GEMM is split)
     g_ms = [ms for kind, _, ms in pre_prof if kind in PROJ]
-    g_fl = [gemm_flops(kind, s, B * Pp) for kind, _, _ in pre_prof if kind in PROJ]
-    gemm_kernel = "gemm_big_kernel" if B * Pp >= 4096 else "gemm_kernel / gemm_big_kernel split-K"
+    g_fl = [gemm_flops(kind, s, B * Pp, wq) for kind, _, _ in pre_prof if kind in PROJ]
+    gemm_kernel = ("gemm_sp24_kernel (sparse MFMA)" if wq == "sp24" else
+                   "gemm_big_kernel" if B * Pp >= 4096 else "gemm_kernel / gemm_big_kernel split-K")
     roof_gemm = roofline_entry(f"{gemm_kernel} (prefill projections qkv/o/gate_up/down)", "mfma",
                                sum(g_fl) / (sum(g_ms) / 1e3) / 1e12, MFMA16_PEAK_TFLOPS, "TFLOP/s",
                                statistics.fmean(g_ms), statistics.fmean(g_fl),
@@ -368,7 +372,7 @@ def run_workload(name, args, torch, timed_out=None):
     roof["family"] = dom
     roof["share_of_pass"] = round(pass_time[dom] / (statistics.median(prefill_ms) + statistics.median(decode_ms)), 4)
 
-    pflops = prefill_flops(s, B, Pp)
+    pflops = prefill_flops(s, B, Pp, wq)
     pre_med = statistics.median(prefill_ms)
     out = {
         "value": round(value, 2), "unit": "tokens/s",

@@ -48,7 +48,11 @@ typedef enum {
 typedef enum {
     FP_WQ_BF16 = 0,          /* unquantised 16-bit weights */
     FP_WQ_INT8_CHANNEL = 1,  /* symmetric int8, one fp16 scale per output row */
-    FP_WQ_INT4_G128 = 2      /* asymmetric int4, fp16 scale and integer zero per 128 inputs */
+    FP_WQ_INT4_G128 = 2,     /* asymmetric int4, fp16 scale and integer zero per 128 inputs */
+    FP_WQ_BF16_2OF4 = 3      /* 2:4 semi-structured sparse bf16 (pruning, Sec. 3.3, Table A.1):
+                                in every 4 consecutive inputs of a row the 2 weights of largest
+                                magnitude are kept (the lower input first among equal ones);
+                                runs on the sparse matrix cores */
 } fp_weight_quant;
 
 /* KV-cache compression (Sec. 3.2, "KV-cache quantization"). */
@@ -66,6 +70,7 @@ typedef enum {
  *  - max_seq >= max_prompt (max_seq == max_prompt leaves no room for a decode step
  *    after a full-length prompt)                                    (FP_ERR_INVALID_ARG)
  *  - vocab >= 0 and a multiple of 16                              (FP_ERR_INVALID_ARG)
+ *  - 2:4 sparse weights: hidden, n_heads*head_dim and ffn multiples of 64 (FP_ERR_INVALID_ARG)
  *  - head_dim 64 or 128; query group n_heads / n_kv_heads from 1 to 16;
  *    max_batch <= 64; max_batch * max_prompt <= 2^24               (FP_ERR_UNSUPPORTED) */
 typedef struct {
@@ -276,6 +281,7 @@ fp_status fp_device_memory(size_t* used, size_t* total);
  *  int8:  codes = int8 [N, K], scales = fp16 [N]
  *  int4:  codes = int32 [N, K/8] with nibble j of word w holding column 8w+j,
  *         scales = fp16 [N, K/128], zeros = fp16 [N, K/128] (integer values)
+ *  2:4:   codes = bf16 [N, K], dense, the pruned weights zero (scales, zeros unused)
  * Norm gains (FP_T_ATTN_NORM, FP_T_MLP_NORM): codes = bf16 [hidden].
  * With vocab > 0 and l = -1: FP_T_EMBED and FP_T_LM_HEAD codes = bf16 [vocab, hidden],
  * FP_T_FINAL_NORM codes = bf16 [hidden].

@@ -18,7 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libfp_mi355x.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "fp.h")
 
-WQ = {"bf16": 0, "int8": 1, "int4": 2}
+WQ = {"bf16": 0, "int8": 1, "int4": 2, "sp24": 3}
 KVQ = {"bf16": 0, "int8": 1}
 TENSOR = {"attn_norm": 0, "q": 1, "k": 2, "v": 3, "o": 4, "mlp_norm": 5, "gate": 6, "up": 7,
           "down": 8, "input": 15, "embed": 16, "final_norm": 17, "lm_head": 18}
@@ -356,7 +356,7 @@ class Fingerprint:
                    "fp_export_weight")
             return g, None, None
         N, K = self.weight_shape(name)
-        if self.wq == "bf16":
+        if self.wq in ("bf16", "sp24"):
             c = np.empty((N, K), np.uint16)
             _check(L.fp_export_weight(self._h, layer, TENSOR[name], c.ctypes.data, None, None),
                    "fp_export_weight")

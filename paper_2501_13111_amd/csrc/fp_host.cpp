@@ -82,6 +82,7 @@ struct Mat {
     uint16_t* scales = nullptr;
     uint16_t* zeros = nullptr;
     uint32_t* sz = nullptr;       // int4: scale | zero << 16 per (row, group)
+    uint16_t* sidx = nullptr;     // 2:4 sparse: 16-bit index words, 128-byte blocks (codes: value blocks)
     int N = 0, K = 0;
     int kst = 0;                  // K-steps (1 KiB blocks) per 16-row block row
 };
@@ -239,7 +240,7 @@ void free_all(fp_layer* h) {
 
 fp_status validate_shape(const fp_shape* s, int wq, int kvq) {
     if (!s) return fail(FP_ERR_INVALID_ARG, "shape is NULL");
-    if (wq < FP_WQ_BF16 || wq > FP_WQ_INT4_G128) return fail(FP_ERR_INVALID_ARG, "bad weight quant %d", wq);
+    if (wq < FP_WQ_BF16 || wq > FP_WQ_BF16_2OF4) return fail(FP_ERR_INVALID_ARG, "bad weight quant %d", wq);
     if (kvq < FP_KV_BF16 || kvq > FP_KV_INT8) return fail(FP_ERR_INVALID_ARG, "bad kv quant %d", kvq);
     if (s->n_layers <= 0 || s->hidden <= 0 || s->n_heads <= 0 || s->n_kv_heads <= 0 ||
         s->head_dim <= 0 || s->ffn <= 0 || s->max_batch <= 0 || s->max_prompt <= 0 || s->max_seq <= 0)
@@ -252,7 +253,7 @@ fp_status validate_shape(const fp_shape* s, int wq, int kvq) {
     if (s->vocab < 0 || s->vocab % 16 != 0)
         return fail(FP_ERR_INVALID_ARG, "vocab %d must be 0 or a positive multiple of 16", s->vocab);
     const int q_dim = s->n_heads * s->head_dim;
-    const int mult = (wq == FP_WQ_INT4_G128) ? 128 : 16;
+    const int mult = (wq == FP_WQ_INT4_G128) ? 128 : (wq == FP_WQ_BF16_2OF4 ? 64 : 16);
     if (s->hidden % mult || q_dim % mult || s->ffn % mult)
         return fail(FP_ERR_INVALID_ARG, "hidden (%d), n_heads*head_dim (%d) and ffn (%d) must be multiples of %d",
                     s->hidden, q_dim, s->ffn, mult);
@@ -278,6 +279,10 @@ fp_status alloc_mat(fp_layer* h, Mat* m, int N, int K, int wf) {
     m->kst = (K + KS - 1) / KS;
     const size_t nk = (size_t)N * K;
     fp_status st;
+    if (wf == W_SP24) {        // 32-row x 32-input blocks: 1 KiB of values, 128 B of index words
+        if ((st = dev_alloc(h, &m->codes, (size_t)(N / 32) * m->kst * 1024, &h->bytes_w))) return st;
+        return alloc_t(h, &m->sidx, (size_t)(N / 32) * m->kst * 64, &h->bytes_w);
+    }
     if ((st = dev_alloc(h, &m->codes, (size_t)(N / 16) * m->kst * 1024, &h->bytes_w))) return st;
     if (wf == W_INT8) return alloc_t(h, &m->scales, (size_t)N, &h->bytes_w);
     if (wf == W_INT4) {
@@ -297,6 +302,10 @@ fp_status synth_rows(fp_layer* h, Mat* m, int row0, int n, int layer, int tensor
     const int64_t cnt = (int64_t)n * K;
     const int KS = weight_kstep(m->wf), eb = weight_ebits(m->wf);
     HIPCHK(launch_fill_bf16(tmp, cnt, key, 0.f, 0.02f, 0));
+    if (m->wf == W_SP24) {
+        HIPCHK(launch_sp24_compress(tmp, n, K, (uint16_t*)m->codes, m->sidx, row0, 0));
+        return FP_OK;
+    }
     const void* src = tmp;
     if (m->wf == W_INT8) {
         HIPCHK(launch_quant_int8(tmp, n, K, (int8_t*)tmpq, m->scales + row0, 0));
@@ -389,7 +398,13 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
 // and the consumer reads back (ks * M * N floats each way, at about 5 TB/s, against a
 // chunk time of the workgroup's weight bytes at about 25 GB/s per compute unit).
 constexpr int NCU = 256;
+void plan_sp24(const Mat& m, int M, int* ks_out, int* kr_out);
+
 void plan_skinny_batch(const fp_layer* h, const Mat& m, int M, int dual_F, int* ks_out, int* kr_out) {
+    if (m.wf == W_SP24) {
+        plan_sp24(m, M, ks_out, kr_out);
+        return;
+    }
     const int KC = skinny_batch_chunk();
     const int nch = (m.K + KC - 1) / KC;
     (void)h;
@@ -411,8 +426,38 @@ void plan_skinny_batch(const fp_layer* h, const Mat& m, int M, int dual_F, int* 
     *ks_out = (nch + per - 1) / per;
 }
 
+// Split of a 2:4 sparse decode projection: about TARGET_WG workgroups of 128 rows, within
+// the LDS bound on the staged activation slice.
+void plan_sp24(const Mat& m, int M, int* ks_out, int* kr_out) {
+    const int nsteps = m.K / 32;
+    const int tiles = (m.N + 127) / 128;
+    const int maxsteps = sp24_max_krange(M) / 32;
+    int ks = std::max(1, std::min((TARGET_WG + tiles - 1) / tiles, std::max(1, nsteps / 4)));
+    int per = (nsteps + ks - 1) / ks;
+    if (per > maxsteps) per = maxsteps;
+    *kr_out = per * 32;
+    *ks_out = (nsteps + per - 1) / per;
+}
+
 fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, float* part,
                            int* ks_out, hipStream_t st) {
+    if (m.wf == W_SP24) {      // the [gate; up] matrix is a plain [2F, K] matrix here
+        Sp24Args a{};
+        a.X = X;
+        a.Wv = (const uint16_t*)m.codes;
+        a.Wi = m.sidx;
+        a.M = M;
+        a.N = m.N;
+        a.K = m.K;
+        a.kst = m.kst;
+        a.part = part;
+        int ks;
+        plan_sp24(m, M, &ks, &a.krange);
+        if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
+        HIPCHK(launch_sp24_gemv(a, ks, st));
+        *ks_out = ks;
+        return FP_OK;
+    }
     SkinnyArgs a{};
     a.X = X;
     a.W = m.codes;
@@ -436,6 +481,23 @@ fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, 
 
 fp_status run_gemm(fp_layer* h, const uint16_t* X, const Mat& m, int M, int epi, float* out32,
                    uint16_t* out16, const uint16_t* resid, hipStream_t st) {
+    if (m.wf == W_SP24) {
+        Sp24Args a{};
+        a.X = X;
+        a.Wv = (const uint16_t*)m.codes;
+        a.Wi = m.sidx;
+        a.M = M;
+        a.N = m.N;
+        a.K = m.K;
+        a.F = h->s.ffn;
+        a.kst = m.kst;
+        a.out32 = out32;
+        a.out16 = out16;
+        a.resid = resid;
+        a.out_fmt = h->act_fmt;
+        HIPCHK(launch_gemm_sp24(a, epi, st));
+        return FP_OK;
+    }
     GemmArgs a{};
     a.X = X;
     a.W = m.codes;
@@ -487,7 +549,7 @@ RopeKvArgs rope_args(fp_layer* h, int l, const float* part, int ks, int M, int T
 // workgroup, which bounds the hidden size.
 int prefill_split(const fp_layer* h, int M, int N, int K, int dual_F, int* krange) {
     const int H = h->s.hidden;
-    if (H % 8 != 0 || H > 16384) return 1;
+    if (H % 8 != 0 || H > 16384 || h->wq == FP_WQ_BF16_2OF4) return 1;
     return gemm_split_factor(M, N, K, dual_F, h->wq, krange);
 }
 
@@ -725,8 +787,11 @@ fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipS
     return FP_OK;
 }
 
+// 2:4 sparse weights run every batch size, one sequence included, on the batch schedule
+// (their projection kernel stages plain activations).
 fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
-    return h->B == 1 ? enqueue_decode_single(h, x, y, st) : enqueue_decode_batch(h, x, y, st);
+    return h->B == 1 && h->wq != FP_WQ_BF16_2OF4 ? enqueue_decode_single(h, x, y, st)
+                                                 : enqueue_decode_batch(h, x, y, st);
 }
 
 // Final RMSNorm, LM head and greedy argmax of position T - 1 of each of B sequences of
@@ -763,7 +828,7 @@ void decode_scratch_floats(const fp_layer* h, int B, size_t* part, size_t* part2
     const fp_shape& s = h->s;
     const LayerW& W = h->L[0];
     int kq, ko, kg, kd, kr;
-    if (B == 1) {
+    if (B == 1 && h->wq != FP_WQ_BF16_2OF4) {
         plan_skinny(h, W.qkv, B, 0, &kq, &kr);
         plan_skinny(h, W.o, B, 0, &ko, &kr);
         plan_skinny(h, W.gu, B, s.ffn, &kg, &kr);
@@ -952,7 +1017,7 @@ static fp_status create_impl(const fp_shape* shape, fp_weight_quant wq, fp_kv_qu
     h->kvq = kvq;
     h->seed = seed;
     h->unbacked = unbacked;
-    h->act_fmt = (wq == FP_WQ_BF16) ? ACT_BF16 : ACT_F16;
+    h->act_fmt = (wq == FP_WQ_BF16 || wq == FP_WQ_BF16_2OF4) ? ACT_BF16 : ACT_F16;
     const fp_shape& s = h->s;
     h->q_dim = s.n_heads * s.head_dim;
     h->kv_dim = s.n_kv_heads * s.head_dim;
@@ -1413,6 +1478,31 @@ fp_status fp_export_weight(fp_layer* h, int32_t l, int32_t tensor, void* codes, 
         default: return fail(FP_ERR_INVALID_ARG, "unknown tensor id %d", tensor);
     }
     const int K = m->K, wf = m->wf;
+    if (wf == W_SP24) {
+        // value and index blocks -> dense bf16 rows (pruned weights zero)
+        HIPCHK(hipDeviceSynchronize());
+        const size_t nblk = (size_t)(n / 32) * m->kst;
+        std::vector<uint16_t> vals(nblk * 512), idx(nblk * 64);
+        HIPCHK(hipMemcpy(vals.data(), (const uint16_t*)m->codes + (size_t)(row0 / 32) * m->kst * 512, vals.size() * 2,
+                         hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(idx.data(), m->sidx + (size_t)(row0 / 32) * m->kst * 64, idx.size() * 2,
+                         hipMemcpyDeviceToHost));
+        uint16_t* dst = (uint16_t*)codes;
+        std::memset(dst, 0, (size_t)n * K * 2);
+        for (int rb = 0; rb < n / 32; ++rb)
+            for (int kb = 0; kb < m->kst; ++kb)
+                for (int L = 0; L < 64; ++L) {
+                    const size_t b = (size_t)rb * m->kst + kb;
+                    const int r = 32 * rb + (L & 31), s = L >> 5;
+                    const uint32_t word = idx[b * 64 + L];
+                    for (int i = 0; i < 8; ++i) {
+                        const int g = i / 2, pos = (word >> (2 * i)) & 3;
+                        const int k = 32 * kb + (g < 2 ? 0 : 16) + 8 * s + 4 * (g & 1) + pos;
+                        dst[(size_t)r * K + k] = vals[b * 512 + L * 8 + i];
+                    }
+                }
+        return FP_OK;
+    }
     if (wf != W_BF16 && !scales) return fail(FP_ERR_INVALID_ARG, "scales is NULL");
     if (wf == W_INT4 && !zeros) return fail(FP_ERR_INVALID_ARG, "zeros is NULL");
     HIPCHK(hipDeviceSynchronize());

@@ -30,7 +30,7 @@ extern thread_local LaunchTimer g_launch_timer;
         }                                                                                      \
     } while (0)
 
-enum WFmt { W_BF16 = 0, W_INT8 = 1, W_INT4 = 2 };
+enum WFmt { W_BF16 = 0, W_INT8 = 1, W_INT4 = 2, W_SP24 = 3 };
 // EPI_PART: fp32 partial sums of one k-split, [ks, M, N] (or [ks, M, 2F] for the
 // [gate; up] matrix), multiplied by the int8 row scales; a reduction kernel finishes.
 enum Epi { EPI_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PART = 3 };
@@ -163,8 +163,9 @@ struct AttnPreArgs {
 
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint64_t key, float mean, float sigma,
                             hipStream_t st);
-// Fragment-major weight layout (see tile_kernel): KS = k per 1 KiB block row-slice.
-inline int weight_kstep(int wf) { return wf == W_BF16 ? 32 : (wf == W_INT8 ? 64 : 128); }
+// Fragment-major weight layout (see tile_kernel): KS = k per 1 KiB block row-slice (2:4 sparse
+// weights: 32 rows x 32 inputs per 1 KiB block, see sparse.hip).
+inline int weight_kstep(int wf) { return wf == W_BF16 ? 32 : (wf == W_INT8 ? 64 : (wf == W_INT4 ? 128 : 32)); }
 inline int weight_ebits(int wf) { return wf == W_BF16 ? 16 : (wf == W_INT8 ? 8 : 4); }
 hipError_t launch_tile(const void* src, int n, int K, int ebits, int KS, void* dst, int row0, hipStream_t st);
 hipError_t launch_quant_int8(const uint16_t* w, int N, int K, int8_t* codes, uint16_t* scales,
@@ -213,6 +214,29 @@ void attn_decode_split(int max_seq, int B, int nkv, int group, int* nsplit, int*
 bool attn_decode_supported(int d, int group);
 hipError_t launch_attn_decode(const AttnDecArgs& a, int B, hipStream_t st);
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st);
+
+// 2:4 sparse weights (sparse.hip): values in 32-row x 32-input blocks of 1 KiB (the 64
+// lanes' 16-byte operand pieces of the sparse MFMA) and 16-bit index words in 128-byte
+// blocks, both block-row-major over K / 32 blocks.
+struct Sp24Args {
+    const uint16_t* X;        // activations bf16 [M, K]
+    const uint16_t* Wv;       // value blocks
+    const uint16_t* Wi;       // index blocks
+    int M, N, K, F;           // F: SwiGLU width (N = 2F rows of [gate; up])
+    int kst;                  // blocks per 32-row block row (K / 32)
+    int krange;               // decode: k per split (multiple of 32)
+    float* part;              // decode: [ks, M, N]
+    float* out32;             // prefill EPI_F32: [M, N]
+    uint16_t* out16;          // prefill EPI_RESID: bf16 [M, N]; EPI_SWIGLU: act [M, F]
+    const uint16_t* resid;    // prefill EPI_RESID: bf16 [M, N]
+    int out_fmt;
+    int tiles_m, tiles_n;     // set by the launcher
+};
+hipError_t launch_sp24_compress(const uint16_t* w, int n, int K, uint16_t* vals, uint16_t* idx, int row0,
+                                hipStream_t st);
+int sp24_max_krange(int M);
+hipError_t launch_sp24_gemv(const Sp24Args& a, int ks, hipStream_t st);
+hipError_t launch_gemm_sp24(const Sp24Args& a, int epi, hipStream_t st);
 
 // The blocks outside the hidden layers (head.hip).
 hipError_t launch_embed(const int* ids, int64_t M, const uint16_t* E, int V, int H, uint16_t* x, hipStream_t st);

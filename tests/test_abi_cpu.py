@@ -46,6 +46,8 @@ def _create_status(shape, wq=0, kvq=0, unbacked=True):
     (dict(max_prompt=64, max_seq=48), 0, -1),
     (dict(rms_eps=0.0), 0, -1),
     (dict(n_layers=0), 0, -1),
+    (dict(hidden=288, n_heads=4, head_dim=64), 3, -1),   # 2:4 sparse: hidden 288 not a multiple of 64
+    (dict(ffn=416), 3, -1),                              # nor ffn 416
 ])
 def test_shape_validation(kw, wq, code):
     base = dict(n_layers=1, hidden=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn=384,
@@ -150,11 +152,14 @@ def _hand_weight_bytes(s, wq):
     and one k-step of 32 bf16 / 64 int8 / 128 int4 inputs (k padded to whole steps);
     int8 adds an fp16 scale per row; int4 an fp16 scale, an fp16 zero and a packed u32
     scale|zero word per (row, group of 128).  Plus two bf16 gains of hidden."""
-    ks = {"bf16": 32, "int8": 64, "int4": 128}[wq]
+    ks = {"bf16": 32, "int8": 64, "int4": 128, "sp24": 32}[wq]
     qd, kd = s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
     mats = [(qd + 2 * kd, s.hidden), (s.hidden, qd), (2 * s.ffn, s.hidden), (s.hidden, s.ffn)]
     per_layer = 2 * s.hidden * 2
     for N, K in mats:
+        if wq == "sp24":          # 32 x 32 blocks: 1 KiB of kept values + 128 B of index words
+            per_layer += (N // 32) * (K // 32) * (1024 + 128)
+            continue
         per_layer += (N // 16) * (-(-K // ks)) * 1024
         if wq == "int8":
             per_layer += N * 2
@@ -175,7 +180,7 @@ def _hand_kv_bytes(s, kvq):
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama2-7b-bf16", "llama2-7b-int8", "llama2-13b-int4",
-                                  "llama2-70b-tp8-int4"])
+                                  "llama2-70b-tp8-int4", "llama2-7b-sp24"])
 def test_memory_bytes_match_the_storage_layout(name):
     c = CONFIGS[name]
     s = c["shape"]
@@ -201,6 +206,9 @@ def test_memory_bytes_scale_with_weight_format_and_layers():
     gains = s.n_layers * 2 * s.hidden * 2
     assert abs((w8 - gains) / (wb - gains) - 0.5) < 1e-3
     assert abs((w4 - gains) / (wb - gains) - (0.25 + 8 / 256)) < 1e-3
+    # 2:4 sparsity (Sec. 3.3): half the bf16 values plus 2 bits per kept value
+    ws = _planned_bytes(s, "sp24", "bf16")[0]
+    assert abs((ws - gains) / (wb - gains) - 9 / 16) < 1e-9
     one = [_planned_bytes(dataclasses.replace(s, n_layers=n), "int4", "int8") for n in (1, 2, 3)]
     for i in range(2):       # weights and KV are linear; the workspace does not grow with layers
         assert one[2][i] - one[1][i] == one[1][i] - one[0][i]

@@ -82,3 +82,19 @@ def test_cpu_baseline_sample_reports_the_host(monkeypatch):
     assert r["kind"] == "oracle" and r["unit"] == "tokens/s" and r["value"] > 0
     assert r["cores"] >= 1 and r["nproc"] >= 1 and isinstance(r["cpu_model"], str)
     assert "1 of 3 layers" in r["sample"] and "float32" in r["sample"]
+
+
+def test_sparse_bytes_and_flops_by_hand():
+    """2:4 sparse weights: half the weights kept as bf16 with a 2-bit position each (9/16 of
+    the dense bf16 bytes); the prefill's projection work is that of the kept half."""
+    c = CONFIGS["llama2-7b-sp24"]
+    s = c["shape"]
+    H, F = 4096, 11008
+    w_dense = (3 * H * H + H * H + 2 * F * H + H * F)
+    assert bench.weight_bytes(3 * H, H, "sp24") == 3 * H * H * 1.125
+    b_sp = bench.decode_step_bytes(s, "sp24", "bf16", 1, 512)
+    b_bf = bench.decode_step_bytes(s, "bf16", "bf16", 1, 512)
+    assert b_bf - b_sp == 2 * w_dense * (2 - 1.125)
+    P = 512
+    attn = 4 * 128 * 32 * (P * (P + 1) // 2)
+    assert bench.prefill_flops(s, 1, P, "sp24") == 2 * (2 * P * w_dense // 2 + attn)

@@ -23,14 +23,14 @@ import pytest
 import fpgen
 from fpgen.workloads import CONFIGS
 from oracle.layer import Fingerprint as OracleFingerprint, TENSOR_ID, weight_shapes
-from oracle.quant import quant_kv_int8, quant_int8_channel, quant_int4_g128, pack_int4
+from oracle.quant import quant_kv_int8, quant_int8_channel, quant_int4_g128, pack_int4, prune_2of4
 from tests.gpu_harness import TOL, log, run_parity, rel_inf
 
 pytestmark = pytest.mark.gpu
 
 # sampled sequences per workload: the oracle's cost grows with each one
 FULL = [("llama2-7b-bf16", None), ("llama2-7b-int8", (0, 15)), ("llama2-13b-int4", (31,)),
-        ("llama2-70b-tp8-int4", (0, 63))]
+        ("llama2-70b-tp8-int4", (0, 63)), ("llama2-7b-sp24", (0, 15))]
 CHAIN_DRIFT_FACTOR = 1.5
 
 
@@ -144,6 +144,9 @@ def _oracle_rows(wq, seed, layer, name, N, K, rows):
                   for r in rows])
     if wq == "bf16":
         return (w.view(np.uint32) >> 16).astype(np.uint16), None, None
+    if wq == "sp24":
+        d = np.where(prune_2of4(w), w, np.float32(0)).astype(np.float32)
+        return (d.view(np.uint32) >> 16).astype(np.uint16), None, None
     if wq == "int8":
         c, sc = quant_int8_channel(w)
         return c, sc, None

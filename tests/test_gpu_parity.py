@@ -42,7 +42,7 @@ WSHAPE = Shape(n_layers=2, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn
                max_batch=2, max_prompt=16, max_seq=24)
 
 
-@pytest.mark.parametrize("wq", ["bf16", "int8", "int4"])
+@pytest.mark.parametrize("wq", ["bf16", "int8", "int4", "sp24"])
 def test_weight_codes_bit_exact(wq):
     from paper_2501_13111_amd import Fingerprint
     log(f"weight codes {wq}")
@@ -56,7 +56,7 @@ def test_weight_codes_bit_exact(wq):
             for name in ("q", "k", "v", "o", "gate", "up", "down"):
                 c, s, z = fp.export_weight(l, name)
                 oc, os_, oz = orc.export_weight(l, name)
-                if wq == "bf16":
+                if wq in ("bf16", "sp24"):
                     assert np.array_equal(c, (oc.view(np.uint32) >> 16).astype(np.uint16)), (l, name)
                 elif wq == "int8":
                     assert np.array_equal(c, oc), (l, name)
@@ -109,6 +109,12 @@ CASES = [
     ("splitk-bf16", Shape(2, 512, 4, 4, 128, 1024, 2, 160, 164), "bf16", "bf16", 2, 160, 2),
     ("splitk-int4-int8kv", Shape(2, 1024, 8, 8, 128, 2048, 2, 160, 164), "int4", "int8", 2, 160, 2),
     ("splitk-int8-gqa", Shape(2, 1024, 8, 4, 128, 2048, 1, 300, 302), "int8", "int8", 1, 300, 2),
+    # 2:4 sparse weights on the sparse MFMA: one sequence (batch schedule), a ragged 128-row
+    # weight tile (hidden 576) under GQA 3:1, 40 sequences (two 32-token tiles in decode,
+    # ragged 128-token prefill tiles), and an int8 cache
+    ("sp24-single-gqa3", Shape(2, 576, 9, 3, 64, 704, 1, 70, 76), "sp24", "bf16", 1, 70, 4),
+    ("sp24-batch3", Shape(1, 1024, 8, 8, 128, 2048, 3, 130, 134), "sp24", "bf16", 3, 130, 3),
+    ("sp24-batch40-int8kv", Shape(2, 512, 4, 4, 128, 1024, 40, 50, 54), "sp24", "int8", 40, 50, 3),
 ]
 
 
