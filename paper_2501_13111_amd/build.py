@@ -53,7 +53,9 @@ def build(verbose: bool = False, out: str | None = None, defines: dict | None = 
         objs = list(ex.map(lambda s: _compile(s, hipcc, build_dir, extra), srcs))
     LIB_ = lib
     tmp = LIB_ + ".tmp"
-    cmd = [hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", *objs, "-o", tmp]
+    # -z defs: an unresolved symbol (e.g. a kernel whose host stub was not emitted) fails the
+    # link instead of the first load
+    cmd = [hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", "-Wl,-z,defs", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

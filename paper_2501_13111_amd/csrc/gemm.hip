@@ -342,7 +342,8 @@ hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st)
 // accumulators instead: a stage is one 128-input group, and a lane's accumulators of a
 // 32x32 tile all belong to one output column (one scale), so before each stage the lane
 // re-expresses them in units of that stage's scale (acc *= s_prev / s_cur) and the
-// epilogue multiplies by the last one.  No weight is rounded to fp16.
+// epilogue multiplies by the last one.  No weight is rounded to fp16.  The fragments take
+// one shift per word (i4x8_to_f16x8_q).
 typedef __attribute__((address_space(3))) void lvoid_t;
 
 constexpr int BT = 256;
@@ -361,6 +362,24 @@ struct BigT {
     static constexpr int EPI_BYTES = 8 * 64 * 72 * 4;
     static constexpr int SMEM = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
 };
+
+// Eight int4 codes of one word (device nibble order) -> exact fp16 q - z, one shift: the
+// nibbles in bits 0-3 of each 16-bit half become fp16 1024 + q (exponent 0x64), those in bits
+// 4-7 become 64 + q (exponent 0x54, whose ulp is 1/16); b1024 = 1024 + z, b64 = 64 + z.
+// Same values, in the same order, as i4x8_to_f16x8.
+__device__ __forceinline__ u32x4 i4x8_to_f16x8_q(uint32_t w, f16x2 b1024, f16x2 b64) {
+    const uint32_t w8 = w >> 8;
+    const uint32_t p0 = and_or(w, 0x000F000Fu, 0x64006400u);
+    const uint32_t p1 = and_or(w, 0x00F000F0u, 0x54005400u);
+    const uint32_t p2 = and_or(w8, 0x000F000Fu, 0x64006400u);
+    const uint32_t p3 = and_or(w8, 0x00F000F0u, 0x54005400u);
+    u32x4 r;
+    r.x = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, p0) - b1024);
+    r.y = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, p1) - b64);
+    r.z = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, p2) - b1024);
+    r.w = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, p3) - b64);
+    return r;
+}
 
 template <int CPR>
 __device__ __forceinline__ int a_swz(int row) { return CPR == 8 ? ((row >> 1) & 7) : (row & 15); }
@@ -411,8 +430,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
 
     uint32_t nsz[2], csz[2];       // int4: scale | zero << 16 of the lane's two columns, next / current stage
     float s_unit[2] = {1.f, 1.f};  // int4: the scale the lane's accumulators of column tile j are in
-    f16x2 qbias[2];                // int4: fp16 1024 + z of the current group (1024 for a zero scale)
-    bool qzero[2] = {false, false};// int4: the current group's scale is zero (its weights are zero)
+    f16x2 qbias[2], qbias64[2];    // int4: fp16 1024 + z and 64 + z of the current group
 
     // Copies of one stage, issued in parts from inside the previous stage's MFMA loop so
     // that no wave stalls on a burst of copies.  They go through buffer resources: rows
@@ -421,9 +439,6 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     constexpr int NA = BT * T::CPR / 512;            // A copies per thread per stage
     constexpr int NB = 16 * T::NBLK / 8;             // B copies per thread per stage
     constexpr int NPART = T::TK / 16;                // parts = 16-k MFMA steps of a stage
-    const __amdgpu_buffer_rsrc_t xres = buf_rsrc(a.X, (uint32_t)min((int64_t)a.M * a.K * 2, (int64_t)0xFFFFFFF0));
-    const __amdgpu_buffer_rsrc_t wres = buf_rsrc(a.W, (uint32_t)min((int64_t)(DUAL ? 2 * nrb : nrb) * a.kst * 1024,
-                                                                    (int64_t)0xFFFFFFF0));
     uint32_t aoff[NA];
     int akc[NA];
 #pragma unroll
@@ -443,22 +458,35 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
         const int gb = grow_block(blk / T::NBLK, v);
         boff[i] = v ? (uint32_t)((((int64_t)gb * a.kst + bkb[i]) * 64 + lane) * 16) : BUF_OOB;
     }
+    // When K is a whole number of stages (every k of every stage exists), the k advance goes
+    // into the buffer resources (uniform: base moved forward, size cut by as much) and the
+    // per-lane offsets stay fixed; the past-the-end offsets of rows past M and of blocks
+    // past the matrix stay past the end.
+    const bool kwhole = a.K % T::TK == 0;
+    const uint32_t xbytes = (uint32_t)min((int64_t)a.M * a.K * 2, (int64_t)0xFFFFFFF0);
+    const uint32_t wbytes = (uint32_t)min((int64_t)(DUAL ? 2 * nrb : nrb) * a.kst * 1024, (int64_t)0xFFFFFFF0);
     auto issue_part = [&](int stage, int k0, int q) {
         char* sA = smem + stage * T::STAGE;
         char* sB = sA + T::A_BYTES;
+        const uint32_t xadv = kwhole ? 2u * (uint32_t)k0 : 0u;
+        const uint32_t wadv = kwhole ? (uint32_t)(k0 / T::KSW) * 1024u : 0u;
+        const __amdgpu_buffer_rsrc_t xr = buf_rsrc((const char*)a.X + xadv, xbytes - xadv);
+        const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)a.W + wadv, wbytes - wadv);
 #pragma unroll
         for (int i = 0; i < NA; ++i)
             if ((i * NPART) / NA == q) {
-                const uint32_t off = (aoff[i] != BUF_OOB && k0 + akc[i] < a.K) ? aoff[i] + 2u * k0 : BUF_OOB;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lvoid_t*)(sA + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
+                const uint32_t off =
+                    kwhole ? aoff[i] : ((aoff[i] != BUF_OOB && k0 + akc[i] < a.K) ? aoff[i] + 2u * k0 : BUF_OOB);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lvoid_t*)(sA + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
             }
 #pragma unroll
         for (int i = 0; i < NB; ++i)
             if ((i * NPART) / NB == q) {
-                const int kblk = k0 / T::KSW + bkb[i];
                 const uint32_t off =
-                    (boff[i] != BUF_OOB && kblk < a.kst) ? boff[i] + (uint32_t)(k0 / T::KSW) * 1024u : BUF_OOB;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lvoid_t*)(sB + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
+                    kwhole ? boff[i]
+                           : ((boff[i] != BUF_OOB && k0 / T::KSW + bkb[i] < a.kst)
+                                  ? boff[i] + (uint32_t)(k0 / T::KSW) * 1024u : BUF_OOB);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lvoid_t*)(sB + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
             }
         if constexpr (WF == W_INT4) {
             if (q == 0) {
@@ -492,25 +520,31 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     // multiply stage `stage` out of LDS; with nk0 >= 0, issue the copies of the stage at
     // k offset nk0 into the other buffer, two parts per 16-k step over the first half of
     // the steps (the second half covers their latency before the stage's closing wait)
+    // int4: the stage is one group; the accumulators go to units of its scale, and the
+    // biases that turn the extracted nibbles into q - z are set (two per column: nibbles in
+    // bits 0-3 of an fp16 half read as 1024 + q, in bits 4-7 with exponent 0x54 as 64 + q)
+    // A group whose scale is zero (its weights dequantise to zero) gets the unit 2^-64: the
+    // accumulators are scaled up by s_prev * 2^64 and the group's own contribution, taken in
+    // that unit, ends up 2^-64 / s_next of the value -- some 1e-18 of it, far below the
+    // accumulators' rounding -- with no per-fragment work.
+    auto regroup = [&]() {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const float sc = h2f((uint16_t)(csz[j] & 0xFFFFu));
+            const float s_new = sc == 0.f ? 0x1p-64f : sc;
+            const float ratio = s_unit[j] / s_new;
+            s_unit[j] = s_new;
+            const float z = h2f((uint16_t)(csz[j] >> 16));
+            const _Float16 b0 = (_Float16)(1024.0f + z), b1 = (_Float16)(64.0f + z);
+            qbias[j] = f16x2{b0, b0};
+            qbias64[j] = f16x2{b1, b1};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i][j] *= ratio;
+        }
+    };
     auto compute = [&](int stage, int nk0) {
         const char* sA = smem + stage * T::STAGE;
         const char* sB = sA + T::A_BYTES;
-        if constexpr (WF == W_INT4) {
-            // the stage is one group: accumulators to units of its scale
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const float sc = h2f((uint16_t)(csz[j] & 0xFFFFu));
-                qzero[j] = sc == 0.f;
-                const float s_new = qzero[j] ? s_unit[j] : sc;
-                const float ratio = s_unit[j] / s_new;
-                s_unit[j] = s_new;
-                const _Float16 bz = qzero[j] ? (_Float16)1024.0f
-                                             : (_Float16)(1024.0f + h2f((uint16_t)(csz[j] >> 16)));
-                qbias[j] = f16x2{bz, bz};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i][j] *= ratio;
-            }
-        }
 #pragma unroll
         for (int kk = 0; kk < T::TK / 16; ++kk) {            // 16-k MFMA steps
             if (nk0 >= 0 && kk < T::TK / 32) {
@@ -538,10 +572,9 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                     bop[j] = u32x4{c0.x, c0.y, c1.x, c1.y};
                 } else {
                     // one 128-k block: lane r + 16 g holds k 32 g .. 32 g + 31, 8 per dword
-                    // exact q - z (a zero-scale group contributes nothing: codes 0, bias 1024)
-                    uint32_t wd = *(const uint32_t*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 4 * (2 * hh + h32));
-                    if (qzero[j]) wd = 0u;
-                    bop[j] = i4x8_to_f16x8(wd, qbias[j]);
+                    // exact q - z
+                    const uint32_t wd = *(const uint32_t*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 4 * (2 * hh + h32));
+                    bop[j] = i4x8_to_f16x8_q(wd, qbias[j], qbias64[j]);
                 }
             }
 #pragma unroll
@@ -563,7 +596,9 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
 #pragma unroll
             for (int j = 0; j < 2; ++j) csz[j] = nsz[j];
         }
-        compute(kt & 1, kt + 1 < nk ? kb + (kt + 1) * T::TK : -1);
+        const int nk0 = kt + 1 < nk ? kb + (kt + 1) * T::TK : -1;
+        if constexpr (WF == W_INT4) regroup();
+        compute(kt & 1, nk0);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
