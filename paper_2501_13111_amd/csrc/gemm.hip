@@ -39,7 +39,8 @@ constexpr int GBN = 128, GBK = 64, GPAD = 8;
 #define GEMM_BIG_MIN_TILES 128   // 256 x 256 tiles from this many
 #endif
 #ifndef GEMM_GM
-#define GEMM_GM 8                // tile rows per group of the grouped raster
+#define GEMM_GM 2                // tile rows per group of the grouped raster (256-row tiles: a
+                                 // group keeps 2 activation row-tiles per XCD in flight)
 #endif
 #ifndef GEMM_SMALL_TILES
 #define GEMM_SMALL_TILES 256
