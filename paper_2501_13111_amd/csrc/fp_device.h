@@ -192,6 +192,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uin
 __device__ __forceinline__ u32x4 buf_load_nt(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
 }
+// LDS pointer type of the buffer-to-LDS copy builtin
+typedef __attribute__((address_space(3))) void lvoid_t;
 constexpr uint32_t BUF_OOB = 0xFFFFFFF0u;   // an offset past the end of every resource
 
 // off if live, else BUF_OOB.  The mask passes through an empty asm statement, so the

@@ -345,7 +345,6 @@ hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st)
 // re-expresses them in units of that stage's scale (acc *= s_prev / s_cur) and the
 // epilogue multiplies by the last one.  No weight is rounded to fp16.  The fragments take
 // one shift per word (i4x8_to_f16x8_q).
-typedef __attribute__((address_space(3))) void lvoid_t;
 
 constexpr int BT = 256;
 template <int WF>
