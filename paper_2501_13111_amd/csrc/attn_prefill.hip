@@ -25,10 +25,11 @@
 // first key block (taken exactly, across the two lane halves) is the reference m for all
 // later blocks, whose probabilities exp2(s - m) may then exceed 1.  Softmax does not
 // depend on m and bf16 probabilities keep their relative precision over the fp32 range, so
-// only overflow matters: a block with a probability above 2^64 records its exact maximum,
-// and the workgroup repeats the prompt once with the larger reference.  The loop never
-// rescales the accumulators, and its P.V MFMAs sit on a single path, so they accumulate in
-// place.  Each lane half keeps its own partial sum, added once at the end.
+// only overflow matters: a block with a probability above a.pmax (2^64: bf16 probabilities,
+// fp32 accumulators) records its exact maximum, and the workgroup repeats the prompt once
+// with the larger reference.  The loop never rescales the accumulators, and its P.V MFMAs
+// sit on a single path, so they accumulate in place.  Each lane half keeps its own partial
+// sum, added once at the end.
 //
 // int8 caches: K codes are scaled into fp16 on the way to LDS (code * s_k / kappa, kappa =
 // the largest key scale of the prompt; fp16 MFMA with the queries in fp16, kappa folded
@@ -65,7 +66,6 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     // pieces per thread per block: int8, 4D 8-code pieces of K and as many of V; bf16, one
     // 16-byte piece per lane of each chunk
     constexpr int NPT = KV8 ? (4 * D + NT - 1) / NT : (CH * 64 + NT - 1) / NT;
-    constexpr float PMAX = 0x1p64f;             // bf16 probabilities, fp32 accumulators
     __shared__ __attribute__((aligned(1024))) char smem[NBUF * SB];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -312,7 +312,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
             psum += x0 + x1;
             put_pair(pf, e, x0, x1);
         }
-        if (__ballot(!(pmax <= PMAX))) {
+        if (__ballot(!(pmax <= a.pmax))) {
             asm volatile("" ::: "memory");     // a real branch: never computed speculatively
             m_seen = fmaxf(m_seen, block_max(s, acc, DM));
             over = true;

@@ -23,6 +23,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <tuple>
@@ -35,6 +36,17 @@ using namespace fpk;
 thread_local LaunchTimer fpk::g_launch_timer;
 
 namespace {
+
+// Prefill attention takes probabilities against a fixed reference per query and repeats a
+// prompt once if one would pass this limit (2^64).  FP_ATTN_PROB_LIMIT_LOG2 (1 .. 64)
+// lowers it, so that tests can drive the repeat on ordinary inputs.
+float attn_prob_limit() {
+    const char* e = std::getenv("FP_ATTN_PROB_LIMIT_LOG2");
+    int v = e ? std::atoi(e) : 64;
+    v = v < 1 ? 1 : v > 64 ? 64 : v;
+    return std::ldexp(1.0f, v);
+}
+
 
 thread_local std::string g_err;
 
@@ -613,6 +625,7 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
         aa.nblk = vt_blocks(s.max_seq);
         aa.kv_stride = kv_row_stride(s.max_seq);
         aa.scale = scale;
+        aa.pmax = attn_prob_limit();
         aa.out = h->act_o;
         aa.out_fmt = h->act_fmt;
         h->prof.mark(FP_K_ATTN, l);

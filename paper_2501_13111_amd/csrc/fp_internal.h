@@ -157,6 +157,7 @@ struct AttnPreArgs {
     int kv_int8, P, nh, nkv, d, max_seq, nblk;
     int kv_stride;            // key / scale rows per (sequence, kv head)
     float scale;
+    float pmax;               // largest probability against the reference before a repeat
     uint16_t* out;            // [B*P, nh*d]
     int out_fmt;
 };

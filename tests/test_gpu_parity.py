@@ -380,3 +380,21 @@ def test_parity_large_prefill_tiles(case):
     _report(name, res)
     assert res.prefill_err <= TOL
     assert max(res.decode_errs) <= TOL
+
+
+REPEAT_CASES = [c for c in CASES if c[0] in ("mha-bf16", "gqa8-d128-int4-int8", "long-ctx-bf16", "sp24-batch3")]
+
+
+@pytest.mark.parametrize("case", REPEAT_CASES, ids=[c[0] for c in REPEAT_CASES])
+def test_prefill_attention_repeat_path(case, monkeypatch):
+    """The prefill attention's second pass (a probability against the first block's
+    maximum passing the limit) forced from the host with a limit of 2: most workgroups
+    repeat their prompt with a larger reference, and the result still meets the bar."""
+    name, shape, wq, kvq, B, P, S = case
+    monkeypatch.setenv("FP_ATTN_PROB_LIMIT_LOG2", "1")
+    log(f"case {name} (probability limit 2): {shape} {wq}/{kvq} B={B} P={P} S={S}")
+    res = run_parity(shape, wq, kvq, B, P, S, layerwise=shape.n_layers > 1)
+    _report(name + "-repeat", res)
+    assert res.prefill_err <= TOL
+    assert all(e <= TOL for e in res.layer_errs)
+    assert max(res.decode_errs) <= TOL
