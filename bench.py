@@ -45,7 +45,10 @@ PROJ = {"qkv", "o", "gate_up", "down"}
 # were taken on (hash of the kernel's source files and of its argument block in
 # fp_internal.h); the summaries and commands are in profiles/.
 TRAFFIC = {
-    ("decode_proj", "llama2-7b-bf16"): {"src": "0c9dbcae40e4d6b9", "bytes_per_launch": 102925568},
+    ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "ea8124fbfacc3bad", "bytes_per_launch": 9325581037},
+    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "a81c9ea5d6815384", "bytes_per_launch": 1237241720},
+    ("decode_proj", "llama2-70b-tp8-int4"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 27572483},
+    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "149bcd6e8889c86c", "bytes_per_launch": 60844003},
 }
 FAMILY_SRC = {
     "decode_proj": (("skinny.hip", "fp_device.h"), r"enum XForm \{.*?\n\};\n.*?struct SkinnyArgs \{.*?\n\};"),
@@ -416,6 +419,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=4.0,
                     help="seconds of oracle decode per workload for the CPU baseline")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device to device once (the reference kernel that "
+                         "calibrates rocprofv3's FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this benchmark runs on one GPU; --gpus {args.gpus} is not supported "
@@ -425,6 +431,15 @@ def main():
     import torch
     import paper_2501_13111_amd as P
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_probe > 0:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n}), flush=True)
+        return
     P.load()
 
     headline, names = workload_names()
