@@ -333,7 +333,7 @@ __global__ void __launch_bounds__(D) attn_merge_kernel(AttnDecArgs a, int nsw) {
     a.out[((int64_t)b * a.nh + h) * D + i] = act_store(bfround(o / l), a.out_fmt);
 }
 
-// Splits of the context: about 2048 waves over all (sequence, kv head) pairs for a
+// Splits of the context: about 1024 waves over all (sequence, kv head) pairs for a
 // batch (long waves keep their chunk loads pipelined), fewer for one sequence (fewer
 // partials for the consumer to merge), at least one 32-key block each and four
 // splits per pair when the context has four blocks.  The grid depends only on the
@@ -341,7 +341,7 @@ __global__ void __launch_bounds__(D) attn_merge_kernel(AttnDecArgs a, int nsw) {
 void attn_decode_split(int max_seq, int B, int nkv, int group, int* nsplit, int* keys_per_split) {
     (void)group;
 #ifndef FP_ATTN_WAVES
-#define FP_ATTN_WAVES 2048
+#define FP_ATTN_WAVES 1024
 #endif
     const int target = B == 1 ? 512 : FP_ATTN_WAVES;
     const int want = (target + B * nkv - 1) / (B * nkv);

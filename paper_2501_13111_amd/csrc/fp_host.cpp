@@ -412,7 +412,18 @@ fp_status run_skinny(fp_layer* h, const uint16_t* X, const Mat& m, int M, int du
 constexpr int NCU = 256;
 void plan_sp24(const Mat& m, int M, int* ks_out, int* kr_out);
 
-void plan_skinny_batch(const fp_layer* h, const Mat& m, int M, int dual_F, int* ks_out, int* kr_out) {
+// Bytes of one split of the qkv projection's partial sums that batch decode attention
+// reads beyond their one read: every attention workgroup of a (sequence, kv head) reduces
+// the sums of the group's queries itself.
+double qkv_reread(const fp_layer* h, int B) {
+    const fp_shape& s = h->s;
+    int nsplit = 0, kps = 0;
+    attn_decode_split(s.max_seq, B, s.n_kv_heads, s.n_heads / s.n_kv_heads, &nsplit, &kps);
+    const int nsw = attn_decode_partials(nsplit);
+    return (double)B * s.n_kv_heads * (nsw - 1) * s.n_heads / s.n_kv_heads * s.head_dim * 4.0;
+}
+
+void plan_skinny_batch(const fp_layer* h, const Mat& m, int M, int dual_F, int* ks_out, int* kr_out, double reread = 0.0) {
     if (m.wf == W_SP24) {
         plan_sp24(m, M, ks_out, kr_out);
         return;
@@ -424,7 +435,9 @@ void plan_skinny_batch(const fp_layer* h, const Mat& m, int M, int dual_F, int* 
     const int rows = skinny_batch_rows(m.N, dual_F, m.wf);
     const double bpw = m.wf == W_BF16 ? 2.0 : (m.wf == W_INT8 ? 1.0 : 0.5);
     const double chunk_s = rows * KC * bpw / 25e9;
-    const double split_s = (double)M * (dual_F > 0 ? 2.0 * dual_F : m.N) * 8.0 / 5e12;
+    // each split's partials are written and read once, and `reread` more bytes by a
+    // consumer that reads them several times (decode attention re-reads the queries' sums)
+    const double split_s = ((double)M * (dual_F > 0 ? 2.0 * dual_F : m.N) * 8.0 + reread) / 5e12;
     int per = nch;
     double best = 1e30;
     for (int k = 1; k <= std::min(nch, KSMAX); ++k) {
@@ -452,7 +465,7 @@ void plan_sp24(const Mat& m, int M, int* ks_out, int* kr_out) {
 }
 
 fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, int dual_F, float* part,
-                           int* ks_out, hipStream_t st) {
+                           int* ks_out, hipStream_t st, double reread = 0.0) {
     if (m.wf == W_SP24) {      // the [gate; up] matrix is a plain [2F, K] matrix here
         Sp24Args a{};
         a.X = X;
@@ -484,7 +497,7 @@ fp_status run_skinny_batch(fp_layer* h, const uint16_t* X, const Mat& m, int M, 
     a.part = part;
     a.xf = XF_COPY;
     int ks;
-    plan_skinny_batch(h, m, M, dual_F, &ks, &a.krange);
+    plan_skinny_batch(h, m, M, dual_F, &ks, &a.krange, reread);
     if (ks > KSMAX) return fail(FP_ERR_UNSUPPORTED, "split-K factor %d exceeds %d", ks, KSMAX);
     HIPCHK(launch_skinny_batch(a, m.wf, ks, st));
     *ks_out = ks;
@@ -775,7 +788,7 @@ fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipS
         uint16_t* out = (l == s.n_layers - 1) ? y : h->xbuf;
         float* dump = h->dump ? h->dump + (size_t)l * 2 * B * h->kv_dim : nullptr;
         h->prof.mark(FP_K_QKV, l);
-        if ((rc = run_skinny_batch(h, h->act_in, W.qkv, B, 0, h->part, &ks, st))) return rc;
+        if ((rc = run_skinny_batch(h, h->act_in, W.qkv, B, 0, h->part, &ks, st, qkv_reread(h, B)))) return rc;
         h->prof.mark(FP_K_ATTN, l);
         HIPCHK(launch_attn_decode(attn_args(h, l, ks, B, dump), B, st));
         h->prof.mark(FP_K_O, l);
@@ -847,7 +860,7 @@ void decode_scratch_floats(const fp_layer* h, int B, size_t* part, size_t* part2
         plan_skinny(h, W.gu, B, s.ffn, &kg, &kr);
         plan_skinny(h, W.down, B, 0, &kd, &kr);
     } else {
-        plan_skinny_batch(h, W.qkv, B, 0, &kq, &kr);
+        plan_skinny_batch(h, W.qkv, B, 0, &kq, &kr, qkv_reread(h, B));
         plan_skinny_batch(h, W.o, B, 0, &ko, &kr);
         plan_skinny_batch(h, W.gu, B, s.ffn, &kg, &kr);
         plan_skinny_batch(h, W.down, B, 0, &kd, &kr);
