@@ -109,9 +109,15 @@ __device__ __forceinline__ int qdim(int j, int g) {
     else return 32 * j + 8 * g;
 }
 
+#ifndef ATTN_DEC_PD
+#define ATTN_DEC_PD 2
+#endif
 template <int D, bool KV8>
 struct DecChunk {
     static constexpr int NK = KV8 ? D / 64 : D / 32;   // 16-byte K loads per key tile
+    // chunks in flight per wave (measured: three or four in flight are no faster than
+    // two on the batched workloads, four slower)
+    static constexpr int PD = ATTN_DEC_PD;
     u32x4 k[2][NK];
     typename std::conditional<KV8, u32x2, u32x4>::type v[D / 16];   // int8: 8 codes; bf16: 8 values
     u32x2 ks[2], vs[2];                                 // int8: fp16 scales of keys 16 t + 4 g + i
@@ -272,16 +278,27 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
         }
     };
 
-    // chunks in pairs, ping-ponging two register sets: the next chunk's loads are in
-    // flight while the current one is multiplied
-    DecChunk<D, KV8> ca, cb;
-    if (k_beg < k_end) load(k_beg, ca);
-    for (int base = k_beg; base < k_end; base += 2 * VT_BLK) {
-        if (base + VT_BLK < k_end) load(base + VT_BLK, cb);
-        compute(base, ca);
-        if (base + VT_BLK >= k_end) break;
-        if (base + 2 * VT_BLK < k_end) load(base + 2 * VT_BLK, ca);
-        compute(base + VT_BLK, cb);
+    // the wave's chunks through a ring of PD register sets: PD chunks of loads in flight
+    // while one is multiplied.  Every trip of the main loop issues its loads unconditionally
+    // (past the wave's range: its last chunk again, never used), so the compiler's wait
+    // counts stay exact; the last nch % PD chunks follow without loads.
+    constexpr int PD = DecChunk<D, KV8>::PD;
+    const int nch = k_beg < k_end ? (k_end - k_beg + VT_BLK - 1) / VT_BLK : 0;
+    if (nch > 0) {
+        DecChunk<D, KV8> cr[PD];
+#pragma unroll
+        for (int p = 0; p < PD; ++p) load(k_beg + VT_BLK * min(p, nch - 1), cr[p]);
+        int i = 0;
+        for (; i + PD <= nch; i += PD) {
+#pragma unroll
+            for (int p = 0; p < PD; ++p) {
+                compute(k_beg + VT_BLK * (i + p), cr[p]);
+                load(k_beg + VT_BLK * min(i + p + PD, nch - 1), cr[p]);
+            }
+        }
+#pragma unroll
+        for (int p = 0; p < PD - 1; ++p)
+            if (i + p < nch) compute(k_beg + VT_BLK * (i + p), cr[p]);
     }
 
     // ---- merge the 4 splits of the workgroup: lane (c, g) holds dims 16 dd + 4 g + i of head c
