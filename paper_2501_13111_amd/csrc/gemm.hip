@@ -338,14 +338,23 @@ hipError_t launch_gemm_small(const GemmArgs& a, int wf, int epi, hipStream_t st)
 // MFMA steps of the first half of the current stage.  A rows are stored with an XOR swizzle of their 16-byte
 // chunks so that MFMA fragment reads are free of bank conflicts; weight blocks
 // keep their fragment-major order, so a fragment is one contiguous 1 KiB read.
-// Quantised weights stay packed in LDS and are converted to fp16 per fragment.  For int4
-// the fragments hold the exact integers q - z, and the group scale goes to the fp32
-// accumulators instead: a stage is one 128-input group, and a lane's accumulators of a
-// 32x32 tile all belong to one output column (one scale), so before each stage the lane
-// re-expresses them in units of that stage's scale (acc *= s_prev / s_cur) and the
-// epilogue multiplies by the last one.  No weight is rounded to fp16.  The fragments take
-// one shift per word (i4x8_to_f16x8_q).
+// Quantised weights stay packed in LDS and are converted to fp16 per fragment.  For the
+// int4 qkv projection (fp32 output, whose K / V rows become cache codes) the fragments hold
+// the exact integers q - z, and the group scale goes to the fp32 accumulators instead: a
+// stage is one 128-input group, and a lane's accumulators of a 32x32 tile all belong to
+// one output column (one scale), so before each stage the lane re-expresses them in units
+// of that stage's scale (acc *= s_prev / s_cur) and the epilogue multiplies by the last
+// one; no weight is rounded to fp16.  The other int4 projections (o, [gate; up], down)
+// multiply the exact q - z by the group scale in fp16 instead -- the dequantised weight
+// rounded once to fp16, relative error at most 2^-11 -- which takes one packed multiply
+// per two weights instead of the rescaling of 128 accumulators per lane every stage.  The
+// fragments take one shift per word (i4x8_to_f16x8_q).
 
+// int4 projections other than qkv: weights (q - z) * s rounded to fp16 (0: every int4
+// projection takes the exact scheme)
+#ifndef GEMM_FASTQ
+#define GEMM_FASTQ 1
+#endif
 constexpr int BT = 256;
 template <int WF>
 struct BigT {
@@ -431,6 +440,8 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     uint32_t nsz[2], csz[2];       // int4: scale | zero << 16 of the lane's two columns, next / current stage
     float s_unit[2] = {1.f, 1.f};  // int4: the scale the lane's accumulators of column tile j are in
     f16x2 qbias[2], qbias64[2];    // int4: fp16 1024 + z and 64 + z of the current group
+    f16x2 qs2[2];                  // int4, rounded weights: the group scale, twice
+    constexpr bool EXQ = !GEMM_FASTQ || EPI == EPI_F32;   // int4: exact scheme (qkv)
 
     // Copies of one stage, issued in parts from inside the previous stage's MFMA loop so
     // that no wave stalls on a burst of copies.  They go through buffer resources: rows
@@ -440,65 +451,70 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     constexpr int NB = 16 * T::NBLK / 8;             // B copies per thread per stage
     constexpr int NPART = T::TK / 16;                // parts = 16-k MFMA steps of a stage
     uint32_t aoff[NA];
-    int akc[NA];
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
         const int pp = (i * 8 + w) * 64 + lane;
         const int row = pp / T::CPR, slot = pp % T::CPR;
-        akc[i] = (slot ^ a_swz<T::CPR>(row)) * 8;
-        aoff[i] = m0 + row < a.M ? (uint32_t)(((int64_t)(m0 + row) * a.K + akc[i]) * 2) : BUF_OOB;
+        const int kc = (slot ^ a_swz<T::CPR>(row)) * 8;
+        aoff[i] = m0 + row < a.M ? (uint32_t)(((int64_t)(m0 + row) * a.K + kc) * 2) : BUF_OOB;
     }
     uint32_t boff[NB];
-    int bkb[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
         const int blk = i * 8 + w;
-        bkb[i] = blk % T::NBLK;
         bool v;
         const int gb = grow_block(blk / T::NBLK, v);
-        boff[i] = v ? (uint32_t)((((int64_t)gb * a.kst + bkb[i]) * 64 + lane) * 16) : BUF_OOB;
+        boff[i] = v ? (uint32_t)((((int64_t)gb * a.kst + blk % T::NBLK) * 64 + lane) * 16) : BUF_OOB;
     }
-    // When K is a whole number of stages (every k of every stage exists), the k advance goes
-    // into the buffer resources (uniform: base moved forward, size cut by as much) and the
-    // per-lane offsets stay fixed; the past-the-end offsets of rows past M and of blocks
-    // past the matrix stay past the end.
-    const bool kwhole = a.K % T::TK == 0;
+    // int4: the lane's column of each column tile in the group-major scale / zero words
+    // (-1: past the matrix)
+    int szcol[2] = {-1, -1};
+    if constexpr (WF == W_INT4) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            bool v;
+            const int gb = grow_block(col_rb(2 * j + ((lane & 31) >> 4)), v);
+            szcol[j] = v ? gb * 16 + r : -1;
+        }
+    }
+    // K is a whole number of stages (the launcher sends other K to the small tiling), so
+    // every k of every stage exists: the k advance goes into the buffer resources (uniform:
+    // base moved forward, size cut by as much) and the per-lane offsets stay fixed; the
+    // past-the-end offsets of rows past M and of blocks past the matrix stay past the end.
+    // The LDS destinations are wave-uniform (scalar arithmetic, no per-copy VALU work).
     const uint32_t xbytes = (uint32_t)min((int64_t)a.M * a.K * 2, (int64_t)0xFFFFFFF0);
     const uint32_t wbytes = (uint32_t)min((int64_t)(DUAL ? 2 * nrb : nrb) * a.kst * 1024, (int64_t)0xFFFFFFF0);
+    const int wu = __builtin_amdgcn_readfirstlane(w);
     auto issue_part = [&](int stage, int k0, int q) {
         char* sA = smem + stage * T::STAGE;
         char* sB = sA + T::A_BYTES;
-        const uint32_t xadv = kwhole ? 2u * (uint32_t)k0 : 0u;
-        const uint32_t wadv = kwhole ? (uint32_t)(k0 / T::KSW) * 1024u : 0u;
+        const uint32_t xadv = 2u * (uint32_t)k0;
+        const uint32_t wadv = (uint32_t)(k0 / T::KSW) * 1024u;
         const __amdgpu_buffer_rsrc_t xr = buf_rsrc((const char*)a.X + xadv, xbytes - xadv);
         const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)a.W + wadv, wbytes - wadv);
 #pragma unroll
         for (int i = 0; i < NA; ++i)
             if ((i * NPART) / NA == q) {
-                const uint32_t off =
-                    kwhole ? aoff[i] : ((aoff[i] != BUF_OOB && k0 + akc[i] < a.K) ? aoff[i] + 2u * k0 : BUF_OOB);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lvoid_t*)(sA + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
+                // through a local: an array element passed straight to the builtin left the
+                // kernels' host stubs unemitted (no diagnostic; the link caught it)
+                const uint32_t off = aoff[i];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lvoid_t*)(sA + (i * 8 + wu) * 1024), 16, off, 0, 0, 0);
             }
 #pragma unroll
         for (int i = 0; i < NB; ++i)
             if ((i * NPART) / NB == q) {
-                const uint32_t off =
-                    kwhole ? boff[i]
-                           : ((boff[i] != BUF_OOB && k0 / T::KSW + bkb[i] < a.kst)
-                                  ? boff[i] + (uint32_t)(k0 / T::KSW) * 1024u : BUF_OOB);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lvoid_t*)(sB + (i * 8 + w) * 1024), 16, off, 0, 0, 0);
+                const uint32_t off = boff[i];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lvoid_t*)(sB + (i * 8 + wu) * 1024), 16, off, 0, 0, 0);
             }
         if constexpr (WF == W_INT4) {
             if (q == 0) {
                 // raw words, not converted here: a conversion would wait for them (and
                 // for the stage's copies issued before them)
-                const int grp = k0 / 128;
+                const uint32_t* szg = a.sz + (int64_t)(k0 / 128) * a.N;
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
-                    bool v;
-                    const int gb = grow_block(col_rb(2 * j + ((lane & 31) >> 4)), v);
                     nsz[j] = 0u;
-                    if (v) nsz[j] = a.sz[(int64_t)grp * a.N + gb * 16 + r];
+                    if (szcol[j] >= 0) nsz[j] = szg[szcol[j]];
                 }
             }
         }
@@ -528,11 +544,23 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     // that unit, ends up 2^-64 / s_next of the value -- some 1e-18 of it, far below the
     // accumulators' rounding -- with no per-fragment work.
     auto regroup = [&]() {
+        if constexpr (!EXQ) {
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const float z = h2f((uint16_t)(csz[j] >> 16));
+                const _Float16 b0 = (_Float16)(1024.0f + z), b1 = (_Float16)(64.0f + z);
+                qbias[j] = f16x2{b0, b0};
+                qbias64[j] = f16x2{b1, b1};
+                const _Float16 sc = __builtin_bit_cast(_Float16, (uint16_t)(csz[j] & 0xFFFFu));
+                qs2[j] = f16x2{sc, sc};
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             const float sc = h2f((uint16_t)(csz[j] & 0xFFFFu));
             const float s_new = sc == 0.f ? 0x1p-64f : sc;
-            const float ratio = s_unit[j] / s_new;
+            const float ratio = s_unit[j] * __builtin_amdgcn_rcpf(s_new);   // within 1 ulp
             s_unit[j] = s_new;
             const float z = h2f((uint16_t)(csz[j] >> 16));
             const _Float16 b0 = (_Float16)(1024.0f + z), b1 = (_Float16)(64.0f + z);
@@ -575,6 +603,10 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                     // exact q - z
                     const uint32_t wd = *(const uint32_t*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 4 * (2 * hh + h32));
                     bop[j] = i4x8_to_f16x8_q(wd, qbias[j], qbias64[j]);
+                    if constexpr (!EXQ) {
+                        const u32x4 d = bop[j];
+                        bop[j] = u32x4{mul_h2(d.x, qs2[j]), mul_h2(d.y, qs2[j]), mul_h2(d.z, qs2[j]), mul_h2(d.w, qs2[j])};
+                    }
                 }
             }
 #pragma unroll
@@ -769,7 +801,7 @@ int gemm_split_factor(int M, int N, int K, int dual_F, int wf, int* krange) {
     const int tk = big_tk(wf);
     const int stages = (K + tk - 1) / tk;
     *krange = stages * tk;
-    if (M < BT || tiles >= 256) return 1;
+    if (M < BT || tiles >= 256 || K % tk != 0) return 1;
     // one round of workgroups (one per compute unit), at least four stages per split
     int ks = 256 / tiles;
     if (ks > GEMM_SPLIT_MAX) ks = GEMM_SPLIT_MAX;
@@ -781,7 +813,7 @@ int gemm_split_factor(int M, int N, int K, int dual_F, int wf, int* krange) {
 }
 
 hipError_t launch_gemm_split(const GemmArgs& a, int wf, bool dual, int ks, hipStream_t st) {
-    if (ks < 1 || a.krange <= 0 || a.krange % big_tk(wf) != 0 || (int64_t)ks * a.krange < a.K ||
+    if (ks < 1 || a.krange <= 0 || a.krange % big_tk(wf) != 0 || a.K % big_tk(wf) != 0 || (int64_t)ks * a.krange < a.K ||
         (int64_t)(ks - 1) * a.krange >= a.K)
         return hipErrorInvalidValue;
     switch (wf) {
@@ -793,6 +825,7 @@ hipError_t launch_gemm_split(const GemmArgs& a, int wf, bool dual, int ks, hipSt
 }
 
 hipError_t launch_gemm_big(const GemmArgs& a, int wf, int epi, hipStream_t st) {
+    if (a.K % big_tk(wf) != 0) return hipErrorInvalidValue;     // whole stages only
     switch (wf) {
         case W_BF16: return launch_big<W_BF16>(a, epi, st);
         case W_INT8: return launch_big<W_INT8>(a, epi, st);
@@ -803,7 +836,7 @@ hipError_t launch_gemm_big(const GemmArgs& a, int wf, int epi, hipStream_t st) {
 
 hipError_t launch_gemm(const GemmArgs& a, int wf, int epi, hipStream_t st) {
     const int tiles = ((a.M + BT - 1) / BT) * ((epi == EPI_SWIGLU) ? (a.F + 127) / 128 : (a.N + BT - 1) / BT);
-    if (tiles >= GEMM_BIG_MIN_TILES) return launch_gemm_big(a, wf, epi, st);
+    if (tiles >= GEMM_BIG_MIN_TILES && a.K % big_tk(wf) == 0) return launch_gemm_big(a, wf, epi, st);
     return launch_gemm_small(a, wf, epi, st);
 }
 
