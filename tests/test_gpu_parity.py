@@ -3,6 +3,8 @@ tails, every weight / KV format, grouped-query attention, multi-chunk decode
 attention).  Bars: bit-exact weight codes and device-generated data; KV codes
 bit-exact for identical quantiser inputs; bf16 activations within 2e-2
 normwise (teacher-forced decode)."""
+import json
+
 import numpy as np
 import pytest
 
@@ -71,6 +73,12 @@ def _report(name, res):
     log(f"{name}: prefill {res.prefill_err:.3e} (l2 {res.prefill_err2:.3e}) per layer "
         f"{[f'{e:.2e}' for e in res.layer_errs]} decode max "
         f"{max(res.decode_errs) if res.decode_errs else 0:.3e}")
+    # one machine-readable record per case (tests/parity_table.py collects them)
+    log("PARITY " + json.dumps(dict(kind="reduced", workload=name,
+                                    prefill_layer_err=[round(e, 5) for e in res.layer_errs],
+                                    prefill_chained_err=round(res.prefill_err, 5),
+                                    decode_max_err=round(max(res.decode_errs), 5) if res.decode_errs else None,
+                                    decode_steps=len(res.decode_errs))))
 
 
 def test_tiny_config_end_to_end():
