@@ -17,9 +17,11 @@
 namespace fpk {
 
 // ---------------------------------------------------------------- RMSNorm
-// One workgroup per row, 16-byte accesses (H is a multiple of 16).
-// out = act(bf16(x * r * g)), r = 1 / sqrt(mean(x^2) + eps).  The second pass reads the
-// row again (it is in L2).
+// One workgroup per row, 16-byte accesses (H is a multiple of 8).
+// out = act(bf16(x * r * g)), r = 1 / sqrt(mean(x^2) + eps).  Rows of up to RMS_MAXV
+// 16-byte pieces per thread stay in registers between the two passes; longer rows read
+// their pieces again (from L2).
+constexpr int RMS_MAXV = 8;
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const uint16_t* __restrict__ x, int H,
                                                        const uint16_t* __restrict__ g, float eps,
                                                        uint16_t* __restrict__ out, int out_fmt) {
@@ -27,22 +29,30 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const uint16_t* __restrict
     const int64_t row = blockIdx.x;
     const u32x4* xr = (const u32x4*)(x + row * (int64_t)H);
     const int nv = H / 8;
+    u32x4 keep[RMS_MAXV];
+#pragma unroll
+    for (int i = 0; i < RMS_MAXV; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        keep[i] = c < nv ? xr[c] : u32x4{0u, 0u, 0u, 0u};
+    }
     float ss = 0.f;
-    for (int c = threadIdx.x; c < nv; c += 256) {
-        const u32x4 v = xr[c];
+    auto sq = [&](const u32x4& v) {
         const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const float e0 = __uint_as_float(w4[j] << 16), e1 = __uint_as_float(w4[j] & 0xFFFF0000u);
             ss += e0 * e0 + e1 * e1;
         }
-    }
+    };
+#pragma unroll
+    for (int i = 0; i < RMS_MAXV; ++i) sq(keep[i]);
+    for (int c = threadIdx.x + 256 * RMS_MAXV; c < nv; c += 256) sq(xr[c]);
     ss = block_sum(ss, red);
     const float r = 1.0f / __fsqrt_rn(ss / (float)H + eps);
     u32x4* orow = (u32x4*)(out + row * (int64_t)H);
     const u32x4* gv = (const u32x4*)g;
-    for (int c = threadIdx.x; c < nv; c += 256) {
-        const u32x4 v = xr[c], gg = gv[c];
+    auto put = [&](int c, const u32x4& v) {
+        const u32x4 gg = gv[c];
         const uint32_t w4[4] = {v.x, v.y, v.z, v.w}, g4[4] = {gg.x, gg.y, gg.z, gg.w};
         uint32_t o[4];
 #pragma unroll
@@ -52,7 +62,13 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const uint16_t* __restrict
             o[j] = (uint32_t)act_store(e0, out_fmt) | ((uint32_t)act_store(e1, out_fmt) << 16);
         }
         orow[c] = u32x4{o[0], o[1], o[2], o[3]};
+    };
+#pragma unroll
+    for (int i = 0; i < RMS_MAXV; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nv) put(c, keep[i]);
     }
+    for (int c = threadIdx.x + 256 * RMS_MAXV; c < nv; c += 256) put(c, xr[c]);
 }
 
 // ---------------------------------------------------------------- residual epilogue

@@ -161,14 +161,19 @@ def test_graph_replay_matches_eager():
     assert torch.equal(outs[False].view(torch.int16), outs[True].view(torch.int16))
 
 
-def test_decode_steps_match_single_steps():
+@pytest.mark.parametrize("B,wq,kvq", [(3, "int4", "int8"), (1, "bf16", "bf16"), (1, "int8", "int8")],
+                         ids=["batch3-int4-int8kv", "single-bf16", "single-int8-int8kv"])
+def test_decode_steps_match_single_steps(B, wq, kvq):
     """n steps in one call (one graph) give bit for bit what n calls of fp_decode_step
-    give, with the decode graph on and off, for odd and even n; the last output is in
-    y for odd n and in x for even n."""
+    give, with the decode graph on and off, for odd and even n, the batch schedule and the
+    single-sequence one; the last call ends exactly at the cache's capacity.  The last
+    output is in y for odd n and in x for even n."""
     import torch
     from paper_2501_13111_amd import Fingerprint, fill_normal
     shape = Shape(2, 256, 4, 2, 64, 384, 3, 30, 44)
-    B, P = 3, 30
+    P = 30
+    steps = (1, 4, 3, 1, 5)                   # odd and even n, up to max_seq = 44
+    assert P + sum(steps) == shape.max_seq
 
     def start(fp):
         x = torch.empty(B * P * 256, dtype=torch.bfloat16, device="cuda")
@@ -178,27 +183,27 @@ def test_decode_steps_match_single_steps():
         return y.view(B, P, 256)[:, -1, :].contiguous()
 
     ref = []
-    with Fingerprint(shape, "int4", "int8", seed=5) as fp:
+    with Fingerprint(shape, wq, kvq, seed=5) as fp:
         a = start(fp)
         b = torch.empty_like(a)
-        for _ in range(9):
+        for _ in range(sum(steps)):
             fp.decode_step(a, b)
             a, b = b, a
             ref.append(a.clone())
     for graph in (True, False):
-        with Fingerprint(shape, "int4", "int8", seed=5) as fp:
+        with Fingerprint(shape, wq, kvq, seed=5) as fp:
             fp.set_decode_graph(graph)
             x = start(fp)
             y = torch.empty_like(x)
             done = 0
-            for n in (1, 4, 3, 1):            # odd and even n, 9 steps in all
+            for n in steps:
                 out = fp.decode_steps(x, y, n)
                 done += n
                 torch.cuda.synchronize()
                 assert torch.equal(out.view(torch.int16), ref[done - 1].view(torch.int16)), (graph, n)
                 if out is y:                  # continue from the last output
                     x, y = y, x
-            assert fp.position() == (P + 9, B)
+            assert fp.position() == (shape.max_seq, B)
 
 
 def test_kv_codes_bit_exact_for_same_quantiser_input():
