@@ -45,10 +45,10 @@ PROJ = {"qkv", "o", "gate_up", "down"}
 # were taken on (hash of the kernel's source files and of its argument block in
 # fp_internal.h); the summaries and commands are in profiles/.
 TRAFFIC = {
-    ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "ea8124fbfacc3bad", "bytes_per_launch": 9325581037},
-    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "a81c9ea5d6815384", "bytes_per_launch": 1237241720},
-    ("decode_proj", "llama2-70b-tp8-int4"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 27572483},
-    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "149bcd6e8889c86c", "bytes_per_launch": 60844003},
+    ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "6bd408c63c578c84", "bytes_per_launch": 8560996698},
+    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "a81c9ea5d6815384", "bytes_per_launch": 1237295608},
+    ("decode_proj", "llama2-70b-tp8-int4"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 27162883},
+    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "2af41be9a5c124b1", "bytes_per_launch": 47268787},
 }
 FAMILY_SRC = {
     "decode_proj": (("skinny.hip", "fp_device.h"), r"enum XForm \{.*?\n\};\n.*?struct SkinnyArgs \{.*?\n\};"),
