@@ -613,6 +613,9 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<AF>(af[i], bop[j], acc[i][j]);
+            // quantised weights: the compiler's interleaving strategy 1 for the step's LDS reads,
+            // unpacking and MFMAs (measured 1.5-4% faster; bf16 weights are faster without it)
+            if constexpr (WF != W_BF16) __builtin_amdgcn_iglp_opt(1);
         }
     };
 
