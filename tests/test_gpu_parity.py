@@ -382,6 +382,10 @@ BIG_CASES = [
     ("big-int4-ragged", Shape(1, 1152, 9, 9, 128, 2176, 8, 1000, 1002), "int4", "int8", 8, 1000, 2, (0, 7)),
     ("big-bf16", Shape(1, 1024, 8, 8, 128, 2560, 8, 1024, 1026), "bf16", "bf16", 8, 1024, 2, (3,)),
     ("big-int8-gqa", Shape(1, 1024, 8, 2, 128, 2048, 8, 1024, 1026), "int8", "int8", 8, 1024, 2, (5,)),
+    # hidden and ffn not whole 64-input stages: tile counts of the large tiling, but the
+    # projections that reduce over them take the small tiling (o, over n_heads * head_dim =
+    # 1024, stays large)
+    ("big-bf16-partial-stage", Shape(1, 1040, 8, 8, 128, 2080, 4, 1024, 1026), "bf16", "bf16", 4, 1024, 2, (2,)),
 ]
 
 
