@@ -177,33 +177,53 @@ hipError_t launch_sp24_gemv(const Sp24Args& a, int ks, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------- prefill projection
-// C^T tiles of 128 weight rows x 128 tokens, 4 waves of 64 x 64 (2 x 2 sparse 32x32x32
-// MFMA tiles), 64 inputs per stage.  Activation rows (128 B per stage) and weight value
-// blocks are copied into LDS by buffer loads that write LDS directly (two stages; rows
-// past M and blocks past the matrix land as zeros), activation chunks stored with an XOR
-// swizzle so that fragment reads are free of bank conflicts.  The lanes' index words of
-// the next stage are loaded into registers one stage ahead.  A lane's accumulators hold
-// one token and runs of 4 consecutive weight rows, so the epilogues write 16- and 8-byte
-// pieces of the [M, N] outputs directly; the SwiGLU tiling gives each wave a gate block
-// and the matching up block.
-constexpr int SG_TM = 128, SG_TN = 128, SG_TK = 64;
-constexpr int SG_X_BYTES = SG_TM * SG_TK * 2;                 // 16 KiB
-constexpr int SG_W_BYTES = (SG_TN / 32) * (SG_TK / 32) * 1024;  // 8 KiB
-constexpr int SG_STAGE = SG_X_BYTES + SG_W_BYTES;
+// C^T tiles of TN weight rows x TM tokens: waves of NBW 32-row weight blocks x MW 32-token
+// tiles (NBW x MW sparse 32x32x32 MFMA tiles), 64 inputs per stage.  Large products take
+// 256 x 256 tiles of 8 waves with 4 x 2 tiles each (per 32 inputs a wave reads 4 weight
+// fragments and 4 activation pieces for 8 MFMAs); smaller ones take 128 x 128 tiles of 4
+// waves with 2 x 2, so that more workgroups fill the GPU.  Activation rows (128 B per
+// stage), weight value blocks and the blocks' index words are copied into LDS by buffer
+// loads that write LDS directly (rows past M and blocks past the matrix land as zeros),
+// activation chunks stored with an XOR swizzle so that fragment reads are free of bank
+// conflicts.  Three LDS stages: a stage's copies are issued two stages ahead (a stage holds
+// only 16 MFMAs per wave, too few to cover a copy's latency on its own), and each wave waits
+// for all but the newest stage's copies, an exact count since they are its only
+// vector-memory instructions in the loop.  A lane's accumulators hold one token and runs of
+// 4 consecutive weight rows, so the epilogues write 16- and 8-byte pieces of the [M, N]
+// outputs directly; the SwiGLU tiling gives each wave gate blocks and the matching up blocks.
+constexpr int SG_TK = 64;
+
+template <int TM, int TN, int MW, int NBW>
+struct SgT {
+    static constexpr int WGM = TM / (32 * MW), WGN = TN / (32 * NBW);   // waves along m and n
+    static constexpr int NW = WGM * WGN, NT = 64 * NW;
+    static constexpr int X_BYTES = TM * SG_TK * 2;
+    static constexpr int W_BYTES = (TN / 32) * (SG_TK / 32) * 1024;
+    static constexpr int I_BYTES = (TN / 32) * 256;                    // index words: 2 k-blocks x 64 lanes per row-block
+    static constexpr int STAGE = X_BYTES + W_BYTES + I_BYTES;
+    static constexpr int NX = X_BYTES / 1024 / NW;                     // activation copies per thread
+    static constexpr int NWB = W_BYTES / 1024 / NW;                    // weight-block copies per thread
+    static constexpr int LPS = NX + NWB + 1;                           // copies per thread per stage (one of index words)
+    static_assert(NX * NW * 1024 == X_BYTES && NWB * NW * 1024 == W_BYTES && TN / 32 == NW, "copy split");
+};
 
 __device__ __forceinline__ int sg_swz(int row) { return (row >> 1) & 7; }
 
-template <int EPI>
-__global__ void __launch_bounds__(256) gemm_sp24_kernel(Sp24Args a) {
+template <int EPI, int TM, int TN, int MW, int NBW>
+__global__ void __launch_bounds__(64 * (TM / (32 * MW)) * (TN / (32 * NBW))) gemm_sp24_kernel(Sp24Args a) {
+    using T = SgT<TM, TN, MW, NBW>;
     constexpr bool DUAL = EPI == EPI_SWIGLU;
-    __shared__ __attribute__((aligned(1024))) char smem[2 * SG_STAGE];
+    constexpr int RB = TN / 32;                     // weight row-blocks of a tile
+    static_assert(!DUAL || NBW % 2 == 0, "SwiGLU: gate and up blocks in pairs");
+    constexpr int NS = 3;                           // LDS stages: copies run two stages ahead
+    __shared__ __attribute__((aligned(1024))) char smem[NS * T::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int s = lane >> 5, c32 = lane & 31;
-    const int wn = w >> 1, wm = w & 1;
+    const int wn = w / T::WGM, wm = w % T::WGM;
     int mt, nt;
     {
-        const int T = a.tiles_m * a.tiles_n, bid = blockIdx.x;
-        const int x = bid & 7, j = bid >> 3, q = T >> 3, rm = T & 7;
+        const int Tn = a.tiles_m * a.tiles_n, bid = blockIdx.x;
+        const int x = bid & 7, j = bid >> 3, q = Tn >> 3, rm = Tn & 7;
         const int t = x * q + (x < rm ? x : rm) + j;
         const int GM = 8;
         const int grp = t / (GM * a.tiles_n);
@@ -213,132 +233,168 @@ __global__ void __launch_bounds__(256) gemm_sp24_kernel(Sp24Args a) {
         mt = gm0 + tt % gsz;
         nt = tt / gsz;
     }
-    const int m0 = mt * SG_TM;
+    const int m0 = mt * TM;
     const int nrb = a.N / 32;                       // row-blocks of the matrix
-    // global row-block of the tile's row-block rb (0..3): plain, or [gate 2 | up 2] for SwiGLU
+    // global row-block of the tile's row-block rb: plain, or [gate RB/2 | up RB/2] for SwiGLU
     auto grb = [&](int rb, bool& v) -> int {
         if constexpr (DUAL) {
-            const int fb = nt * 2 + (rb & 1);
+            const int fb = nt * (RB / 2) + (rb % (RB / 2));
             v = fb < a.F / 32;
-            return (rb < 2 ? 0 : a.F / 32) + fb;
+            return (rb < RB / 2 ? 0 : a.F / 32) + fb;
         } else {
-            const int b = nt * 4 + rb;
+            const int b = nt * RB + rb;
             v = b < nrb;
             return b;
         }
     };
-    // the tile row-block of this wave's n-block bn: a gate block and its up block (SwiGLU)
-    auto wrb = [&](int bn) -> int { return DUAL ? (bn == 0 ? wn : 2 + wn) : 2 * wn + bn; };
+    // the tile row-block of this wave's n-block bn (SwiGLU: gate blocks, then their up blocks)
+    auto wrb = [&](int bn) -> int {
+        if constexpr (DUAL) return bn < NBW / 2 ? wn * (NBW / 2) + bn : RB / 2 + wn * (NBW / 2) + (bn - NBW / 2);
+        else return wn * NBW + bn;
+    };
 
     const __amdgpu_buffer_rsrc_t xres = buf_rsrc(a.X, (uint32_t)min((int64_t)a.M * a.K * 2, (int64_t)0xFFFFFFF0));
     const __amdgpu_buffer_rsrc_t wres = buf_rsrc(a.Wv, (uint32_t)min((int64_t)nrb * a.kst * 1024, (int64_t)0xFFFFFFF0));
-    // per-thread copy slots: 4 activation pieces (16 wave copies of 1 KiB) and 2 weight blocks
-    uint32_t xoff[4];
+    const __amdgpu_buffer_rsrc_t ires = buf_rsrc(a.Wi, (uint32_t)min((int64_t)nrb * a.kst * 128, (int64_t)0xFFFFFFF0));
+    // per-thread copy slots: NX activation pieces and NWB weight blocks (1 KiB wave copies)
+    uint32_t xoff[T::NX];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int p = (i * 4 + w) * 64 + lane;
+    for (int i = 0; i < T::NX; ++i) {
+        const int p = (i * T::NW + w) * 64 + lane;
         const int row = p >> 3, slot = p & 7;
         const int kc = (slot ^ sg_swz(row)) * 8;
         xoff[i] = m0 + row < a.M ? (uint32_t)(((int64_t)(m0 + row) * a.K + kc) * 2) : BUF_OOB;
     }
-    uint32_t woff[2];
+    uint32_t woff[T::NWB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int b = i * 4 + w, rb = b >> 1, kb = b & 1;
+    for (int i = 0; i < T::NWB; ++i) {
+        const int b = i * T::NW + w, rb = b >> 1, kb = b & 1;
         bool v;
         const int g = grb(rb, v);
         woff[i] = v ? (uint32_t)((((int64_t)g * a.kst + kb) * 64 + lane) * 16) : BUF_OOB;
     }
-    uint32_t nidx[2][2], cidx[2][2];   // index words of (n-block, k-step): next / current stage
-    auto issue = [&](int stage, int k0) {
-        char* sX = smem + stage * SG_STAGE;
-        char* sW = sX + SG_X_BYTES;
+    // the index words of tile row-block w (one per wave): the two k-blocks of a stage are 256
+    // contiguous bytes, one dword per lane
+    uint32_t ioff;
+    {
+        bool v;
+        const int g = grb(w, v);
+        ioff = v ? (uint32_t)((int64_t)g * a.kst * 128 + lane * 4) : BUF_OOB;
+    }
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    auto issue = [&](int sl, int k0) {
+        char* sX = smem + sl * T::STAGE;
+        char* sW = sX + T::X_BYTES;
+        char* sI = sW + T::W_BYTES;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < T::NX; ++i) {
             const uint32_t off = xoff[i] != BUF_OOB ? xoff[i] + 2u * k0 : BUF_OOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lvoid_t*)(sX + (i * 4 + w) * 1024), 16, off, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lvoid_t*)(sX + (i * T::NW + wu) * 1024), 16, off, 0, 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < T::NWB; ++i) {
             const uint32_t off = woff[i] != BUF_OOB ? woff[i] + (uint32_t)(k0 / 32) * 1024u : BUF_OOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lvoid_t*)(sW + (i * 4 + w) * 1024), 16, off, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lvoid_t*)(sW + (i * T::NW + wu) * 1024), 16, off, 0, 0, 0);
         }
-#pragma unroll
-        for (int bn = 0; bn < 2; ++bn) {
-            bool v;
-            const int g = grb(wrb(bn), v);
-#pragma unroll
-            for (int kk = 0; kk < 2; ++kk)
-                nidx[bn][kk] = v ? (uint32_t)a.Wi[((int64_t)g * a.kst + k0 / 32 + kk) * 64 + lane] : 0u;
-        }
+        const uint32_t off = ioff != BUF_OOB ? ioff + (uint32_t)(k0 / 32) * 128u : BUF_OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ires, (lvoid_t*)(sI + wu * 256), 4, off, 0, 0, 0);
     };
 
-    f32x16 acc[2][2];
+    f32x16 acc[NBW][MW];
 #pragma unroll
-    for (int bn = 0; bn < 2; ++bn)
+    for (int bn = 0; bn < NBW; ++bn)
 #pragma unroll
-        for (int bm = 0; bm < 2; ++bm) acc[bn][bm] = f32x16{};
+        for (int bm = 0; bm < MW; ++bm) acc[bn][bm] = f32x16{};
 
-    const int nk = a.K / SG_TK;
-    issue(0, 0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-#pragma unroll
-        for (int bn = 0; bn < 2; ++bn)
-#pragma unroll
-            for (int kk = 0; kk < 2; ++kk) cidx[bn][kk] = nidx[bn][kk];
-        const int stage = kt & 1;
-        if (kt + 1 < nk) issue(stage ^ 1, (kt + 1) * SG_TK);
-        const char* sX = smem + stage * SG_STAGE;
-        const char* sW = sX + SG_X_BYTES;
+    // stage sl: multiply it out of LDS (the index words come from its LDS region too)
+    auto compute = [&](int sl) {
+        const char* sX = smem + sl * T::STAGE;
+        const char* sW = sX + T::X_BYTES;
+        const char* sI = sW + T::W_BYTES;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            u32x4 af[2], b0[2], b1[2];
+            u32x4 af[NBW], b0[MW], b1[MW];
+            uint32_t ix[NBW];
 #pragma unroll
-            for (int bn = 0; bn < 2; ++bn) af[bn] = *(const u32x4*)(sW + (wrb(bn) * 2 + kk) * 1024 + lane * 16);
+            for (int bn = 0; bn < NBW; ++bn) {
+                af[bn] = *(const u32x4*)(sW + (wrb(bn) * 2 + kk) * 1024 + lane * 16);
+                ix[bn] = *(const uint16_t*)(sI + wrb(bn) * 256 + kk * 128 + lane * 2);
+            }
 #pragma unroll
-            for (int bm = 0; bm < 2; ++bm) {
-                const int row = wm * 64 + bm * 32 + c32;
+            for (int bm = 0; bm < MW; ++bm) {
+                const int row = wm * 32 * MW + bm * 32 + c32;
                 const int ch = 4 * kk + 2 * s;
                 b0[bm] = *(const u32x4*)(sX + row * 128 + ((ch ^ sg_swz(row)) * 16));
                 b1[bm] = *(const u32x4*)(sX + row * 128 + (((ch + 1) ^ sg_swz(row)) * 16));
             }
 #pragma unroll
-            for (int bn = 0; bn < 2; ++bn)
+            for (int bn = 0; bn < NBW; ++bn)
 #pragma unroll
-                for (int bm = 0; bm < 2; ++bm) acc[bn][bm] = smfmac(af[bn], b0[bm], b1[bm], cidx[bn][kk], acc[bn][bm]);
+                for (int bm = 0; bm < MW; ++bm) acc[bn][bm] = smfmac(af[bn], b0[bm], b1[bm], ix[bn], acc[bn][bm]);
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-    }
+    };
+    // the copies of a stage are the wave's only vector-memory instructions in the loop, LPS of
+    // them, so "all but the last stage's" is an exact wait count
+    auto wait_all_but_one_stage = [&]() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(T::LPS) : "memory"); };
+    auto wait_all = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+    auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
-    // epilogue: lane holds token m = m0 + 64 wm + 32 bm + c32 and, per q, rows
+    const int nk = a.K / SG_TK;
+    issue(0, 0);
+    if (nk > 1) {
+        issue(1, SG_TK);
+        wait_all_but_one_stage();
+    } else {
+        wait_all();
+    }
+    barrier();
+    // trip kt: copies of stage kt + 2 into the slot stage kt - 1 used, multiply stage kt, then
+    // wait for stage kt + 1 (the slots are kt % 3: three trips per loop turn)
+    auto trip = [&](int kt, int sl) {
+        if (kt + 2 < nk) issue((sl + 2) % NS, (kt + 2) * SG_TK);
+        compute(sl);
+        if (kt + 2 < nk) wait_all_but_one_stage();
+        else wait_all();
+        barrier();
+    };
+    int kt = 0;
+    for (; kt + NS <= nk; kt += NS) {
+        trip(kt, 0);
+        trip(kt + 1, 1);
+        trip(kt + 2, 2);
+    }
+    if (kt < nk) trip(kt, 0);
+    if (kt + 1 < nk) trip(kt + 1, 1);
+
+    // epilogue: lane holds token m = m0 + 32 MW wm + 32 bm + c32 and, per q, rows
     // r0 + 8 q + 4 s .. + 3 of its n-block (accumulator elements 4 q .. 4 q + 3)
 #pragma unroll
-    for (int bm = 0; bm < 2; ++bm) {
-        const int m = m0 + wm * 64 + bm * 32 + c32;
+    for (int bm = 0; bm < MW; ++bm) {
+        const int m = m0 + wm * 32 * MW + bm * 32 + c32;
         if (m >= a.M) continue;
         if constexpr (DUAL) {
-            bool v;
-            const int g = grb(wrb(0), v);            // gate row-block; up is g + F / 32
-            if (!v) continue;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int f = g * 32 + 8 * q + 4 * s;
-                uint32_t o[2];
+            for (int jg = 0; jg < NBW / 2; ++jg) {
+                bool v;
+                const int g = grb(wrb(jg), v);          // gate row-block; up is g + F / 32
+                if (!v) continue;
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const float g0 = acc[0][bm][4 * q + 2 * h], u0 = acc[1][bm][4 * q + 2 * h];
-                    const float g1 = acc[0][bm][4 * q + 2 * h + 1], u1 = acc[1][bm][4 * q + 2 * h + 1];
-                    o[h] = (uint32_t)act_store(bfround(silu_f(g0) * u0), a.out_fmt) |
-                           ((uint32_t)act_store(bfround(silu_f(g1) * u1), a.out_fmt) << 16);
+                for (int q = 0; q < 4; ++q) {
+                    const int f = g * 32 + 8 * q + 4 * s;
+                    uint32_t o[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const float g0 = acc[jg][bm][4 * q + 2 * h], u0 = acc[jg + NBW / 2][bm][4 * q + 2 * h];
+                        const float g1 = acc[jg][bm][4 * q + 2 * h + 1], u1 = acc[jg + NBW / 2][bm][4 * q + 2 * h + 1];
+                        o[h] = (uint32_t)act_store(bfround(silu_f(g0) * u0), a.out_fmt) |
+                               ((uint32_t)act_store(bfround(silu_f(g1) * u1), a.out_fmt) << 16);
+                    }
+                    *(u32x2*)(a.out16 + (int64_t)m * a.F + f) = u32x2{o[0], o[1]};
                 }
-                *(u32x2*)(a.out16 + (int64_t)m * a.F + f) = u32x2{o[0], o[1]};
             }
         } else {
 #pragma unroll
-            for (int bn = 0; bn < 2; ++bn) {
+            for (int bn = 0; bn < NBW; ++bn) {
                 bool v;
                 const int g = grb(wrb(bn), v);
                 if (!v) continue;
@@ -363,19 +419,35 @@ __global__ void __launch_bounds__(256) gemm_sp24_kernel(Sp24Args a) {
     }
 }
 
+template <int EPI, int TM, int TN, int MW, int NBW>
+static void launch_sg_shape(const Sp24Args& a, hipStream_t st) {
+    Sp24Args b = a;
+    b.tiles_m = (a.M + TM - 1) / TM;
+    b.tiles_n = EPI == EPI_SWIGLU ? (a.F + TN / 2 - 1) / (TN / 2) : (a.N + TN - 1) / TN;
+    FP_LAUNCH((gemm_sp24_kernel<EPI, TM, TN, MW, NBW>), dim3(b.tiles_m * b.tiles_n), dim3(SgT<TM, TN, MW, NBW>::NT), 0,
+              st, b);
+}
+
+// the large tiling from this many 256 x 256 tiles (fewer: 128 x 128 tiles, four times as many)
+#ifndef SG_BIG_MIN_TILES
+#define SG_BIG_MIN_TILES 128
+#endif
+template <int EPI>
+static void launch_sg(const Sp24Args& a, hipStream_t st) {
+    const int big = ((a.M + 255) / 256) * (EPI == EPI_SWIGLU ? (a.F + 127) / 128 : (a.N + 255) / 256);
+    if (big >= SG_BIG_MIN_TILES) launch_sg_shape<EPI, 256, 256, 2, 4>(a, st);
+    else launch_sg_shape<EPI, 128, 128, 2, 2>(a, st);
+}
+
 hipError_t launch_gemm_sp24(const Sp24Args& a, int epi, hipStream_t st) {
     if (a.K % SG_TK != 0 || a.N % 32 != 0 || a.kst != a.K / 32 || a.M < 1) return hipErrorInvalidValue;
     if ((int64_t)a.M * a.K * 2 >= ((int64_t)1 << 32) - 16) return hipErrorInvalidValue;   // 32-bit buffer offsets
     if (epi == EPI_SWIGLU && (a.F % 32 != 0 || a.N != 2 * a.F)) return hipErrorInvalidValue;
     if ((int64_t)(a.N / 32) * a.kst * 1024 >= ((int64_t)1 << 32) - 16) return hipErrorInvalidValue;
-    Sp24Args b = a;
-    b.tiles_m = (a.M + SG_TM - 1) / SG_TM;
-    b.tiles_n = epi == EPI_SWIGLU ? (a.F + 63) / 64 : (a.N + SG_TN - 1) / SG_TN;
-    const dim3 grid(b.tiles_m * b.tiles_n);
     switch (epi) {
-        case EPI_F32: FP_LAUNCH(gemm_sp24_kernel<EPI_F32>, grid, dim3(256), 0, st, b); break;
-        case EPI_RESID: FP_LAUNCH(gemm_sp24_kernel<EPI_RESID>, grid, dim3(256), 0, st, b); break;
-        case EPI_SWIGLU: FP_LAUNCH(gemm_sp24_kernel<EPI_SWIGLU>, grid, dim3(256), 0, st, b); break;
+        case EPI_F32: launch_sg<EPI_F32>(a, st); break;
+        case EPI_RESID: launch_sg<EPI_RESID>(a, st); break;
+        case EPI_SWIGLU: launch_sg<EPI_SWIGLU>(a, st); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

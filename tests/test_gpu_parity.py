@@ -386,6 +386,8 @@ BIG_CASES = [
     # projections that reduce over them take the small tiling (o, over n_heads * head_dim =
     # 1024, stays large)
     ("big-bf16-partial-stage", Shape(1, 1040, 8, 8, 128, 2080, 4, 1024, 1026), "bf16", "bf16", 4, 1024, 2, (2,)),
+    # 2:4 weights on the large sparse tiling, with a ragged last column tile
+    ("big-sp24-ragged", Shape(1, 1024, 8, 4, 128, 2112, 8, 1000, 1002), "sp24", "int8", 8, 1000, 2, (0, 7)),
 ]
 
 
