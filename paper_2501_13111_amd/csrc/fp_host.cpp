@@ -773,15 +773,21 @@ fp_status enqueue_decode_single(fp_layer* h, const uint16_t* x, uint16_t* y, hip
 }
 
 // A batch: the RMSNorm of each projection input and the SwiGLU are formed once
-// (every workgroup re-forming them from B rows would cost more than the weights).
-fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
+// (every workgroup re-forming them from B rows would cost more than the weights).  The last
+// layer's residual kernel also normalises the step's output with layer 0's gain, so a step
+// whose input is the previous step's output (chained: n steps in one call) starts from that
+// (the same kernel computes it from the same bf16 row, so the result is bit for bit the one
+// the step's own first RMSNorm would give).
+fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st, bool chained) {
     const fp_shape& s = h->s;
     const int B = h->B;
     fp_status rc;
     int ks;
-    h->prof.mark(FP_K_RMSNORM, 0);
-    HIPCHK(launch_resid_norm(nullptr, 0, B, s.hidden, x, nullptr, h->L[0].attn_norm, s.rms_eps, h->act_in,
-                             h->act_fmt, h->ssq, nullptr, st));
+    if (!chained) {
+        h->prof.mark(FP_K_RMSNORM, 0);
+        HIPCHK(launch_resid_norm(nullptr, 0, B, s.hidden, x, nullptr, h->L[0].attn_norm, s.rms_eps, h->act_in,
+                                 h->act_fmt, h->ssq, nullptr, st));
+    }
     for (int l = 0; l < s.n_layers; ++l) {
         const LayerW& W = h->L[l];
         const uint16_t* in = (l == 0) ? x : h->xbuf;
@@ -804,7 +810,7 @@ fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipS
         if ((rc = run_skinny_batch(h, h->act_f, W.down, B, 0, h->part, &ks, st))) return rc;
         const bool last = (l == s.n_layers - 1);
         h->prof.mark(FP_K_RESID_NORM, l);
-        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, last ? nullptr : h->L[l + 1].attn_norm,
+        HIPCHK(launch_resid_norm(h->part, ks, B, s.hidden, h->hbuf, out, h->L[last ? 0 : l + 1].attn_norm,
                                  s.rms_eps, h->act_in, h->act_fmt, h->ssq, last ? h->d_pos : nullptr, st));
         if (h->ldump) HIPCHK(hipMemcpyAsync(h->ldump + (size_t)l * B * s.hidden, out, (size_t)B * s.hidden * 2,
                                             hipMemcpyDeviceToDevice, st));
@@ -815,9 +821,9 @@ fp_status enqueue_decode_batch(fp_layer* h, const uint16_t* x, uint16_t* y, hipS
 
 // 2:4 sparse weights run every batch size, one sequence included, on the batch schedule
 // (their projection kernel stages plain activations).
-fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st) {
+fp_status enqueue_decode(fp_layer* h, const uint16_t* x, uint16_t* y, hipStream_t st, bool chained = false) {
     return h->B == 1 && h->wq != FP_WQ_BF16_2OF4 ? enqueue_decode_single(h, x, y, st)
-                                                 : enqueue_decode_batch(h, x, y, st);
+                                                 : enqueue_decode_batch(h, x, y, st, chained);
 }
 
 // Final RMSNorm, LM head and greedy argmax of position T - 1 of each of B sequences of
@@ -1252,7 +1258,7 @@ fp_status fp_decode_steps(fp_layer* h, void* x, void* y, int32_t n, void* stream
             for (int i = 0; i < n; ++i) {
                 const uint16_t* src = (const uint16_t*)((i & 1) ? y : x);
                 uint16_t* dst = (uint16_t*)((i & 1) ? x : y);
-                fp_status rc = enqueue_decode(h, src, dst, s);
+                fp_status rc = enqueue_decode(h, src, dst, s, i > 0);   // step i > 0 reads step i - 1's output
                 if (rc) return rc;
             }
             return FP_OK;
