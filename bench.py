@@ -45,10 +45,11 @@ PROJ = {"qkv", "o", "gate_up", "down"}
 # were taken on (hash of the kernel's source files and of its argument block in
 # fp_internal.h); the summaries and commands are in profiles/.
 TRAFFIC = {
-    ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "6bd408c63c578c84", "bytes_per_launch": 8560996698},
-    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "a81c9ea5d6815384", "bytes_per_launch": 1237295608},
-    ("decode_proj", "llama2-70b-tp8-int4"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 27162883},
-    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "2af41be9a5c124b1", "bytes_per_launch": 47268787},
+    ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "f4b5df64886dc990", "bytes_per_launch": 8561753373},
+    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "a81c9ea5d6815384", "bytes_per_launch": 1237281570},
+    ("decode_proj", "llama2-70b-tp8-int4"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 27162882},
+    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "2af41be9a5c124b1", "bytes_per_launch": 47269468},
+    ("decode_proj", "llama2-7b-bf16"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 102930895},
 }
 FAMILY_SRC = {
     "decode_proj": (("skinny.hip", "fp_device.h"), r"enum XForm \{.*?\n\};\n.*?struct SkinnyArgs \{.*?\n\};"),
