@@ -16,10 +16,9 @@
 //
 // Keys go in 32-key blocks; the LDS holds each block in fragment-major order (one 1 KiB
 // chunk per MFMA operand, lane l's 16 bytes at 16 l), so every fragment read is one
-// conflict-free ds_read_b128.  Blocks are brought in through registers two blocks ahead
-// (loaded at the top of a trip, written to LDS at its end) and the waves meet once per
-// block.  Two waves per SIMD; within a wave, the MFMAs of S for block s + 1 are issued
-// beside the softmax of block s.
+// conflict-free ds_read_b128.  The waves meet once per block.  Four waves per workgroup
+// and two workgroups per CU (two waves per SIMD, from workgroups that run out of step);
+// within a wave, the MFMAs of S for block s + 1 are issued beside the softmax of block s.
 //
 // Softmax in the base-2 domain against a fixed reference: each query's maximum over its
 // first key block (taken exactly, across the two lane halves) is the reference m for all
@@ -31,12 +30,19 @@
 // sit on a single path, so they accumulate in place.  Each lane half keeps its own partial
 // sum, added once at the end.
 //
-// int8 caches: K codes are scaled into fp16 on the way to LDS (code * s_k / kappa, kappa =
-// the largest key scale of the prompt; fp16 MFMA with the queries in fp16, kappa folded
-// into the score scale) and V codes into bf16 (code * s_v / sigma, sigma likewise; sigma
-// multiplies the output).  Workgroups of NW waves hold HPW heads that share one kv head
-// (GQA: the blocks are staged once for all of them) times NW / HPW consecutive 32-query
-// blocks; the heaviest (latest) query tiles are launched first.
+// Blocks reach the LDS by buffer-to-LDS copies, so no thread holds them in registers:
+// each 1 KiB fragment chunk is one copy, issued three blocks ahead into a ring of four
+// slots.  int8 caches are first dequantised once per block of the prompt by
+// attn_stage_kernel into the same fragment-major layout: K codes into fp16
+// (code * s_k / kappa_b, kappa_b the largest key scale of the block's keys inside the
+// prompt, so at most 127 in size; fp16 MFMA with the queries in fp16, kappa_b folded into
+// the block's score scale and copied with the block) and V codes into bf16 (code * s_v).
+// Every workgroup that reads a block then copies it as it would a bf16 cache block, instead
+// of dequantising it again.  The copies are issued in asm with explicit wait counts: the
+// compiler cannot tell a copy's target slot from the slots being read, and would wait for
+// every copy in flight before each LDS read.  Workgroups of NW waves hold HPW heads that
+// share one kv head (GQA: the blocks are staged once for all of them) times NW / HPW
+// consecutive 32-query blocks; the heaviest (latest) query tiles are launched first.
 #include <type_traits>
 
 #include "fp_device.h"
@@ -50,33 +56,79 @@ __device__ __forceinline__ uint32_t mul_f16x2(uint32_t x, uint32_t y) {
     return __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, x) * __builtin_bit_cast(f16x2, y));
 }
 
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// The four words of a raw buffer resource over [base, base + bytes): no stride, 32-bit data
+// format (the resource __builtin_amdgcn_make_buffer_rsrc builds), for copies written in asm.
+__device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
+    const uint64_t p = (uint64_t)base;
+    return i32x4{(int32_t)(uint32_t)p, (int32_t)((uint32_t)(p >> 32) & 0xFFFFu), (int32_t)bytes, 0x00020000};
+}
+
+// Buffer-to-LDS copy: lane l's W bytes (16 or 4) at voff + soff of the resource land at LDS
+// address lds + W l (past the resource's end: zeros).  M0 carries the LDS address and is
+// restored afterwards; one wait state separates its write from the copy.
+template <int W>
+__device__ __forceinline__ void lds_copy(const i32x4& r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    uint32_t keep;
+    if constexpr (W == 16)
+        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                     "buffer_load_dwordx4 %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
+                     : "=&s"(keep) : "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory");
+    else
+        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                     "buffer_load_dword %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
+                     : "=&s"(keep) : "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory");
+}
+
 template <int D, bool KV8, int NW, int HPW>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) attn_prefill_kernel(AttnPreArgs a) {
     static_assert(NW % HPW == 0 && PK == VT_BLK, "workgroup shape");
     constexpr int NT = 64 * NW;
     constexpr int QW = NW / HPW;                // waves (32-query blocks) per head
-    // LDS blocks: the one being multiplied, the next one, and the one being written (the
-    // buffer of block s is s & (NBUF - 1))
-    constexpr int NBUF = 4;
     constexpr int AQ = KV8 ? ACT_F16 : ACT_BF16;  // S = K Q^T operands; P.V runs on bf16
     constexpr int NKC = D / 16;                 // K chunks per block (MFMA k-steps)
     constexpr int NVC = 2 * (D / 32);           // V chunks per block (2 key steps x dim tiles)
     constexpr int CH = NKC + NVC;
-    constexpr int SB = CH * 1024;               // LDS bytes per block
-    // pieces per thread per block: int8, 4D 8-code pieces of K and as many of V; bf16, one
-    // 16-byte piece per lane of each chunk
-    constexpr int NPT = KV8 ? (4 * D + NT - 1) / NT : (CH * 64 + NT - 1) / NT;
-    __shared__ __attribute__((aligned(1024))) char smem[NBUF * SB];
+    constexpr int SB = CH * 1024;               // LDS bytes per staged block
+    // fragment ring: copies land 3 blocks ahead (4 slots, block b in slot b & 3)
+    constexpr int NBF = 4;
+    constexpr int AHEAD = 3;                    // copies of block s + AHEAD start in trip s
+    // copy jobs per block and wave: the CH chunks; int8, also the block's kappa (a 4-byte
+    // copy by every wave, into the slot's kappa row)
+    static_assert(CH % NW == 0, "copy jobs spread evenly over the waves");
+    constexpr int JPW = CH / NW + (KV8 ? 1 : 0);
+    constexpr int SBK = SB + 256;               // int8: bytes per staged block (kappa row last)
+    __shared__ __attribute__((aligned(1024))) char smem[NBF * SB];
+    __shared__ __attribute__((aligned(16))) float kap[KV8 ? NBF : 1][64];   // int8: kappa rows
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);     // wave index (uniform)
     const int l32 = lane & 31, h32 = lane >> 5;
-    const int ngrp = a.nh / HPW;
-    const int b = blockIdx.x / ngrp, hg = blockIdx.x % ngrp;
+    // workgroup -> (sequence, kv head, head group, query tile); a unit is a head group times
+    // a query tile of one (sequence, kv head).  While the caches of all sequences fit in
+    // half the 256 MB last-level cache, units go heaviest first over the whole grid (the
+    // latest query tiles of every kv head, then the next ones, ...), which balances the CUs
+    // best.  Larger caches would be streamed from HBM once per query tile; then the units
+    // of one kv head, heaviest first, are consecutive workgroups of one XCD (workgroup i
+    // runs on XCD i % 8) and stream the same blocks at about the same time through its L2.
+    const int hgs = a.nh / a.nkv / HPW;                // head groups per kv head
     const int nqt = (a.P + 32 * QW - 1) / (32 * QW);
-    const int qt = nqt - 1 - (int)blockIdx.y;          // heaviest first (y varies slowest)
-    const int h = hg * HPW + w % HPW;
-    const int kvh = (hg * HPW * a.nkv) / a.nh;         // shared by the HPW heads
+    const int units = hgs * nqt;
+    const int ngroups = (int)gridDim.x / units;       // sequences x kv heads
+    const int L = blockIdx.x;
+    int g, u;
+    if (ngroups % 8 == 0 && (int64_t)ngroups * a.P * D * (KV8 ? 2 : 4) > (128ll << 20)) {
+        g = (L >> 3) / units * 8 + (L & 7);
+        u = (L >> 3) % units;
+    } else {
+        const int hgi = L % hgs;
+        g = (L / hgs) % ngroups;
+        u = L / (hgs * ngroups) * hgs + hgi;
+    }
+    const int b = g / a.nkv, kvh = g % a.nkv;
+    const int qt = nqt - 1 - u / hgs;
+    const int h = (kvh * hgs + u % hgs) * HPW + w % HPW;
     const int q0 = qt * 32 * QW;
     const int wq0 = q0 + 32 * (w / HPW);               // this wave's first query
     const int wglast = min(a.P - 1, q0 + 32 * QW - 1);
@@ -84,160 +136,100 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     const int wlast = wq0 < a.P ? min(a.P - 1, wq0 + 31) / PK : -1;   // last block of the wave
     const float sl2 = a.scale * 1.4426950408889634f;   // scores in the base-2 domain
 
+    const int64_t crow0 = ((int64_t)b * a.nkv + kvh) * a.kv_stride;   // key row of position 0
+    const int64_t vblk0 = ((int64_t)b * a.nkv + kvh) * a.nblk;        // value block of position 0
+    const int nsb = (a.P + PK - 1) / PK;               // int8: staged blocks per (sequence, kv head)
+    i32x4 rk, rv;
+    if constexpr (KV8) {
+        rk = rsrc_words((const char*)a.staged + (int64_t)g * nsb * SBK, (uint32_t)((int64_t)nsb * SBK));
+        rv = rk;
+    } else {
+        rk = rsrc_words((const char*)a.kc + crow0 * D * 2, (uint32_t)((int64_t)a.kv_stride * D * 2));
+        rv = rsrc_words((const char*)a.vc + vblk0 * D * VT_BLK * 2, (uint32_t)((int64_t)a.nblk * D * VT_BLK * 2));
+    }
+    // the wave's copy jobs (job j = w + NW i): kind, per-lane offset, place in the slot
+    // (wave-uniform)
+    uint32_t jv[JPW];
+    int jkind[JPW];                                    // 0 K, 1 V, 2 kappa row
+    uint32_t jl[JPW];
+#pragma unroll
+    for (int i = 0; i < JPW; ++i) {
+        const int j = w + NW * i;
+        if (KV8 && i == JPW - 1) {
+            jkind[i] = 2;
+            jv[i] = (uint32_t)(SB + 4 * lane);
+            jl[i] = 0;
+        } else if constexpr (KV8) {                    // staged blocks are fragment-major already
+            jkind[i] = 0;
+            jv[i] = (uint32_t)(j * 1024 + 16 * lane);
+            jl[i] = (uint32_t)(j * 1024);
+        } else {
+            jl[i] = (uint32_t)(j * 1024);
+            if (j < NKC) {       // key l % 32, dims 16 j + 8 (l / 32) .. + 7
+                jkind[i] = 0;
+                jv[i] = (uint32_t)(((lane % 32) * D + 16 * j + 8 * (lane / 32)) * 2);
+            } else {             // value dims 32 dt + l % 32, slots 16 j2 + 8 (l / 32) .. + 7
+                const int t = j - NKC, j2 = t / (D / 32), dt = t % (D / 32);
+                jkind[i] = 1;
+                jv[i] = (uint32_t)((((32 * dt + lane % 32) * VT_BLK) + 16 * j2 + 8 * (lane / 32)) * 2);
+            }
+        }
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lvoid_t*)smem;
+    const uint32_t kap0 = (uint32_t)(uintptr_t)(lvoid_t*)&kap[0][0];
+    auto slot = [](int bb) { return bb & (NBF - 1); };
+    // copies of block bb (past the workgroup's blocks: of its last block, into bb's free
+    // slot, so that every wave issues JPW copies per block and the wait counts stay exact)
+    auto issue = [&](int bb) {
+        const int bc = min(bb, ns - 1);
+#pragma unroll
+        for (int i = 0; i < JPW; ++i) {
+            const int k = jkind[i];
+            if (k == 2) {
+                lds_copy<4>(rk, jv[i], (uint32_t)(bc * SBK), kap0 + (uint32_t)slot(bb) * 256u);
+            } else {
+                const uint32_t dst = (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + slot(bb) * SB + jl[i]);
+                if constexpr (KV8) lds_copy<16>(rk, jv[i], (uint32_t)(bc * SBK), dst);
+                else if (k == 0) lds_copy<16>(rk, jv[i], (uint32_t)(bc * PK * D * 2), dst);
+                else lds_copy<16>(rv, jv[i], (uint32_t)(bc * D * VT_BLK * 2), dst);
+            }
+        }
+    };
+    // all but the copies issued in the current trip are complete
+    auto wait_older_copies = [&]() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(JPW) : "memory"); };
+    auto wait_all_copies = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+    auto barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+
+    // the first blocks' copies go out before the queries are read
+    issue(0);
+    issue(1);
+    issue(2);
+
     // Q^T fragments for the D/16 k-steps: lane l supplies query l % 32, dims
-    // 16 j + 8 (l / 32) .. + 7
+    // 16 j + 8 (l / 32) .. + 7.  Every load is issued before any is used (one round trip):
+    // lanes past the prompt read row 0 and keep zeros.
     u32x4 qf[D / 16];
     const int qpos = wq0 + l32;
     {
         const bool qv = qpos < a.P;
         const float* qrow = a.q + ((int64_t)b * a.P + (qv ? qpos : 0)) * a.nh * D + h * D;
+        float4 x[D / 16][2];
 #pragma unroll
         for (int j = 0; j < D / 16; ++j) {
-            uint32_t v[4] = {0u, 0u, 0u, 0u};
-            if (qv) {
-                const float4 x0 = *(const float4*)(qrow + 16 * j + 8 * h32);
-                const float4 x1 = *(const float4*)(qrow + 16 * j + 8 * h32 + 4);
-                if constexpr (KV8) {
-                    v[0] = pack_f16_hw(x0.x, x0.y); v[1] = pack_f16_hw(x0.z, x0.w);
-                    v[2] = pack_f16_hw(x1.x, x1.y); v[3] = pack_f16_hw(x1.z, x1.w);
-                } else {
-                    v[0] = pack_bf16_hw(x0.x, x0.y); v[1] = pack_bf16_hw(x0.z, x0.w);
-                    v[2] = pack_bf16_hw(x1.x, x1.y); v[3] = pack_bf16_hw(x1.z, x1.w);
-                }
-            }
-            qf[j] = u32x4{v[0], v[1], v[2], v[3]};
+            x[j][0] = *(const float4*)(qrow + 16 * j + 8 * h32);
+            x[j][1] = *(const float4*)(qrow + 16 * j + 8 * h32 + 4);
+        }
+#pragma unroll
+        for (int j = 0; j < D / 16; ++j) {
+            const float4 x0 = x[j][0], x1 = x[j][1];
+            u32x4 v;
+            if constexpr (KV8) v = u32x4{pack_f16_hw(x0.x, x0.y), pack_f16_hw(x0.z, x0.w), pack_f16_hw(x1.x, x1.y), pack_f16_hw(x1.z, x1.w)};
+            else v = u32x4{pack_bf16_hw(x0.x, x0.y), pack_bf16_hw(x0.z, x0.w), pack_bf16_hw(x1.x, x1.y), pack_bf16_hw(x1.z, x1.w)};
+            qf[j] = qv ? v : u32x4{0u, 0u, 0u, 0u};
         }
     }
-
-    const int64_t crow0 = ((int64_t)b * a.nkv + kvh) * a.kv_stride;   // key row of position 0
-    const int64_t vblk0 = ((int64_t)b * a.nkv + kvh) * a.nblk;        // value block of position 0
-
-    // int8: kappa and sigma = the largest key and value scales over the prompt (1 if all
-    // are zero); the staged values are code * scale / kappa (or sigma), at most 127
-    float kappa = 1.f, sigma = 1.f;
-    if constexpr (KV8) {
-        float mk = 0.f, mv = 0.f;
-        for (int p0 = 0; p0 < a.P; p0 += 512) {      // 8 independent loads per lane and array
-            uint16_t kk[8], vv[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int p = p0 + 64 * i + lane;
-                kk[i] = p < a.P ? a.k_scales[crow0 + p] : (uint16_t)0;
-                vv[i] = p < a.P ? a.v_scales[crow0 + p] : (uint16_t)0;
-            }
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                mk = fmaxf(mk, h2f(kk[i]));
-                mv = fmaxf(mv, h2f(vv[i]));
-            }
-        }
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) {
-            mk = fmaxf(mk, __shfl_xor(mk, o, 64));
-            mv = fmaxf(mv, __shfl_xor(mv, o, 64));
-        }
-        kappa = mk > 0.f ? mk : 1.f;
-        sigma = mv > 0.f ? mv : 1.f;
-    }
-    const float kinv = 1.0f / kappa, vinv = 1.0f / sigma;
-    const float kmul = KV8 ? kappa * sl2 : sl2;        // score = S * kmul (base-2 domain)
-
-    // ---- staging of key block s into buffer s & (NBUF - 1).  Chunk j < NKC: K fragment
-    // of k-step j (lane l: key l % 32, dims 16 j + 8 (l / 32) .. + 7); chunk NKC + t,
-    // t = j2 (D / 32) + dt: V^T fragment of key step j2, dims 32 dt + l % 32, slots
-    // 16 j2 + 8 (l / 32) .. + 7 of the value block.
-    const __amdgpu_buffer_rsrc_t kr =
-        buf_rsrc((const char*)a.kc + crow0 * D * (KV8 ? 1 : 2), (uint32_t)((int64_t)a.kv_stride * D * (KV8 ? 1 : 2)));
-    const __amdgpu_buffer_rsrc_t vr =
-        buf_rsrc((const char*)a.vc + vblk0 * D * VT_BLK * (KV8 ? 1 : 2), (uint32_t)((int64_t)a.nblk * D * VT_BLK * (KV8 ? 1 : 2)));
-    // bf16: piece p = chunk p / 64, lane slot p % 64, loaded into registers and written to
-    // its place in the chunk
-    struct RegsB {
-        u32x4 v[NPT];
-    };
-    auto load_bf = [&](int s, RegsB& r) {
-#pragma unroll
-        for (int i = 0; i < NPT; ++i) {
-            const int p = tid + NT * i;
-            if (p >= CH * 64) break;
-            const int c = p / 64, l = p % 64;
-            if (c < NKC) {
-                r.v[i] = __builtin_amdgcn_raw_buffer_load_b128(
-                    kr, (uint32_t)(((s * PK + l % 32) * D + 16 * c + 8 * (l / 32)) * 2), 0, 0);
-            } else {
-                const int t = c - NKC, j2 = t / (D / 32), dt = t % (D / 32);
-                r.v[i] = __builtin_amdgcn_raw_buffer_load_b128(
-                    vr, (uint32_t)((((s * D + 32 * dt + l % 32) * VT_BLK) + 16 * j2 + 8 * (l / 32)) * 2), 0, 0);
-            }
-        }
-    };
-    auto store_bf = [&](int s, const RegsB& r) {
-        char* base = smem + (s & (NBUF - 1)) * SB;
-#pragma unroll
-        for (int i = 0; i < NPT; ++i) {
-            const int p = tid + NT * i;
-            if (p >= CH * 64) break;
-            *(u32x4*)(base + p * 16) = r.v[i];
-        }
-    };
-    // int8: 8-code pieces through registers, scaled on the way to LDS (one rounding); each
-    // thread takes pieces of both kinds.  K piece p: key p % 32, dims 8 (p / 32) .. + 7, times
-    // the key's scale over kappa, fp16.  V piece p: dim p % D, slots 8 o .. 8 o + 7
-    // (o = p / D), which hold positions 4 o .. + 3 and 16 + 4 o .. + 3 of the block
-    // (vt_slot order), each times its scale over sigma, bf16.  The value scales over sigma
-    // (32 per block) are staged in LDS one block ahead of their codes by threads 0 .. 31.
-    __shared__ __attribute__((aligned(16))) float vsl[KV8 ? NBUF : 1][PK];
-    struct Regs {
-        u32x2 k[NPT], v[NPT];
-        uint16_t ks[NPT];
-        uint16_t vs;
-    };
-    auto load_codes = [&](int s, Regs& r) {
-#pragma unroll
-        for (int i = 0; i < NPT; ++i) {
-            const int p = tid + NT * i;
-            if (p >= 4 * D) break;
-            r.k[i] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(
-                                                   kr, (uint32_t)((s * PK + p % 32) * D + 8 * (p / 32)), 0, 0));
-            r.ks[i] = a.k_scales[crow0 + s * PK + p % 32];
-            r.v[i] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(
-                                                   vr, (uint32_t)((s * D + p % D) * VT_BLK + 8 * (p / D)), 0, 0));
-        }
-    };
-    auto load_vscale = [&](int s, Regs& r) {
-        if (tid < PK) r.vs = a.v_scales[crow0 + s * PK + tid];
-    };
-    auto store_vscale = [&](int s, const Regs& r) {
-        if (tid < PK) vsl[s & (NBUF - 1)][tid] = h2f(r.vs) * vinv;
-    };
-    auto store_codes = [&](int s, const Regs& r) {
-        char* base = smem + (s & (NBUF - 1)) * SB;
-        const float* sv = vsl[s & (NBUF - 1)];
-#pragma unroll
-        for (int i = 0; i < NPT; ++i) {
-            const int p = tid + NT * i;
-            if (p >= 4 * D) break;
-            {
-                const int o = p / 32;
-                const u32x2 c0 = i8x4_to_f16x4(r.k[i].x), c1 = i8x4_to_f16x4(r.k[i].y);
-                const uint32_t k1 = f2h(h2f(r.ks[i]) * kinv), k2 = k1 | (k1 << 16);
-                *(u32x4*)(base + (o >> 1) * 1024 + ((p % 32) + 32 * (o & 1)) * 16) =
-                    u32x4{mul_f16x2(c0.x, k2), mul_f16x2(c0.y, k2), mul_f16x2(c1.x, k2), mul_f16x2(c1.y, k2)};
-            }
-            {
-                const int o = p / D, dim = p % D;
-                const f32x4 sa = *(const f32x4*)(sv + 4 * o), sb = *(const f32x4*)(sv + 16 + 4 * o);
-                // code j of a dword: signed byte j, times its position's scale, to bf16
-                auto cv = [](uint32_t wd, const f32x4& sc) {
-                    return u32x2{pack_bf16_hw((float)(int8_t)wd * sc[0], (float)(int8_t)(wd >> 8) * sc[1]),
-                                 pack_bf16_hw((float)(int8_t)(wd >> 16) * sc[2], (float)(int8_t)(wd >> 24) * sc[3])};
-                };
-                const u32x2 e0 = cv(r.v[i].x, sa), e1 = cv(r.v[i].y, sb);
-                *(u32x4*)(base + (NKC + (o >> 1) * (D / 32) + dim / 32) * 1024 + ((dim % 32) + 32 * (o & 1)) * 16) =
-                    u32x4{e0.x, e0.y, e1.x, e1.y};
-            }
-        }
-    };
+    // score multiplier of block bb (base-2 domain): int8, times the block's kappa
+    auto kmul_of = [&](int bb) { return KV8 ? kap[slot(bb)][0] * sl2 : sl2; };
 
     // ---- softmax helpers.  Element e of a lane holds key offset 8 (e / 4) + e % 4 + 4 h32
     // of the block; it is live when that offset (less 4 h32) is at most lim (the key passes
@@ -250,11 +242,11 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
         pf[(e >> 2) & 1][((e & 3) >> 1) + 2 * (e >> 3)] = pack_bf16_hw(x0, x1);
     };
     // exact maximum of the block's live scores (base-2 domain), across the lane halves
-    auto block_max = [&](int s, const f32x16& acc, bool masked) {
+    auto block_max = [&](int s, const f32x16& acc, bool masked, float km) {
         const int lim = masked ? limit(s) : PK;
         float t = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) t = fmaxf(t, koff(e) <= lim ? acc[e] * kmul : -INFINITY);
+        for (int e = 0; e < 16; ++e) t = fmaxf(t, koff(e) <= lim ? acc[e] * km : -INFINITY);
         return fmaxf(t, __shfl_xor(t, 32, 64));
     };
 
@@ -263,14 +255,14 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     bool over = false;
 
     auto qk = [&](int s) {
-        const char* kb = smem + (s & (NBUF - 1)) * SB + lane * 16;
+        const char* kb = smem + slot(s) * SB + lane * 16;
         f32x16 acc = f32x16{};
 #pragma unroll
         for (int j = 0; j < D / 16; ++j) acc = mfma32<AQ>(*(const u32x4*)(kb + j * 1024), qf[j], acc);
         return acc;
     };
     auto pv = [&](int s, const u32x4 (&pf)[2]) {
-        const char* vb = smem + (s & (NBUF - 1)) * SB + NKC * 1024 + lane * 16;
+        const char* vb = smem + slot(s) * SB + NKC * 1024 + lane * 16;
 #pragma unroll
         for (int j2 = 0; j2 < 2; ++j2)
 #pragma unroll
@@ -279,14 +271,15 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     };
     // block 0: its exact maximum (at least the reference carried over) becomes the reference
     auto first_block = [&](bool masked, const f32x16& acc, u32x4 (&pf)[2]) {
-        m_ref = fmaxf(m_ref, block_max(0, acc, masked));
+        const float km = kmul_of(0);
+        m_ref = fmaxf(m_ref, block_max(0, acc, masked, km));
         const float ms = m_ref == -INFINITY ? 0.f : m_ref;
         const int lim = masked ? limit(0) : PK;
         float psum = 0.f;
 #pragma unroll
         for (int e = 0; e < 16; e += 2) {
-            const float x0 = koff(e) <= lim ? __builtin_amdgcn_exp2f(fmaf(acc[e], kmul, -ms)) : 0.f;
-            const float x1 = koff(e + 1) <= lim ? __builtin_amdgcn_exp2f(fmaf(acc[e + 1], kmul, -ms)) : 0.f;
+            const float x0 = koff(e) <= lim ? __builtin_amdgcn_exp2f(fmaf(acc[e], km, -ms)) : 0.f;
+            const float x1 = koff(e + 1) <= lim ? __builtin_amdgcn_exp2f(fmaf(acc[e + 1], km, -ms)) : 0.f;
             psum += x0 + x1;
             put_pair(pf, e, x0, x1);
         }
@@ -296,13 +289,14 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     // next block (into nxt) run
     auto next_block = [&](int s, auto dm, const f32x16& acc, f32x16& nxt, u32x4 (&pf)[2]) {
         constexpr bool DM = decltype(dm)::value;
+        const float km = kmul_of(s);
         nxt = qk(s + 1);
         int lim = 0;
         if constexpr (DM) lim = limit(s);
         float pmax = 0.f, psum = 0.f;
 #pragma unroll
         for (int e = 0; e < 16; e += 2) {
-            float v0 = fmaf(acc[e], kmul, -m_ref), v1 = fmaf(acc[e + 1], kmul, -m_ref);
+            float v0 = fmaf(acc[e], km, -m_ref), v1 = fmaf(acc[e + 1], km, -m_ref);
             if constexpr (DM) {
                 v0 = koff(e) <= lim ? v0 : -INFINITY;
                 v1 = koff(e + 1) <= lim ? v1 : -INFINITY;
@@ -314,7 +308,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
         }
         if (__ballot(!(pmax <= a.pmax))) {
             asm volatile("" ::: "memory");     // a real branch: never computed speculatively
-            m_seen = fmaxf(m_seen, block_max(s, acc, DM));
+            m_seen = fmaxf(m_seen, block_max(s, acc, DM, km));
             over = true;
         }
         l_run += psum;
@@ -323,30 +317,13 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     using F_ = std::integral_constant<bool, false>;
     auto masked_block = [&](int s) { return s * PK + PK - 1 > wq0 || s * PK + PK > a.P; };
 
-    // ---- block loop: block s is multiplied while block s + 2 is brought in through
-    // registers (int8: and the value scales of block s + 3); the waves meet after each block.
-    using Stage = typename std::conditional<KV8, Regs, RegsB>::type;
-    Stage rg;
-    auto load_block = [&](int s) {
-        if constexpr (KV8) load_codes(s, rg);
-        else load_bf(s, rg);
-    };
-    auto store_block = [&](int s) {
-        if constexpr (KV8) store_codes(s, rg);
-        else store_bf(s, rg);
-    };
-    auto sync_after = [&](int s) {
-        if (s + 2 < ns) store_block(s + 2);
-        if constexpr (KV8) {
-            if (s + 3 < ns) store_vscale(s + 3, rg);
-        }
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    };
-    auto prefetch = [&](int s) {
-        if (s + 2 < ns) load_block(s + 2);
-        if constexpr (KV8) {
-            if (s + 3 < ns) load_vscale(s + 3, rg);
-        }
+    // ---- block loop.  Trip s multiplies block s (and S of block s + 1) while the copies of
+    // block s + AHEAD are in flight; at its end the copies of the previous trip are complete,
+    // and the waves meet.
+    auto trip_begin = [&](int s) { issue(s + AHEAD); };
+    auto trip_end = [&](int s) {
+        wait_older_copies();
+        barrier();
     };
 
     // at most two passes: the second only if a probability left the range, with the
@@ -356,23 +333,19 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
         for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = f32x16{};
         l_run = 0.f;
         over = false;
-        if constexpr (KV8) {
-            // value scales of blocks 0 .. 2 first: a block's codes are scaled with them
-            for (int t = 0; t < 3 && t < ns; ++t) {
-                load_vscale(t, rg);
-                store_vscale(t, rg);
-            }
-            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (pass > 0) {                  // copies left by the first pass go to free slots
+            wait_all_copies();
+            barrier();
+            issue(0);
+            issue(1);
+            issue(2);
         }
-        for (int t = 0; t < 2 && t < ns; ++t) {
-            load_block(t);
-            store_block(t);
-        }
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        wait_all_copies();
+        barrier();
         // S of block s + 1 is computed in trip s, beside the softmax of block s; the two S
         // registers alternate (two trips per loop turn)
         f32x16 accA, accB;
-        prefetch(0);
+        trip_begin(0);
         {
             u32x4 pf[2] = {u32x4{0u, 0u, 0u, 0u}, u32x4{0u, 0u, 0u, 0u}};
             if (0 <= wlast) {
@@ -382,15 +355,15 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
             }
             pv(0, pf);
         }
-        sync_after(0);
+        trip_end(0);
         // the P.V MFMAs stay on one path, so they accumulate in place
         auto trip = [&](int s, const f32x16& cur, f32x16& nxt) {
-            prefetch(s);
+            trip_begin(s);
             u32x4 pf[2];
             if (masked_block(s)) next_block(s, T_{}, cur, nxt, pf);
             else next_block(s, F_{}, cur, nxt, pf);
             pv(s, pf);
-            sync_after(s);
+            trip_end(s);
         };
         int s = 1;
         for (; s + 1 <= wlast; s += 2) {
@@ -399,16 +372,17 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
         }
         if (s <= wlast) trip(s++, accB, accA);
         for (; s < ns; ++s) {                  // a wave past its queries keeps staging blocks
-            prefetch(s);
-            sync_after(s);
+            trip_begin(s);
+            trip_end(s);
         }
         if (!__syncthreads_or(over)) break;
         m_ref = fmaxf(m_ref, m_seen);
     }
+    wait_all_copies();                         // no copy outlives the workgroup
 
     const float lt = l_run + __shfl_xor(l_run, 32, 64);
     if (qpos >= a.P) return;
-    const float inv = (KV8 ? sigma : 1.f) / lt;
+    const float inv = 1.f / lt;
     uint16_t* orow = a.out + ((int64_t)b * a.P + qpos) * a.nh * D + h * D;
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
@@ -422,22 +396,89 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
         }
 }
 
-// Workgroups: 32 queries per wave; HPW = the largest of 8, 4, 2, 1 that divides both the
-// heads per kv head and the waves; 8 waves (two per SIMD).  bf16 caches drop to 4, 2 or 1
+// int8 caches: dequantise block blk of the prompt of (sequence, kv head) g into the
+// fragment-major layout attn_prefill_kernel copies: K chunk c, lane l = key l % 32, dims
+// 16 c + 8 (l / 32) .. + 7 as fp16 code * s_k / kappa_b; V chunk NKC + t (t = j2 (D / 32) +
+// dt), lane l = dim 32 dt + l % 32, slots 16 j2 + 8 (l / 32) .. + 7 as bf16 code * s_v
+// (slots 8 o .. 8 o + 7 hold positions 4 o .. + 3 and 16 + 4 o .. + 3, vt_slot order); then
+// kappa_b 64 times.  Positions past the prompt become zeros.
+template <int D>
+__global__ void __launch_bounds__(256) attn_stage_kernel(AttnPreArgs a) {
+    constexpr int NKC = D / 16, NVC = 2 * (D / 32), CH = NKC + NVC, SBK = CH * 1024 + 256;
+    const int blk = blockIdx.x, g = blockIdx.y, nsb = gridDim.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int64_t crow0 = (int64_t)g * a.kv_stride;
+    const int p0 = blk * PK;
+    char* out = (char*)a.staged + ((int64_t)g * nsb + blk) * SBK;
+    // kappa_b: lanes l and l + 32 of every wave take key l % 32 (the key of all their K items)
+    const int key = lane & 31;
+    const float ks0 = h2f(a.k_scales[crow0 + p0 + key]);
+    const float ks = p0 + key < a.P ? ks0 : 0.f;
+    float km = ks;
+#pragma unroll
+    for (int o = 16; o >= 1; o >>= 1) km = fmaxf(km, __shfl_xor(km, o, 32));
+    const float kappa = km > 0.f ? km : 1.f;
+    if (tid < 64) ((float*)(out + CH * 1024))[tid] = kappa;
+    const uint32_t k1 = f2h(ks / kappa), k2 = k1 | (k1 << 16);
+    for (int it = tid; it < NKC * 64; it += 256) {
+        const int c = it / 64;
+        const u32x2 code = *(const u32x2*)((const int8_t*)a.kc + (crow0 + p0 + key) * D + 16 * c + 8 * (lane / 32));
+        const u32x2 c0 = i8x4_to_f16x4(code.x), c1 = i8x4_to_f16x4(code.y);
+        *(u32x4*)(out + c * 1024 + lane * 16) =
+            u32x4{mul_f16x2(c0.x, k2), mul_f16x2(c0.y, k2), mul_f16x2(c1.x, k2), mul_f16x2(c1.y, k2)};
+    }
+    const uint16_t* vs = a.v_scales + crow0 + p0;
+    for (int it = tid; it < NVC * 64; it += 256) {
+        const int t = it / 64, j2 = t / (D / 32), dt = t % (D / 32);
+        const int dim = 32 * dt + lane % 32, o = 2 * j2 + lane / 32;
+        const u32x2 code = *(const u32x2*)((const int8_t*)a.vc + (((int64_t)g * a.nblk + blk) * D + dim) * VT_BLK + 8 * o);
+        // positions 4 o .. + 3 and 16 + 4 o .. + 3: whole 8-byte words inside the cache rows
+        // (rows are whole blocks), positions past the prompt zeroed after the load
+        const u32x2 sa = *(const u32x2*)(vs + 4 * o), sb = *(const u32x2*)(vs + 16 + 4 * o);
+        const uint32_t sw[4] = {sa.x, sa.y, sb.x, sb.y};
+        float sc[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int pos = p0 + (i < 4 ? 4 * o + i : 16 + 4 * o + i - 4);
+            const float v = h2f((uint16_t)(sw[i / 2] >> (16 * (i & 1))));
+            sc[i] = pos < a.P ? v : 0.f;
+        }
+        auto cv = [&](uint32_t wd, int i0) {
+            return u32x2{pack_bf16_hw((float)(int8_t)wd * sc[i0], (float)(int8_t)(wd >> 8) * sc[i0 + 1]),
+                         pack_bf16_hw((float)(int8_t)(wd >> 16) * sc[i0 + 2], (float)(int8_t)(wd >> 24) * sc[i0 + 3])};
+        };
+        const u32x2 e0 = cv(code.x, 0), e1 = cv(code.y, 4);
+        *(u32x4*)(out + (NKC + t) * 1024 + lane * 16) = u32x4{e0.x, e0.y, e1.x, e1.y};
+    }
+}
+
+size_t attn_stage_bytes(int B, int P, int nkv, int d) {
+    return (size_t)B * nkv * ((P + PK - 1) / PK) * (size_t)(4 * d / 16 * 1024 + 256);
+}
+
+hipError_t launch_attn_stage(const AttnPreArgs& a, int B, hipStream_t st) {
+    if (!a.kv_int8 || a.staged == nullptr || B < 1 || a.P < 1 || a.nkv < 1) return hipErrorInvalidValue;
+    if (a.nblk * VT_BLK < a.P || a.kv_stride < a.nblk * VT_BLK || a.kv_stride % 4 != 0) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((a.P + PK - 1) / PK), (unsigned)(B * a.nkv));
+    if (a.d == 128) FP_LAUNCH(attn_stage_kernel<128>, grid, dim3(256), 0, st, a);
+    else if (a.d == 64) FP_LAUNCH(attn_stage_kernel<64>, grid, dim3(256), 0, st, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+// Workgroups: 32 queries per wave; HPW = the largest of 4, 2, 1 that divides both the heads
+// per kv head and the waves; 4 waves, two workgroups per CU.  bf16 caches drop to 2 or 1
 // wave while the grid is under 128 workgroups (a single short prompt: more, smaller
 // workgroups spread the causal critical path over more CUs).
 template <int D, bool KV8, int NW, int HPW>
 static void launch_shape(const AttnPreArgs& a, int B, hipStream_t st) {
     const int wq = 32 * (NW / HPW);
-    FP_LAUNCH((attn_prefill_kernel<D, KV8, NW, HPW>), dim3((unsigned)(a.nh / HPW * B), (unsigned)((a.P + wq - 1) / wq)),
-              dim3(64 * NW), 0, st, a);
+    const int64_t n = (int64_t)B * (a.nh / HPW) * ((a.P + wq - 1) / wq);
+    FP_LAUNCH((attn_prefill_kernel<D, KV8, NW, HPW>), dim3((unsigned)n), dim3(64 * NW), 0, st, a);
 }
 
 template <int D, bool KV8, int NW>
 static void launch_nw(const AttnPreArgs& a, int B, int hpw, hipStream_t st) {
-    if constexpr (NW >= 8) {
-        if (hpw >= 8) return launch_shape<D, KV8, NW, 8>(a, B, st);
-    }
     if constexpr (NW >= 4) {
         if (hpw >= 4) return launch_shape<D, KV8, NW, 4>(a, B, st);
     }
@@ -450,18 +491,17 @@ static void launch_nw(const AttnPreArgs& a, int B, int hpw, hipStream_t st) {
 template <int D, bool KV8>
 static hipError_t launch_ap(const AttnPreArgs& a, int B, hipStream_t st) {
     const int gq = a.nh / a.nkv;
-    const int hmax = gq % 8 == 0 ? 8 : gq % 4 == 0 ? 4 : gq % 2 == 0 ? 2 : 1;
+    const int hmax = gq % 4 == 0 ? 4 : gq % 2 == 0 ? 2 : 1;
     auto grid = [&](int n) {
         const int hp = hmax < n ? hmax : n, wq = 32 * (n / hp);
         return (int64_t)((a.P + wq - 1) / wq) * (a.nh / hp) * B;
     };
-    int nw = 8;
+    int nw = 4;
     if constexpr (!KV8)
         while (nw > 1 && grid(nw) < 128) nw /= 2;
     const int hpw = hmax < nw ? hmax : nw;
-    if ((int64_t)(a.nh / hpw) * B > INT_MAX) return hipErrorInvalidValue;
-    if (nw == 8) launch_nw<D, KV8, 8>(a, B, hpw, st);
-    else if (nw == 4) launch_nw<D, KV8, 4>(a, B, hpw, st);
+    if ((int64_t)(a.nh / hpw) * B * ((a.P + 31) / 32) > INT_MAX) return hipErrorInvalidValue;
+    if (nw == 4) launch_nw<D, KV8, 4>(a, B, hpw, st);
     else if constexpr (!KV8) {
         if (nw == 2) launch_nw<D, KV8, 2>(a, B, hpw, st);
         else launch_nw<D, KV8, 1>(a, B, hpw, st);
@@ -471,6 +511,7 @@ static hipError_t launch_ap(const AttnPreArgs& a, int B, hipStream_t st) {
 
 hipError_t launch_attn_prefill(const AttnPreArgs& a, int B, hipStream_t st) {
     if (B < 1 || a.P < 1 || a.nkv < 1 || a.nh % a.nkv != 0) return hipErrorInvalidValue;
+    if (a.kv_int8 && a.staged == nullptr) return hipErrorInvalidValue;
     // every key block of the prompt lies inside the cache rows of its (sequence, kv head)
     if (a.nblk * VT_BLK < a.P || a.kv_stride < a.nblk * VT_BLK) return hipErrorInvalidValue;
     if (a.d == 128) return a.kv_int8 ? launch_ap<128, true>(a, B, st) : launch_ap<128, false>(a, B, st);

@@ -163,6 +163,9 @@ struct fp_layer {
     uint16_t* xbuf = nullptr;     // inter-layer hidden state              [Mmax, H]
     float* qkv32 = nullptr;       // prefill q|k|v before rotary          [Mmax, Nqkv]
     float* q32 = nullptr;         // rotated queries                      [Mmax, q_dim]
+    void* stage = nullptr;        // int8 caches: the prompt's K / V blocks dequantised for
+                                  // prefill attention (act_f when that is large enough: it is
+                                  // idle between the rotary step and the gate/up projection)
     float* part = nullptr;        // decode split-K partials              [KSMAX, Bmax, Ncol]
     float* part2 = nullptr;       // gate|up partials (read while down writes part)
     float* ppart = nullptr;       // prefill split-K partials (GEMMs with too few large tiles)
@@ -629,6 +632,7 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
         aa.vc = h->vc[l];
         aa.k_scales = h->ksc[l];
         aa.v_scales = h->vsc[l];
+        aa.staged = h->stage;
         aa.kv_int8 = h->kvq == FP_KV_INT8;
         aa.P = P;
         aa.nh = s.n_heads;
@@ -642,6 +646,7 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
         aa.out = h->act_o;
         aa.out_fmt = h->act_fmt;
         h->prof.mark(FP_K_ATTN, l);
+        if (aa.kv_int8) HIPCHK(launch_attn_stage(aa, B, st));
         HIPCHK(launch_attn_prefill(aa, B, st));
         h->prof.mark(FP_K_O, l);
         if (ks_o > 1) {
@@ -982,6 +987,11 @@ fp_status alloc_storage(fp_layer* h) {
     if ((st = alloc_t(h, &h->act_in, Mmax * H, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->act_o, Mmax * h->q_dim, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->act_f, Mmax * F, &h->bytes_ws))) return st;
+    if (kvq == FP_KV_INT8) {
+        const size_t need = attn_stage_bytes(s.max_batch, s.max_prompt, s.n_kv_heads, s.head_dim);
+        if (need <= Mmax * F * sizeof(uint16_t)) h->stage = h->act_f;
+        else if ((st = dev_alloc(h, &h->stage, need, &h->bytes_ws))) return st;
+    }
     if ((st = alloc_t(h, &h->hbuf, Mmax * H, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->xbuf, Mmax * H, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->qkv32, Mmax * h->nqkv, &h->bytes_ws))) return st;

@@ -154,6 +154,7 @@ struct AttnPreArgs {
     const void* vc;
     const uint16_t* k_scales;
     const uint16_t* v_scales;
+    void* staged;             // int8: the prompt's blocks dequantised by attn_stage_kernel
     int kv_int8, P, nh, nkv, d, max_seq, nblk;
     int kv_stride;            // key / scale rows per (sequence, kv head)
     float scale;
@@ -162,6 +163,9 @@ struct AttnPreArgs {
     int out_fmt;
 };
 
+// bytes of the int8 prompt staging buffer for B sequences of P tokens (0 for bf16 caches)
+size_t attn_stage_bytes(int B, int P, int nkv, int d);
+hipError_t launch_attn_stage(const AttnPreArgs& a, int B, hipStream_t st);
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint64_t key, float mean, float sigma,
                             hipStream_t st);
 // Fragment-major weight layout (see tile_kernel): KS = k per 1 KiB block row-slice (2:4 sparse
