@@ -205,27 +205,25 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     issue(1);
     issue(2);
 
-    // Q^T fragments for the D/16 k-steps: lane l supplies query l % 32, dims
-    // 16 j + 8 (l / 32) .. + 7.  Every load is issued before any is used (one round trip):
-    // lanes past the prompt read row 0 and keep zeros.
+    // Q^T fragments for the D/16 k-steps (the rotary step wrote them in the operand
+    // format): lane l supplies query l % 32, dims 16 j + 8 (l / 32) .. + 7.  Every load is
+    // issued before any is used (one round trip); lanes past the prompt read row 0 and
+    // keep zeros.
     u32x4 qf[D / 16];
     const int qpos = wq0 + l32;
     {
         const bool qv = qpos < a.P;
-        const float* qrow = a.q + ((int64_t)b * a.P + (qv ? qpos : 0)) * a.nh * D + h * D;
-        float4 x[D / 16][2];
+        const uint16_t* qrow = a.q + (((int64_t)b * a.nh + h) * a.P + (qv ? qpos : 0)) * D;
+        u32x4 x[D / 16];
+#pragma unroll
+        for (int j = 0; j < D / 16; ++j) x[j] = *(const u32x4*)(qrow + 16 * j + 8 * h32);
 #pragma unroll
         for (int j = 0; j < D / 16; ++j) {
-            x[j][0] = *(const float4*)(qrow + 16 * j + 8 * h32);
-            x[j][1] = *(const float4*)(qrow + 16 * j + 8 * h32 + 4);
-        }
-#pragma unroll
-        for (int j = 0; j < D / 16; ++j) {
-            const float4 x0 = x[j][0], x1 = x[j][1];
-            u32x4 v;
-            if constexpr (KV8) v = u32x4{pack_f16_hw(x0.x, x0.y), pack_f16_hw(x0.z, x0.w), pack_f16_hw(x1.x, x1.y), pack_f16_hw(x1.z, x1.w)};
-            else v = u32x4{pack_bf16_hw(x0.x, x0.y), pack_bf16_hw(x0.z, x0.w), pack_bf16_hw(x1.x, x1.y), pack_bf16_hw(x1.z, x1.w)};
-            qf[j] = qv ? v : u32x4{0u, 0u, 0u, 0u};
+            qf[j] = qv ? x[j] : u32x4{0u, 0u, 0u, 0u};
+            // the loads are complete here: the compiler does not see the asm waits, and its
+            // own wait for them would otherwise sit inside the block loop (before the first
+            // MFMA of every trip) and drain the block copies in flight
+            asm volatile("" : "+v"(qf[j]));
         }
     }
     // score multiplier of block bb (base-2 domain): int8, times the block's kappa

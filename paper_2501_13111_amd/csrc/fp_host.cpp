@@ -162,7 +162,7 @@ struct fp_layer {
     uint16_t* hbuf = nullptr;     // h = x + attention projection         [Mmax, H]
     uint16_t* xbuf = nullptr;     // inter-layer hidden state              [Mmax, H]
     float* qkv32 = nullptr;       // prefill q|k|v before rotary          [Mmax, Nqkv]
-    float* q32 = nullptr;         // rotated queries                      [Mmax, q_dim]
+    uint16_t* q16 = nullptr;      // rotated queries (fp16 / bf16)        [Mmax, q_dim]
     void* stage = nullptr;        // int8 caches: the prompt's K / V blocks dequantised for
                                   // prefill attention (act_f when that is large enough: it is
                                   // idle between the rotary step and the gate/up projection)
@@ -561,7 +561,7 @@ RopeKvArgs rope_args(fp_layer* h, int l, const float* part, int ks, int M, int T
     r.max_seq = h->s.max_seq;
     r.nblk = vt_blocks(h->s.max_seq);
     r.kv_stride = kv_row_stride(h->s.max_seq);
-    r.qout = h->q32;
+    r.qout = h->q16;
     r.kc = h->kc[l];
     r.vc = h->vc[l];
     r.ks_out = h->ksc[l];
@@ -627,7 +627,7 @@ fp_status enqueue_prefill(fp_layer* h, const uint16_t* x, int B, int P, uint16_t
         h->prof.mark(FP_K_ROPE_KV, l);
         HIPCHK(launch_rope_kv(rope_args(h, l, h->qkv32, 1, M, P, nullptr, dump), st));
         AttnPreArgs aa{};
-        aa.q = h->q32;
+        aa.q = h->q16;
         aa.kc = h->kc[l];
         aa.vc = h->vc[l];
         aa.k_scales = h->ksc[l];
@@ -995,7 +995,7 @@ fp_status alloc_storage(fp_layer* h) {
     if ((st = alloc_t(h, &h->hbuf, Mmax * H, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->xbuf, Mmax * H, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->qkv32, Mmax * h->nqkv, &h->bytes_ws))) return st;
-    if ((st = alloc_t(h, &h->q32, Mmax * h->q_dim, &h->bytes_ws))) return st;
+    if ((st = alloc_t(h, &h->q16, Mmax * h->q_dim, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->part, (size_t)KSMAX * s.max_batch * ncol, &h->bytes_ws))) return st;
     if ((st = alloc_t(h, &h->part2, (size_t)KSMAX * s.max_batch * 2 * F, &h->bytes_ws))) return st;
     {

@@ -115,7 +115,7 @@ struct RopeKvArgs {
     const float* sin_t;
     int max_seq, nblk;        // nblk: value blocks per (sequence, kv head)
     int kv_stride;            // key / scale rows per (sequence, kv head)
-    float* qout;              // [M, nh*d]
+    uint16_t* qout;           // [M / T, nh, T, d] rotated queries: fp16 with an int8 cache, else bf16
     void* kc;
     void* vc;
     uint16_t* ks_out;
@@ -149,7 +149,7 @@ struct AttnDecArgs {
 };
 
 struct AttnPreArgs {
-    const float* q;           // [B*P, nh*d]
+    const uint16_t* q;        // [B, nh, P, d] rotated queries: fp16 with an int8 cache, else bf16
     const void* kc;
     const void* vc;
     const uint16_t* k_scales;

@@ -198,26 +198,35 @@ __global__ void __launch_bounds__(256) swiglu_kernel(const float* __restrict__ p
 // ---------------------------------------------------------------- rotary + KV append (prefill)
 // qkv: the projection output [M, Nqkv] fp32 (columns: q heads, then k heads, then v
 // heads); token m is sequence m / T at position m % T.
-// Rotated queries: fp32 [M, nh*d], one thread per rotation pair (i, i + d/2).
+// Rotated queries head-major [M / T, nh, T, d] (each head's queries of a sequence
+// contiguous) in the attention's operand format (fp16 with an int8 cache, else bf16;
+// rounded to nearest even once here), one thread per two rotation pairs
+// (j, j + d/2) and (j + 1, j + 1 + d/2), so that every store is a whole dword.
 #pragma clang fp contract(off)
+template <bool F16>
 __global__ void __launch_bounds__(256) rope_q_kernel(const float* __restrict__ qkv, int M, int T, int nh,
                                                       int nkv, int d, const float* __restrict__ cos_t,
-                                                      const float* __restrict__ sin_t, float* __restrict__ qout) {
-    const int half = d / 2;
+                                                      const float* __restrict__ sin_t, uint16_t* __restrict__ qout) {
+    const int half = d / 2, hp = half / 2;
     const int Nqkv = (nh + 2 * nkv) * d;
-    const int64_t n = (int64_t)M * nh * half;
+    const int64_t n = (int64_t)M * nh * hp;
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
-        const int j = (int)(i % half);
-        const int64_t mh = i / half;
+        const int j = 2 * (int)(i % hp);
+        const int64_t mh = i / hp;
         const int h = (int)(mh % nh);
         const int64_t m = mh / nh;
         const int pos = (int)(m % T);
         const float* p = qkv + m * Nqkv + (int64_t)h * d;
-        const float u = p[j], v = p[j + half];
-        const float c = cos_t[(int64_t)pos * half + j], s = sin_t[(int64_t)pos * half + j];
-        float* q = qout + m * nh * d + (int64_t)h * d;
-        q[j] = __fsub_rn(__fmul_rn(u, c), __fmul_rn(v, s));
-        q[j + half] = __fadd_rn(__fmul_rn(v, c), __fmul_rn(u, s));
+        const float2 u = *(const float2*)(p + j), v = *(const float2*)(p + j + half);
+        const float2 c = *(const float2*)(cos_t + (int64_t)pos * half + j);
+        const float2 s = *(const float2*)(sin_t + (int64_t)pos * half + j);
+        const float lo0 = __fsub_rn(__fmul_rn(u.x, c.x), __fmul_rn(v.x, s.x));
+        const float lo1 = __fsub_rn(__fmul_rn(u.y, c.y), __fmul_rn(v.y, s.y));
+        const float hi0 = __fadd_rn(__fmul_rn(v.x, c.x), __fmul_rn(u.x, s.x));
+        const float hi1 = __fadd_rn(__fmul_rn(v.y, c.y), __fmul_rn(u.y, s.y));
+        uint16_t* q = qout + (((m / T) * nh + h) * T + pos) * d;
+        *(uint32_t*)(q + j) = F16 ? pack_f16_hw(lo0, lo1) : pack_bf16_hw(lo0, lo1);
+        *(uint32_t*)(q + j + half) = F16 ? pack_f16_hw(hi0, hi1) : pack_bf16_hw(hi0, hi1);
     }
 }
 
@@ -343,10 +352,15 @@ hipError_t launch_swiglu(const float* part, int ks, int M, int F, uint16_t* a, i
 
 hipError_t launch_rope_kv(const RopeKvArgs& a, hipStream_t st) {
     if (a.ks != 1 || a.d_pos != nullptr || a.d > 128 || a.M % a.T != 0) return hipErrorInvalidValue;
-    const int64_t pairs = (int64_t)a.M * a.nh * (a.d / 2);
+    if (a.d % 4 != 0) return hipErrorInvalidValue;
+    const int64_t pairs = (int64_t)a.M * a.nh * (a.d / 4);
     const int nb = (int)std::min<int64_t>((pairs + 255) / 256, 8192);
-    FP_LAUNCH(rope_q_kernel, dim3(nb), dim3(256), 0, st, a.part, a.M, a.T, a.nh, a.nkv, a.d, a.cos_t, a.sin_t,
-              a.qout);
+    if (a.kv_int8)
+        FP_LAUNCH(rope_q_kernel<true>, dim3(nb), dim3(256), 0, st, a.part, a.M, a.T, a.nh, a.nkv, a.d, a.cos_t,
+                  a.sin_t, a.qout);
+    else
+        FP_LAUNCH(rope_q_kernel<false>, dim3(nb), dim3(256), 0, st, a.part, a.M, a.T, a.nh, a.nkv, a.d, a.cos_t,
+                  a.sin_t, a.qout);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const dim3 grid((a.T + VT_BLK - 1) / VT_BLK, a.nkv, a.M / a.T);
