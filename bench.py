@@ -46,7 +46,7 @@ PROJ = {"qkv", "o", "gate_up", "down"}
 # fp_internal.h); the summaries and commands are in profiles/.
 TRAFFIC = {
     ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "f4b5df64886dc990", "bytes_per_launch": 8561753373},
-    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "a81c9ea5d6815384", "bytes_per_launch": 1237281570},
+    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "08d150b3fca9ae0d", "bytes_per_launch": 2808682845},
     ("decode_proj", "llama2-70b-tp8-int4"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 27162882},
     ("decode_attn", "llama2-70b-tp8-int4"): {"src": "2af41be9a5c124b1", "bytes_per_launch": 47269468},
     ("decode_proj", "llama2-7b-bf16"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 102930895},
