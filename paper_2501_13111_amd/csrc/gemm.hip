@@ -573,6 +573,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
     auto compute = [&](int stage, int nk0) {
         const char* sA = smem + stage * T::STAGE;
         const char* sB = sA + T::A_BYTES;
+        u32x2 wd2[2];                                        // int4: the 32-k step's two words
 #pragma unroll
         for (int kk = 0; kk < T::TK / 16; ++kk) {            // 16-k MFMA steps
             if (nk0 >= 0 && kk < T::TK / 32) {
@@ -581,7 +582,10 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             }
             const int s = kk >> 1, hh = kk & 1;              // 32-k sub-step, half
             u32x4 af[4], bop[2];
-            const int chunk = 2 * kk + h32;                  // 16-byte chunk of the A row
+            // 16-byte chunk of the A row: k 8 c .. 8 c + 7 for chunk c.  int4 lanes take the
+            // k of the weight word they hold (below), so the chunk follows it: the MFMA only needs
+            // both operands to agree on k
+            const int chunk = WF == W_INT4 ? 4 * s + 2 * h32 + hh : 2 * kk + h32;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int row = wm * 128 + 32 * i + l32;
@@ -599,9 +603,13 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                     const u32x2 c0 = i8x4_to_f16x4(c.x), c1 = i8x4_to_f16x4(c.y);
                     bop[j] = u32x4{c0.x, c0.y, c1.x, c1.y};
                 } else {
-                    // one 128-k block: lane r + 16 g holds k 32 g .. 32 g + 31, 8 per dword
-                    // exact q - z
-                    const uint32_t wd = *(const uint32_t*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 4 * (2 * hh + h32));
+                    // one 128-k block: lane r + 16 g holds k 32 g .. 32 g + 31, 8 per dword.  A
+                    // lane half h32 takes words 2 h32 and 2 h32 + 1 of the 32-k step (k 32 s +
+                    // 16 h32 + 8 hh ..), both in one 8-byte read at the step's first half: one LDS
+                    // read where two 4-byte reads at a 16-byte lane stride met bank conflicts.
+                    // Exact q - z
+                    if (hh == 0) wd2[j] = *(const u32x2*)(sB + rb * 1024 + (rr + 16 * s) * 16 + 8 * h32);
+                    const uint32_t wd = hh ? wd2[j].y : wd2[j].x;
                     bop[j] = i4x8_to_f16x8_q(wd, qbias[j], qbias64[j]);
                     if constexpr (!EXQ) {
                         const u32x4 d = bop[j];
