@@ -106,21 +106,24 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);     // wave index (uniform)
     const int l32 = lane & 31, h32 = lane >> 5;
     // workgroup -> (sequence, kv head, head group, query tile); a unit is a head group times
-    // a query tile of one (sequence, kv head).  While the caches of all sequences fit in
-    // half the 256 MB last-level cache, units go heaviest first over the whole grid (the
-    // latest query tiles of every kv head, then the next ones, ...), which balances the CUs
-    // best.  Larger caches would be streamed from HBM once per query tile; then the units
-    // of one kv head, heaviest first, are consecutive workgroups of one XCD (workgroup i
-    // runs on XCD i % 8) and stream the same blocks at about the same time through its L2.
+    // a query tile of one (sequence, kv head).  Workgroup i runs on XCD i % 8: each XCD takes
+    // its own kv heads, W at a time (W = 8, 4, 2 or 1, whichever divides its share), and
+    // runs the W heads' units heaviest first across the W (the latest query tiles of all W,
+    // then the next ones, ...).  The units of a kv head then stream the same blocks at about
+    // the same time through that XCD's L2, and the W heads keep its CUs balanced.  Grids
+    // whose kv heads do not split evenly over the XCDs go heaviest first over the whole grid.
     const int hgs = a.nh / a.nkv / HPW;                // head groups per kv head
     const int nqt = (a.P + 32 * QW - 1) / (32 * QW);
     const int units = hgs * nqt;
     const int ngroups = (int)gridDim.x / units;       // sequences x kv heads
     const int L = blockIdx.x;
     int g, u;
-    if (ngroups % 8 == 0 && (int64_t)ngroups * a.P * D * (KV8 ? 2 : 4) > (128ll << 20)) {
-        g = (L >> 3) / units * 8 + (L & 7);
-        u = (L >> 3) % units;
+    if (ngroups % 8 == 0) {
+        const int per = ngroups / 8;
+        const int W = per % 8 == 0 ? 8 : per % 4 == 0 ? 4 : per % 2 == 0 ? 2 : 1;
+        const int k = L >> 3, nwin = W * units, idx = k % nwin;
+        g = ((k / nwin) * W + idx % W) * 8 + (L & 7);
+        u = idx / W;
     } else {
         const int hgi = L % hgs;
         g = (L / hgs) % ngroups;
