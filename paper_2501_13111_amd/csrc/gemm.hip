@@ -574,6 +574,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
         const char* sA = smem + stage * T::STAGE;
         const char* sB = sA + T::A_BYTES;
         u32x2 wd2[2];                                        // int4: the 32-k step's two words
+        u32x4 wd4[2];                                        // int8: the 32-k step's 16 codes
 #pragma unroll
         for (int kk = 0; kk < T::TK / 16; ++kk) {            // 16-k MFMA steps
             if (nk0 >= 0 && kk < T::TK / 32) {
@@ -585,7 +586,7 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
             // 16-byte chunk of the A row: k 8 c .. 8 c + 7 for chunk c.  int4 lanes take the
             // k of the weight word they hold (below), so the chunk follows it: the MFMA only needs
             // both operands to agree on k
-            const int chunk = WF == W_INT4 ? 4 * s + 2 * h32 + hh : 2 * kk + h32;
+            const int chunk = WF != W_BF16 ? 4 * s + 2 * h32 + hh : 2 * kk + h32;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int row = wm * 128 + 32 * i + l32;
@@ -598,8 +599,11 @@ __global__ void __launch_bounds__(512, 1) gemm_big_kernel(GemmArgs a) {
                     // block (rb, s): lane r + 16 g holds k 8 g .. 8 g + 7 of the 32-k step
                     bop[j] = *(const u32x4*)(sB + (rb * 2 + s) * 1024 + (rr + 16 * (2 * hh + h32)) * 16);
                 } else if constexpr (WF == W_INT8) {
-                    // one 64-k block: lane r + 16 g holds k 16 g .. 16 g + 15
-                    const u32x2 c = *(const u32x2*)(sB + rb * 1024 + (rr + 16 * (2 * s + hh)) * 16 + 8 * h32);
+                    // one 64-k block: lane r + 16 g holds k 16 g .. 16 g + 15.  A lane half h32
+                    // takes piece g = 2 s + h32 whole at the step's first half (k 32 s + 16 h32
+                    // + 8 hh ..): one 16-byte read per 32-k step
+                    if (hh == 0) wd4[j] = *(const u32x4*)(sB + rb * 1024 + (rr + 16 * (2 * s + h32)) * 16);
+                    const u32x2 c = hh ? u32x2{wd4[j].z, wd4[j].w} : u32x2{wd4[j].x, wd4[j].y};
                     const u32x2 c0 = i8x4_to_f16x4(c.x), c1 = i8x4_to_f16x4(c.y);
                     bop[j] = u32x4{c0.x, c0.y, c1.x, c1.y};
                 } else {
