@@ -38,6 +38,27 @@
 
 namespace fpk {
 
+// Split-K sums of NS columns (p[c][s * stride] over s < ks, in split order, as sum_parts
+// adds them), with the loads of eight splits of every column in flight together: one
+// memory round trip per eight splits instead of one per column.  Columns with p[c] null
+// give 0 and load nothing.
+template <int NS>
+__device__ __forceinline__ void sum_parts_cols(const float* const (&p)[NS], int ks, int64_t stride, float (&out)[NS]) {
+#pragma unroll
+    for (int c = 0; c < NS; ++c) out[c] = 0.f;
+    for (int s = 0; s < ks; s += 8) {
+        float v[NS][8];
+#pragma unroll
+        for (int c = 0; c < NS; ++c)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[c][i] = (p[c] != nullptr && s + i < ks) ? p[c][(s + i) * stride] : 0.f;
+#pragma unroll
+        for (int c = 0; c < NS; ++c)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) out[c] += v[c][i];
+    }
+}
+
 // ---------------------------------------------------------------------------------
 // The new token's k and v for kv head kvh of sequence b, done by one wave (lane j
 // handles the rotation pair (j, j + D/2)): reduce the qkv projection's split-K
@@ -52,12 +73,14 @@ __device__ __forceinline__ void append_kv(const AttnDecArgs& a, int b, int kvh, 
     float k0 = 0.f, k1 = 0.f, v0 = 0.f, v1 = 0.f;
     if (j < D / 2) {
         const float c = a.cos_t[(int64_t)pos * (D / 2) + j], sn = a.sin_t[(int64_t)pos * (D / 2) + j];
-        const float u = sum_parts(prow + kcol + j, a.ks, pstride);
-        const float x = sum_parts(prow + kcol + j + D / 2, a.ks, pstride);
+        const float* const cols[4] = {prow + kcol + j, prow + kcol + j + D / 2, prow + vcol + j, prow + vcol + j + D / 2};
+        float sum[4];
+        sum_parts_cols<4>(cols, a.ks, pstride, sum);
+        const float u = sum[0], x = sum[1];
         k0 = __fsub_rn(__fmul_rn(u, c), __fmul_rn(x, sn));
         k1 = __fadd_rn(__fmul_rn(x, c), __fmul_rn(u, sn));
-        v0 = sum_parts(prow + vcol + j, a.ks, pstride);
-        v1 = sum_parts(prow + vcol + j + D / 2, a.ks, pstride);
+        v0 = sum[2];
+        v1 = sum[3];
         if (a.dump) {   // [2, B, nkv, D] pre-quantisation K, V
             float* dk = a.dump + ((int64_t)b * a.nkv + kvh) * D;
             float* dv = a.dump + ((int64_t)a.batch * a.nkv + (int64_t)b * a.nkv + kvh) * D;
@@ -183,13 +206,39 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
         const int Nqkv = (a.nh + 2 * a.nkv) * D;
         const int64_t pstride = (int64_t)a.batch * Nqkv;
         const float* prow = a.qkv_part + (int64_t)b * Nqkv + (int64_t)kvh * G * D;
-        for (int i = (tid + 192) & 255; i < G * (D / 2); i += 256) {
+        // the thread's rotation pairs i = i0 + 256 n, all summed together: up to NI for a
+        // group of several heads, one (both halves together) when the group's pairs fit
+        // the 256 threads
+        const int i0 = (tid + 192) & 255;
+        auto rotate = [&](int i, float u, float v) {
             const int c = i / (D / 2), j = i % (D / 2);
             const float cs = a.cos_t[(int64_t)pos * (D / 2) + j], sn = a.sin_t[(int64_t)pos * (D / 2) + j];
-            const float u = sum_parts(prow + c * D + j, a.ks, pstride);
-            const float v = sum_parts(prow + c * D + j + D / 2, a.ks, pstride);
             qs[c * D + j] = act_store(__fsub_rn(__fmul_rn(u, cs), __fmul_rn(v, sn)), AF);
             qs[c * D + j + D / 2] = act_store(__fadd_rn(__fmul_rn(v, cs), __fmul_rn(u, sn)), AF);
+        };
+        auto col = [&](int i, int half) { return prow + (i / (D / 2)) * D + i % (D / 2) + half * (D / 2); };
+        if (G * (D / 2) <= 256) {
+            if (i0 < G * (D / 2)) {
+                const float* const cols[2] = {col(i0, 0), col(i0, 1)};
+                float sum[2];
+                sum_parts_cols<2>(cols, a.ks, pstride, sum);
+                rotate(i0, sum[0], sum[1]);
+            }
+        } else {
+            constexpr int NI = (16 * (D / 2) + 255) / 256;
+            const float* cols[2 * NI];
+#pragma unroll
+            for (int n = 0; n < NI; ++n) {
+                const int i = i0 + 256 * n;
+                const bool live = i < G * (D / 2);
+                cols[2 * n] = live ? col(i, 0) : nullptr;
+                cols[2 * n + 1] = live ? col(i, 1) : nullptr;
+            }
+            float sum[2 * NI];
+            sum_parts_cols<2 * NI>(cols, a.ks, pstride, sum);
+#pragma unroll
+            for (int n = 0; n < NI; ++n)
+                if (i0 + 256 * n < G * (D / 2)) rotate(i0 + 256 * n, sum[2 * n], sum[2 * n + 1]);
         }
     }
     __syncthreads();
