@@ -182,6 +182,27 @@ __device__ __forceinline__ float sum_parts(const float* __restrict__ p, int ks, 
     return acc;
 }
 
+// Split-K sums of NS columns (p[c][s * stride] over s < ks, in split order, as sum_parts
+// adds them), with the loads of eight splits of every column in flight together: one
+// memory round trip per eight splits instead of one per column.  Columns with p[c] null
+// give 0 and load nothing.
+template <int NS>
+__device__ __forceinline__ void sum_parts_cols(const float* const (&p)[NS], int ks, int64_t stride, float (&out)[NS]) {
+#pragma unroll
+    for (int c = 0; c < NS; ++c) out[c] = 0.f;
+    for (int s = 0; s < ks; s += 8) {
+        float v[NS][8];
+#pragma unroll
+        for (int c = 0; c < NS; ++c)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[c][i] = (p[c] != nullptr && s + i < ks) ? p[c][(s + i) * stride] : 0.f;
+#pragma unroll
+        for (int c = 0; c < NS; ++c)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) out[c] += v[c][i];
+    }
+}
+
 // Raw buffer resource over [base, base + bytes), bytes < 2^32.  A load at or past the
 // end returns zeros without a memory access, so a pipelined loop can issue the same
 // loads on every trip (exact wait counts) and pay nothing for the trips past its range.

@@ -134,23 +134,35 @@ __global__ void __launch_bounds__(RN_T) resid_norm_row_kernel(const float* __res
     for (int j = 0; j < 2; ++j) {
         const int n0 = (threadIdx.x + RN_T * j) * 8;
         if (n0 >= N) continue;
+        // the residual piece goes out with the partials' loads below and is unpacked after them
         const u32x4 rv = *(const u32x4*)(resid + m * N + n0);
-        const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+        float acc[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            v[j][2 * e] = __uint_as_float(rw[e] << 16);
-            v[j][2 * e + 1] = __uint_as_float(rw[e] & 0xFFFF0000u);
+        for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+        // eight splits' loads in flight together, added in split order
+        for (int s0 = 0; s0 < ks; s0 += 8) {
+            float4 a0[8], a1[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {                           // past the last split: + 0
+                const float* p = part + (s0 + i) * pstride + m * N + n0;
+                a0[i] = s0 + i < ks ? *(const float4*)p : float4{0.f, 0.f, 0.f, 0.f};
+                a1[i] = s0 + i < ks ? *(const float4*)(p + 4) : float4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                acc[0] += a0[i].x; acc[1] += a0[i].y; acc[2] += a0[i].z; acc[3] += a0[i].w;
+                acc[4] += a1[i].x; acc[5] += a1[i].y; acc[6] += a1[i].z; acc[7] += a1[i].w;
+            }
+        }
+        {
+            const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[j][2 * e] = __uint_as_float(rw[e] << 16);
+                v[j][2 * e + 1] = __uint_as_float(rw[e] & 0xFFFF0000u);
+            }
         }
         if (ks > 0) {
-            float acc[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-            for (int s = 0; s < ks; ++s) {
-                const float* p = part + s * pstride + m * N + n0;
-                const float4 a0 = *(const float4*)p, a1 = *(const float4*)(p + 4);
-                acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
-                acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
-            }
             uint32_t o[4];
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[j][e] = bfround(v[j][e] + acc[e]);
@@ -190,9 +202,10 @@ __global__ void __launch_bounds__(256) swiglu_kernel(const float* __restrict__ p
     const int64_t m = blockIdx.y;
     const int f = blockIdx.x * blockDim.x + threadIdx.x;
     if (f >= F) return;
-    const float gs = sum_parts(part + m * (2 * (int64_t)F) + f, ks, (int64_t)M * 2 * F);
-    const float us = sum_parts(part + m * (2 * (int64_t)F) + F + f, ks, (int64_t)M * 2 * F);
-    a[m * (int64_t)F + f] = act_store(bfround(silu_f(gs) * us), afmt);
+    const float* const cols[2] = {part + m * (2 * (int64_t)F) + f, part + m * (2 * (int64_t)F) + F + f};
+    float sum[2];
+    sum_parts_cols<2>(cols, ks, (int64_t)M * 2 * F, sum);
+    a[m * (int64_t)F + f] = act_store(bfround(silu_f(sum[0]) * sum[1]), afmt);
 }
 
 // ---------------------------------------------------------------- rotary + KV append (prefill)
