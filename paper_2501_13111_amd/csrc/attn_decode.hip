@@ -359,7 +359,8 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
 }
 
 // One workgroup of D threads per (head, sequence): log-sum-exp merge of the
-// workgroup partials, four of them in flight at a time.
+// workgroup partials.  Up to eight partials: their m, l and o values load together (one
+// memory round trip); more go eight at a time, maxima first.  Sums in partial order.
 template <int D>
 __global__ void __launch_bounds__(D) attn_merge_kernel(AttnDecArgs a, int nsw) {
     const int h = blockIdx.x, b = blockIdx.y, i = threadIdx.x;
@@ -367,13 +368,50 @@ __global__ void __launch_bounds__(D) attn_merge_kernel(AttnDecArgs a, int nsw) {
     const int kpw = 4 * a.keys_per_split;
     const int nv = (len + kpw - 1) / kpw;
     const float* src = a.ws + ((int64_t)b * a.nh + h) * nsw * (D + 4);
-    float m = -INFINITY;
-    for (int c = 0; c < nv; ++c) m = fmaxf(m, src[c * (D + 4) + D]);
-    float l = 0.f, o = 0.f;
-    for (int c = 0; c < nv; ++c) {
-        const float e = __expf(src[c * (D + 4) + D] - m);
-        l += src[c * (D + 4) + D + 1] * e;
-        o += src[c * (D + 4) + i] * e;
+    float m = -INFINITY, l = 0.f, o = 0.f;
+    if (nv <= 8) {
+        float mc[8], lc[8], oc[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const float* q = src + c * (D + 4);
+            mc[c] = c < nv ? q[D] : -INFINITY;
+            lc[c] = c < nv ? q[D + 1] : 0.f;
+            oc[c] = c < nv ? q[i] : 0.f;
+        }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) m = fmaxf(m, mc[c]);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            if (c >= nv) break;
+            const float e = __expf(mc[c] - m);
+            l += lc[c] * e;
+            o += oc[c] * e;
+        }
+    } else {
+        for (int c0 = 0; c0 < nv; c0 += 8) {
+            float mc[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) mc[c] = c0 + c < nv ? src[(c0 + c) * (D + 4) + D] : -INFINITY;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) m = fmaxf(m, mc[c]);
+        }
+        for (int c0 = 0; c0 < nv; c0 += 8) {
+            float mc[8], lc[8], oc[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const float* q = src + (c0 + c) * (D + 4);
+                mc[c] = c0 + c < nv ? q[D] : 0.f;
+                lc[c] = c0 + c < nv ? q[D + 1] : 0.f;
+                oc[c] = c0 + c < nv ? q[i] : 0.f;
+            }
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                if (c0 + c >= nv) break;
+                const float e = __expf(mc[c] - m);
+                l += lc[c] * e;
+                o += oc[c] * e;
+            }
+        }
     }
     a.out[((int64_t)b * a.nh + h) * D + i] = act_store(bfround(o / l), a.out_fmt);
 }
