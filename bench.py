@@ -45,11 +45,11 @@ PROJ = {"qkv", "o", "gate_up", "down"}
 # were taken on (hash of the kernel's source files and of its argument block in
 # fp_internal.h); the summaries and commands are in profiles/.
 TRAFFIC = {
-    ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "70438e6072d899b9", "bytes_per_launch": 8597008210},
-    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "08d150b3fca9ae0d", "bytes_per_launch": 2808682845},
-    ("decode_proj", "llama2-70b-tp8-int4"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 27162882},
-    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "2af41be9a5c124b1", "bytes_per_launch": 47269468},
-    ("decode_proj", "llama2-7b-bf16"): {"src": "335fb5a5ef8f0aa3", "bytes_per_launch": 102930895},
+    ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "ef13af709f851df1", "bytes_per_launch": 8605742090},
+    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "9ecec6a9736da84c", "bytes_per_launch": 1625351408},
+    ("decode_proj", "llama2-70b-tp8-int4"): {"src": "7bbc74de5f69e243", "bytes_per_launch": 27162882},
+    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "5a76dc285b8f9afc", "bytes_per_launch": 47379323},
+    ("decode_proj", "llama2-7b-bf16"): {"src": "7bbc74de5f69e243", "bytes_per_launch": 102930905},
 }
 FAMILY_SRC = {
     "decode_proj": (("skinny.hip", "fp_device.h"), r"enum XForm \{.*?\n\};\n.*?struct SkinnyArgs \{.*?\n\};"),
