@@ -362,7 +362,7 @@ def run_workload(name, args, torch, timed_out=None):
                                measured_traffic("prefill_gemm", name))
     pa_ms = [ms for kind, _, ms in pre_prof if kind == "attn"]
     pa_fl = 4 * s.head_dim * s.n_heads * B * Pp * (Pp + 1) // 2
-    roof_pattn = roofline_entry("attn_prefill_kernel", "mfma", pa_fl * len(pa_ms) / (sum(pa_ms) / 1e3) / 1e12,
+    roof_pattn = roofline_entry("attn_prefill_kernel (attn_prefill_ks_kernel on grids smaller than the CU count)", "mfma", pa_fl * len(pa_ms) / (sum(pa_ms) / 1e3) / 1e12,
                                 MFMA16_PEAK_TFLOPS, "TFLOP/s", statistics.fmean(pa_ms), pa_fl,
                                 measured_traffic("prefill_attn", name))
     # the dominant kernel family: the most time in one pass (prefill once, S decode steps)

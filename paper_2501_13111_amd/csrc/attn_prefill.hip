@@ -397,6 +397,176 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
         }
 }
 
+// Short prompts with bf16 caches (a grid of fewer workgroups than CUs in the layout
+// above: one sequence, few heads): the layout above leaves most SIMDs empty and the
+// latest query tile walks every key block alone.  Here a workgroup takes one 32-query
+// block of one head and its four waves split the key blocks (wave w takes blocks w, w + 4,
+// ...), so the chain of dependent blocks is a quarter as long and the grid four times
+// larger.  Each wave loads its blocks' MFMA fragments straight into registers (block s + 4
+// is in flight while block s is multiplied) and keeps an online softmax: a running
+// maximum m per query, the accumulators and the sum rescaled by exp2(m_old - m_new) when
+// m grows.  The four partial (m, l, O) then merge through LDS: M = max m_w, O = sum
+// O_w exp2(m_w - M), l likewise, and the output is O / l rounded to bf16 (Section 3.2's
+// attention, exactly as above up to rounding order).
+template <int D>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) attn_prefill_ks_kernel(AttnPreArgs a) {
+    constexpr int NKC = D / 16;                 // K fragment chunks per block
+    constexpr int NVC = 2 * (D / 32);           // V fragment chunks per block
+    constexpr int RS = D + 4;                   // LDS row stride of a partial (floats)
+    __shared__ __attribute__((aligned(16))) float po[4][32 * RS];
+    __shared__ float pm[4][32], pl[4][32];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l32 = lane & 31, h32 = lane >> 5;
+    // workgroup -> (query block, sequence, head): the latest query blocks first
+    const int nqb = (a.P + 31) / 32;
+    const int nbh = (int)gridDim.x / nqb;       // sequences x heads
+    const int L = blockIdx.x;
+    const int qb = nqb - 1 - L / nbh;
+    const int b = (L % nbh) / a.nh, h = (L % nbh) % a.nh;
+    const int kvh = h / (a.nh / a.nkv);
+    const int q0 = 32 * qb;
+    const int nb = min(a.P - 1, q0 + 31) / PK + 1;     // key blocks of the query block
+    const int nmine = nb > w ? (nb - w + 3) / 4 : 0;   // this wave's blocks: w + 4 i
+    const float sl2 = a.scale * 1.4426950408889634f;
+
+    const uint16_t* kbase = (const uint16_t*)a.kc + ((int64_t)b * a.nkv + kvh) * a.kv_stride * D;
+    const uint16_t* vbase = (const uint16_t*)a.vc + ((int64_t)b * a.nkv + kvh) * a.nblk * D * VT_BLK;
+    // fragment pieces of lane l: K key l % 32, dims 16 j + 8 (l / 32) .. + 7; V dims
+    // 32 dt + l % 32, keys 16 j2 + 8 (l / 32) .. + 7 (chunk j2 (D / 32) + dt)
+    const int koffl = l32 * D + 8 * h32;
+    const int voffl = l32 * VT_BLK + 8 * h32;
+    struct Blk {
+        u32x4 k[NKC], v[NVC];
+    };
+    // loads of the wave's i-th block (past its last: the last again, from L2; nothing is
+    // loaded by a wave without blocks)
+    auto load = [&](int i, Blk& x) {
+        const int s = w + 4 * min(i, nmine - 1);
+        const uint16_t* kp = kbase + (int64_t)s * PK * D + koffl;
+        const uint16_t* vp = vbase + (int64_t)s * D * VT_BLK + voffl;
+#pragma unroll
+        for (int j = 0; j < NKC; ++j) x.k[j] = *(const u32x4*)(kp + 16 * j);
+#pragma unroll
+        for (int t = 0; t < NVC; ++t) x.v[t] = *(const u32x4*)(vp + (t % (D / 32)) * 32 * VT_BLK + 16 * (t / (D / 32)));
+    };
+
+    // Q^T fragments: lane l supplies query l % 32, dims 16 j + 8 (l / 32) .. + 7; lanes
+    // past the prompt keep zeros
+    u32x4 qf[NKC];
+    const int qpos = q0 + l32;
+    {
+        const bool qv = qpos < a.P;
+        const uint16_t* qrow = a.q + (((int64_t)b * a.nh + h) * a.P + (qv ? qpos : 0)) * D;
+#pragma unroll
+        for (int j = 0; j < NKC; ++j) {
+            const u32x4 x = *(const u32x4*)(qrow + 16 * j + 8 * h32);
+            qf[j] = qv ? x : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+
+    // element e of a lane's scores holds key 8 (e / 4) + e % 4 + 4 h32 of the block; it is
+    // live when that key passes neither the query nor the prompt
+    auto koff = [](int e) { return 8 * (e >> 2) + (e & 3); };
+    f32x16 oacc[D / 32];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = f32x16{};
+    float m_run = -INFINITY, l_run = 0.f;
+    auto block = [&](int i, const Blk& x) {
+        const int s = w + 4 * i;
+        f32x16 acc = f32x16{};
+#pragma unroll
+        for (int j = 0; j < NKC; ++j) acc = mfma32<ACT_BF16>(x.k[j], qf[j], acc);
+        const int lim = min(qpos, a.P - 1) - s * PK - 4 * h32;
+        float t = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            acc[e] = koff(e) <= lim ? acc[e] * sl2 : -INFINITY;
+            t = fmaxf(t, acc[e]);
+        }
+        const float m_new = fmaxf(m_run, fmaxf(t, __shfl_xor(t, 32, 64)));
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);     // 0 on the first block
+        m_run = m_new;
+        u32x4 pf[2];
+        float psum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+            const float x0 = __builtin_amdgcn_exp2f(acc[e] - m_new), x1 = __builtin_amdgcn_exp2f(acc[e + 1] - m_new);
+            psum += x0 + x1;
+            pf[(e >> 2) & 1][((e & 3) >> 1) + 2 * (e >> 3)] = pack_bf16_hw(x0, x1);
+        }
+        l_run = l_run * alpha + psum;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) {
+            oacc[dt] *= alpha;
+#pragma unroll
+            for (int j2 = 0; j2 < 2; ++j2) oacc[dt] = mfma32<ACT_BF16>(x.v[j2 * (D / 32) + dt], pf[j2], oacc[dt]);
+        }
+    };
+    if (nmine > 0) {
+        Blk xa, xb;
+        load(0, xa);
+        load(1, xb);
+        int i = 0;
+        for (; i + 2 <= nmine; i += 2) {
+            block(i, xa);
+            load(i + 2, xa);
+            block(i + 1, xb);
+            load(i + 3, xb);
+        }
+        if (i < nmine) block(i, xa);
+    }
+
+    // merge the four waves' partials
+    const float lt = l_run + __shfl_xor(l_run, 32, 64);
+    if (h32 == 0) {
+        pm[w][l32] = m_run;
+        pl[w][l32] = lt;
+    }
+    __syncthreads();
+    float mm = pm[0][l32];
+#pragma unroll
+    for (int v = 1; v < 4; ++v) mm = fmaxf(mm, pm[v][l32]);
+    const float f = nmine > 0 ? __builtin_amdgcn_exp2f(m_run - mm) : 0.f;
+    // O^T element (dt, e) of lane l: dim 32 dt + 8 (e / 4) + 4 h32 + e % 4, query l % 32
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4)
+            *(f32x4*)&po[w][l32 * RS + 32 * dt + 8 * e4 + 4 * h32] =
+                f32x4{oacc[dt][4 * e4] * f, oacc[dt][4 * e4 + 1] * f, oacc[dt][4 * e4 + 2] * f, oacc[dt][4 * e4 + 3] * f};
+    __syncthreads();
+    // thread t writes query t / 8, dims D / 8 (t % 8) .. + D / 8 - 1
+    constexpr int DPT = D / 8;
+    const int oq = tid >> 3, d0 = DPT * (tid & 7);
+    if (q0 + oq >= a.P) return;
+    float mq = pm[0][oq];
+#pragma unroll
+    for (int v = 1; v < 4; ++v) mq = fmaxf(mq, pm[v][oq]);
+    float lsum = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) lsum += v < nb ? pl[v][oq] * __builtin_amdgcn_exp2f(pm[v][oq] - mq) : 0.f;
+    const float inv = 1.f / lsum;
+    uint16_t* orow = a.out + ((int64_t)b * a.P + q0 + oq) * a.nh * D + h * D + d0;
+#pragma unroll
+    for (int c = 0; c < DPT; c += 8) {
+        uint32_t wd[4];
+#pragma unroll
+        for (int i2 = 0; i2 < 8; i2 += 2) {
+            float o0 = 0.f, o1 = 0.f;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                o0 += po[v][oq * RS + d0 + c + i2];
+                o1 += po[v][oq * RS + d0 + c + i2 + 1];
+            }
+            wd[i2 / 2] = (uint32_t)act_store(bfround(o0 * inv), a.out_fmt) |
+                         ((uint32_t)act_store(bfround(o1 * inv), a.out_fmt) << 16);
+        }
+        *(u32x4*)(orow + c) = u32x4{wd[0], wd[1], wd[2], wd[3]};
+    }
+}
+
 // int8 caches: dequantise block blk of the prompt of (sequence, kv head) g into the
 // fragment-major layout attn_prefill_kernel copies: K chunk c, lane l = key l % 32, dims
 // 16 c + 8 (l / 32) .. + 7 as fp16 code * s_k / kappa_b; V chunk NKC + t (t = j2 (D / 32) +
@@ -497,16 +667,19 @@ static hipError_t launch_ap(const AttnPreArgs& a, int B, hipStream_t st) {
         const int hp = hmax < n ? hmax : n, wq = 32 * (n / hp);
         return (int64_t)((a.P + wq - 1) / wq) * (a.nh / hp) * B;
     };
-    int nw = 4;
-    if constexpr (!KV8)
-        while (nw > 1 && grid(nw) < 128) nw /= 2;
+    if constexpr (!KV8) {
+        // fewer workgroups than CUs: split each query block's keys over four waves
+        if (grid(4) < 256) {
+            const int64_t n = (int64_t)((a.P + 31) / 32) * a.nh * B;
+            if (n > INT_MAX) return hipErrorInvalidValue;
+            FP_LAUNCH(attn_prefill_ks_kernel<D>, dim3((unsigned)n), dim3(256), 0, st, a);
+            return hipGetLastError();
+        }
+    }
+    const int nw = 4;
     const int hpw = hmax < nw ? hmax : nw;
     if ((int64_t)(a.nh / hpw) * B * ((a.P + 31) / 32) > INT_MAX) return hipErrorInvalidValue;
-    if (nw == 4) launch_nw<D, KV8, 4>(a, B, hpw, st);
-    else if constexpr (!KV8) {
-        if (nw == 2) launch_nw<D, KV8, 2>(a, B, hpw, st);
-        else launch_nw<D, KV8, 1>(a, B, hpw, st);
-    }
+    launch_nw<D, KV8, 4>(a, B, hpw, st);
     return hipGetLastError();
 }
 
