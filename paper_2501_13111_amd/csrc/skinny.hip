@@ -409,14 +409,6 @@ __global__ void __launch_bounds__(256) skinny_kernel(SkinnyArgs a) {
 // writes, so the global loads in flight are not drained at every chunk.  The
 // split-K factor only has to fill the GPU.
 constexpr int SB_KC = 128;              // k per activation chunk (one int4 group)
-// XOR key of an activation row's 16-byte pieces: the row's low four bits with bits 2 and
-// 3 swapped.  The plain key (row % 16) gave the 16x16 int4 fragments (lanes l and l + 16
-// read pieces four apart) about four conflict cycles per LDS read, and the other forms
-// none: what a 16-byte read served eight lanes at a time (lanes 0-3 with 20-23, 4-7 with
-// 16-19, 8-11 with 28-31, 12-15 with 24-27, and the same in the upper half) predicts.
-// Under that grouping, and under plain 16-lane groups, this key puts every group on
-// distinct slots for all fragment forms here.
-__device__ __forceinline__ int sb_swz(int rr) { return (rr & 3) | ((rr >> 1) & 4) | ((rr << 1) & 8); }
 #ifndef SKINNY_I4_POST
 #define SKINNY_I4_POST 1                // int4: scale the group sums instead of the weights
 #endif
@@ -476,7 +468,7 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
     const int myrow = row[bsel & (NS - 1)];
     const bool myrv = rv[bsel & (NS - 1)];
     // activation chunk ci: thread piece c = tid + NT i is row c / 16, LDS slot c % 16,
-    // which holds the row's 16-byte piece slot ^ sb_swz(row)
+    // which holds the row's 16-byte piece slot ^ (row % 16)
     // Loads are unconditional (clamped addresses): rows past M only feed output rows
     // that are never stored.  Pieces past the k-range (only in a ragged last chunk; the
     // weights there are padding or clamped copies) are zeroed when the chunk is written
@@ -487,7 +479,7 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
         for (int i = 0; i < NPA; ++i) {
             const int c = tid + NT * i;
             const int rr = min(c >> 4, 16 * MT - 1), slot = c & 15;
-            const int k = kbase + ((slot ^ sb_swz(rr)) * 8);
+            const int k = kbase + ((slot ^ (rr & 15)) * 8);
             ra[i] = *(const u32x4*)(a.X + (int64_t)min(rr, a.M - 1) * a.K + min(k, a.K - 8));
         }
     };
@@ -500,7 +492,7 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
             u32x4 v = ra[i];
             if (ragged) {
                 const int rr = min(c >> 4, 16 * MT - 1), slot = c & 15;
-                if (kbase + ((slot ^ sb_swz(rr)) * 8) >= ke) v = u32x4{0u, 0u, 0u, 0u};
+                if (kbase + ((slot ^ (rr & 15)) * 8) >= ke) v = u32x4{0u, 0u, 0u, 0u};
             }
             if ((256 * MT) % NT == 0 || c < 256 * MT) *(u32x4*)(buf + c * 16) = v;
         }
@@ -555,7 +547,7 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
         else koff = 32 * g + 8 * m;
         const int piece = koff >> 3;
         const int rr = 16 * t + r;
-        return *(const u32x4*)(Ab + rr * 256 + ((piece ^ sb_swz(rr)) << 4));
+        return *(const u32x4*)(Ab + rr * 256 + ((piece ^ (rr & 15)) << 4));
     };
     auto b_op = [&](const u32x4 (*wv)[NS], const uint32_t* sz, int m, int s) {
         if constexpr (WF == W_BF16) {
@@ -642,7 +634,7 @@ __global__ void __launch_bounds__(64 * NWV, 1) skinny_batch_kernel(SkinnyArgs a)
         else koff = 64 * (j >> 2) + 32 * h32 + 8 * (j & 3);
         const int piece = koff >> 3;
         const int rr = 32 * t + (lane & 31);
-        return *(const u32x4*)(Ab + rr * 256 + ((piece ^ sb_swz(rr)) << 4));
+        return *(const u32x4*)(Ab + rr * 256 + ((piece ^ (rr & 15)) << 4));
     };
     auto b_op32 = [&](const u32x4 (*wv)[NS], const uint32_t* sz, int j) {
         if constexpr (WF == W_BF16) {
