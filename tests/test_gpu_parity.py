@@ -123,6 +123,11 @@ CASES = [
     ("sp24-single-gqa3", Shape(2, 576, 9, 3, 64, 704, 1, 70, 76), "sp24", "bf16", 1, 70, 4),
     ("sp24-batch3", Shape(1, 1024, 8, 8, 128, 2048, 3, 130, 134), "sp24", "bf16", 3, 130, 3),
     ("sp24-batch40-int8kv", Shape(2, 512, 4, 4, 128, 1024, 40, 50, 54), "sp24", "int8", 40, 50, 3),
+    # short prompts on a bf16 cache (the key-split prefill attention): a one-token prompt
+    # (three of the four waves without a block), and GQA 4:1 at head_dim 64 over a ragged
+    # 45-token prompt (two blocks)
+    ("prompt1-bf16", Shape(1, 256, 2, 2, 128, 384, 2, 1, 4), "bf16", "bf16", 2, 1, 3),
+    ("gqa4-d64-bf16-short", Shape(1, 512, 8, 2, 64, 768, 3, 45, 48), "int8", "bf16", 3, 45, 3),
 ]
 
 
@@ -401,17 +406,30 @@ def test_parity_large_prefill_tiles(case):
     assert max(res.decode_errs) <= TOL
 
 
-REPEAT_CASES = [c for c in CASES if c[0] in ("mha-bf16", "gqa8-d128-int4-int8", "long-ctx-bf16", "sp24-batch3")]
+# Small grids with a bf16 cache take the short-prompt kernel (online softmax, no second
+# pass; the limit does not apply there), so the bf16 repeat path is exercised by a grid of
+# 256 workgroups (big-bf16-partial-stage, sampled rows); the int8 cases take the regular
+# kernel at any size.
+REPEAT_CASES = [c + (None,) for c in CASES if c[0] in ("mha-bf16", "gqa8-d128-int4-int8", "long-ctx-bf16",
+                                                       "sp24-batch3")] + \
+               [c for c in BIG_CASES if c[0] == "big-bf16-partial-stage"]
 
 
 @pytest.mark.parametrize("case", REPEAT_CASES, ids=[c[0] for c in REPEAT_CASES])
 def test_prefill_attention_repeat_path(case, monkeypatch):
     """The prefill attention's second pass (a probability against the first block's
-    maximum passing the limit) forced from the host with a limit of 2: most workgroups
-    repeat their prompt with a larger reference, and the result still meets the bar."""
-    name, shape, wq, kvq, B, P, S = case
+    maximum passing the limit) forced from the host with a limit of 2: most workgroups of
+    the regular kernel repeat their prompt with a larger reference, and the result still
+    meets the bar."""
+    name, shape, wq, kvq, B, P, S, rows = case
     monkeypatch.setenv("FP_ATTN_PROB_LIMIT_LOG2", "1")
-    log(f"case {name} (probability limit 2): {shape} {wq}/{kvq} B={B} P={P} S={S}")
+    log(f"case {name} (probability limit 2): {shape} {wq}/{kvq} B={B} P={P} S={S} rows={rows}")
+    if rows is not None:
+        res = run_parity(shape, wq, kvq, B, P, S, rows=rows)
+        _report(name + "-repeat", res)
+        assert res.prefill_err <= TOL
+        assert max(res.decode_errs) <= TOL
+        return
     res = run_parity(shape, wq, kvq, B, P, S, layerwise=shape.n_layers > 1)
     _report(name + "-repeat", res)
     assert res.prefill_err <= TOL
