@@ -142,6 +142,37 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
     const int len = *a.d_pos + 1;
     const int kps = a.keys_per_split;
     const int wg_beg = 4 * (int)blockIdx.x * kps;
+    // The queries' split-K partial sums are read before anything waits for the position
+    // (their addresses do not depend on it), so the two round trips overlap.  The thread's
+    // rotation pairs are i = i0 + 256 n: up to NIQ for a group of several heads, one (both
+    // halves together) when the group's pairs fit the 256 threads; wave 0 takes the last
+    // ones, so a small group leaves it free to append.
+    constexpr int NIQ = (16 * (D / 2) + 255) / 256;
+    const int i0 = (tid + 192) & 255;
+    const int npairs = G * (D / 2);
+    float qsum[2 * NIQ];
+    {
+        const int Nqkv = (a.nh + 2 * a.nkv) * D;
+        const int64_t pstride = (int64_t)a.batch * Nqkv;
+        const float* prow = a.qkv_part + (int64_t)b * Nqkv + (int64_t)kvh * G * D;
+        auto col = [&](int i, int half) { return prow + (i / (D / 2)) * D + i % (D / 2) + half * (D / 2); };
+        if (npairs <= 256) {
+            if (i0 < npairs) {
+                const float* const cols[2] = {col(i0, 0), col(i0, 1)};
+                sum_parts_cols<2>(cols, a.ks, pstride, *(float(*)[2])qsum);
+            }
+        } else {
+            const float* cols[2 * NIQ];
+#pragma unroll
+            for (int n = 0; n < NIQ; ++n) {
+                const int i = i0 + 256 * n;
+                const bool live = i < npairs;
+                cols[2 * n] = live ? col(i, 0) : nullptr;
+                cols[2 * n + 1] = live ? col(i, 1) : nullptr;
+            }
+            sum_parts_cols<2 * NIQ>(cols, a.ks, pstride, qsum);
+        }
+    }
     if (wg_beg >= len) return;                         // the whole workgroup is past the context
     const int sp = 4 * blockIdx.x + w;
     const int k_beg = sp * kps;
@@ -176,48 +207,23 @@ __global__ void __launch_bounds__(256, 2) attn_decode_kernel(AttnDecArgs a, int 
 
     // The workgroup whose range holds the new position appends its k and v first (one
     // wave; the barrier below publishes the row to the other waves, and no other
-    // workgroup reads that position).  Every workgroup reduces and rotates the queries
-    // of its group into LDS, in the MFMA operand format, starting from wave 1 so that a
-    // small group's queries are staged while wave 0 appends.
+    // workgroup reads that position).  Every workgroup rotates the queries of its group
+    // into LDS, in the MFMA operand format.
     const int pos = len - 1;
     if (pos / (4 * kps) == (int)blockIdx.x && w == 0) append_kv<D, KV8>(a, b, kvh, pos, lane);
     {
-        const int Nqkv = (a.nh + 2 * a.nkv) * D;
-        const int64_t pstride = (int64_t)a.batch * Nqkv;
-        const float* prow = a.qkv_part + (int64_t)b * Nqkv + (int64_t)kvh * G * D;
-        // the thread's rotation pairs i = i0 + 256 n, all summed together: up to NI for a
-        // group of several heads, one (both halves together) when the group's pairs fit
-        // the 256 threads
-        const int i0 = (tid + 192) & 255;
         auto rotate = [&](int i, float u, float v) {
             const int c = i / (D / 2), j = i % (D / 2);
             const float cs = a.cos_t[(int64_t)pos * (D / 2) + j], sn = a.sin_t[(int64_t)pos * (D / 2) + j];
             qs[c * D + j] = act_store(__fsub_rn(__fmul_rn(u, cs), __fmul_rn(v, sn)), AF);
             qs[c * D + j + D / 2] = act_store(__fadd_rn(__fmul_rn(v, cs), __fmul_rn(u, sn)), AF);
         };
-        auto col = [&](int i, int half) { return prow + (i / (D / 2)) * D + i % (D / 2) + half * (D / 2); };
-        if (G * (D / 2) <= 256) {
-            if (i0 < G * (D / 2)) {
-                const float* const cols[2] = {col(i0, 0), col(i0, 1)};
-                float sum[2];
-                sum_parts_cols<2>(cols, a.ks, pstride, sum);
-                rotate(i0, sum[0], sum[1]);
-            }
+        if (npairs <= 256) {
+            if (i0 < npairs) rotate(i0, qsum[0], qsum[1]);
         } else {
-            constexpr int NI = (16 * (D / 2) + 255) / 256;
-            const float* cols[2 * NI];
 #pragma unroll
-            for (int n = 0; n < NI; ++n) {
-                const int i = i0 + 256 * n;
-                const bool live = i < G * (D / 2);
-                cols[2 * n] = live ? col(i, 0) : nullptr;
-                cols[2 * n + 1] = live ? col(i, 1) : nullptr;
-            }
-            float sum[2 * NI];
-            sum_parts_cols<2 * NI>(cols, a.ks, pstride, sum);
-#pragma unroll
-            for (int n = 0; n < NI; ++n)
-                if (i0 + 256 * n < G * (D / 2)) rotate(i0 + 256 * n, sum[2 * n], sum[2 * n + 1]);
+            for (int n = 0; n < NIQ; ++n)
+                if (i0 + 256 * n < npairs) rotate(i0 + 256 * n, qsum[2 * n], qsum[2 * n + 1]);
         }
     }
     __syncthreads();
