@@ -48,7 +48,7 @@ TRAFFIC = {
     ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "ef13af709f851df1", "bytes_per_launch": 8605742090},
     ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "8f6c94ae0e178b13", "bytes_per_launch": 1622333522},
     ("decode_proj", "llama2-70b-tp8-int4"): {"src": "7bbc74de5f69e243", "bytes_per_launch": 27162882},
-    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "5a76dc285b8f9afc", "bytes_per_launch": 47379323},
+    ("decode_attn", "llama2-70b-tp8-int4"): {"src": "3348a08a368fc693", "bytes_per_launch": 47377051},
     ("decode_proj", "llama2-7b-bf16"): {"src": "7bbc74de5f69e243", "bytes_per_launch": 102930905},
 }
 FAMILY_SRC = {
