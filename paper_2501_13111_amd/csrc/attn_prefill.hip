@@ -406,8 +406,8 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)
 // is in flight while block s is multiplied) and keeps an online softmax: a running
 // maximum m per query, the accumulators and the sum rescaled by exp2(m_old - m_new) when
 // m grows.  The four partial (m, l, O) then merge through LDS: M = max m_w, O = sum
-// O_w exp2(m_w - M), l likewise, and the output is O / l rounded to bf16 (Section 3.2's
-// attention, exactly as above up to rounding order).
+// O_w exp2(m_w - M), l likewise, and the output is O / l rounded to bf16: the same causal
+// softmax attention as the kernel above, up to rounding order.
 template <int D>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) attn_prefill_ks_kernel(AttnPreArgs a) {
     constexpr int NKC = D / 16;                 // K fragment chunks per block
