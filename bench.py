@@ -46,7 +46,7 @@ PROJ = {"qkv", "o", "gate_up", "down"}
 # fp_internal.h); the summaries and commands are in profiles/.
 TRAFFIC = {
     ("prefill_gemm", "llama2-70b-tp8-int4"): {"src": "ef13af709f851df1", "bytes_per_launch": 8605742090},
-    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "6a99c02fa7c5da8b", "bytes_per_launch": 1622333522},
+    ("prefill_attn", "llama2-70b-tp8-int4"): {"src": "4c143c5591b38ef6", "bytes_per_launch": 1622333522},
     ("decode_proj", "llama2-70b-tp8-int4"): {"src": "7bbc74de5f69e243", "bytes_per_launch": 27162882},
     ("decode_attn", "llama2-70b-tp8-int4"): {"src": "3348a08a368fc693", "bytes_per_launch": 47377051},
     ("decode_proj", "llama2-7b-bf16"): {"src": "7bbc74de5f69e243", "bytes_per_launch": 102930905},

@@ -419,11 +419,14 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) a
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31, h32 = lane >> 5;
-    // workgroup -> (query block, sequence, head): the latest query blocks first
+    // workgroup -> (query block, sequence, head): the first half of the grid takes the
+    // latest query blocks first, the second half the earliest first, so that the two
+    // workgroups a CU holds at a time (i and i + half the grid) carry about equal work
     const int nqb = (a.P + 31) / 32;
     const int nbh = (int)gridDim.x / nqb;       // sequences x heads
     const int L = blockIdx.x;
-    const int qb = nqb - 1 - L / nbh;
+    const int u = L / nbh, hq = (nqb + 1) / 2;
+    const int qb = u < hq ? nqb - 1 - u : u - hq;
     const int b = (L % nbh) / a.nh, h = (L % nbh) % a.nh;
     const int kvh = h / (a.nh / a.nkv);
     const int q0 = 32 * qb;
